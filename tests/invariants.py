@@ -1,0 +1,82 @@
+"""Schedule invariants, checked independently of both implementations.
+
+A schedule is an (S, 4) uint32 array: link, chunk, t_start, flags.  For a
+copy schedule (no reduce flag) the checks are:
+  1. every postcondition bit is met by the collective time;
+  2. every send leaves a device that holds the chunk at its start time
+     (precondition, or an earlier arrival at or before t_start);
+  3. no link carries two transfers at once (intervals [t, t+T) disjoint);
+  4. every (device, chunk) pair is received at most once and never by a
+     device that held the chunk before;
+  5. the collective time is the latest transfer end.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+
+def bits_of(bm: np.ndarray, row: int):
+    out = []
+    for w, x in enumerate(bm[row]):
+        x = int(x)
+        while x:
+            b = (x & -x).bit_length() - 1
+            x &= x - 1
+            out.append(w * 64 + b)
+    return out
+
+
+def link_times(topo, chunk_bytes):
+    bw = topo.bw_GBps.astype(np.int64)
+    return topo.alpha_ns.astype(np.int64) + (chunk_bytes + bw - 1) // bw
+
+
+def check_copy_schedule(topo, coll, sends: np.ndarray, collective_time: int):
+    """Raises AssertionError on the first violated invariant."""
+    T = link_times(topo, coll.chunk_bytes)
+    src, dst = topo.src.astype(np.int64), topo.dst.astype(np.int64)
+    N = topo.n_npus
+    holders = {}
+    for v in range(N):
+        for c in bits_of(coll.pre, v):
+            holders.setdefault(c, set()).add(v)
+    arrival = {}  # (device, chunk) -> time
+    for c, hs in holders.items():
+        for v in hs:
+            arrival[(v, c)] = 0
+    order = np.lexsort((sends[:, 0], sends[:, 2])) if len(sends) else np.zeros(0, int)
+    busy = {}
+    end_max = 0
+    for i in order:
+        l, c, t, f = (int(x) for x in sends[i])
+        assert f == 0, "copy schedule has a reduce flag"
+        s, d = int(src[l]), int(dst[l])
+        assert (s, c) in arrival and arrival[(s, c)] <= t, f"send {l, c, t}: source {s} does not hold chunk {c}"
+        assert (d, c) not in arrival, f"device {d} receives chunk {c} twice (or already held it)"
+        arrival[(d, c)] = t + int(T[l])
+        for (a, b) in busy.get(l, []):
+            assert t + T[l] <= a or b <= t, f"link {l} double-booked at {t}"
+        busy.setdefault(l, []).append((t, t + int(T[l])))
+        end_max = max(end_max, t + int(T[l]))
+    assert end_max == collective_time, f"collective time {collective_time} != latest end {end_max}"
+    for v in range(N):
+        for c in bits_of(coll.post, v):
+            assert (v, c) in arrival, f"postcondition unmet: NPU {v} chunk {c}"
+            assert arrival[(v, c)] <= collective_time
+    return arrival
+
+
+def check_reversed_schedule(topo, coll, sends: np.ndarray, copy_time: int):
+    """A reversed schedule (reduce flag) read backwards in time is a valid
+    copy schedule: map (l, c, t) back to (reverse(l), c, C* - t - T)."""
+    T = link_times(topo, coll.chunk_bytes)
+    rev = {(int(s), int(d)): l for l, (s, d) in enumerate(zip(topo.src, topo.dst))}
+    back = []
+    for l, c, t, f in sends:
+        assert f & 1, "reversed schedule without reduce flag"
+        rl = rev[(int(topo.dst[l]), int(topo.src[l]))]
+        assert T[rl] == T[l]
+        back.append((rl, c, copy_time - int(t) - int(T[l]), 0))
+    back = np.array(back, dtype=np.int64).reshape(-1, 4)
+    check_copy_schedule(topo, coll, back, copy_time)

@@ -1,0 +1,393 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these compare the oracle with the GPU library or with a retyped copy
+of its own arithmetic: they check closed forms, hand-worked examples,
+textbook special cases (Floyd-Warshall distances), exhaustive optimal
+schedules on tiny inputs, published SplitMix64 vectors and the schedule
+invariants of tests/invariants.py.
+"""
+
+import numpy as np
+import pytest
+from scipy.sparse import csr_matrix
+from scipy.sparse.csgraph import floyd_warshall
+
+from oracle import oracle as O
+from paper_2606_07019_amd import workloads as W
+
+from bruteforce import optimal_makespan
+from invariants import bits_of, check_copy_schedule, check_reversed_schedule, link_times
+
+
+def run(wl, mode=O.MODE_SKIP_IDLE):
+    r = O.run_workload(wl, mode)
+    assert r.status == 0, r.message
+    return r
+
+
+def wl_of(topo, coll, seed=0, name="t"):
+    return W.Workload(name, topo, coll, seed)
+
+
+def single_chunk(n_npus, src, dests, chunk_bytes=1 << 20, members=None):
+    members = members if members is not None else range(n_npus)
+    return W.collective_from_lists(n_npus, 1, chunk_bytes, [src], [dests], [list(members)])
+
+
+# ---------------------------------------------------------------- SplitMix64
+def test_splitmix64_published_vectors():
+    # Reference outputs of SplitMix64 (Vigna's public-domain splitmix64.c):
+    # seed 1234567 -> 6457827717110365317, 3203168211198807973, ...
+    ref = [6457827717110365317, 3203168211198807973, 9817491932198370423,
+           4593380528125082431, 16408922859458223821]
+    assert [O.splitmix64(1234567, c) for c in range(5)] == ref
+    assert O.splitmix64(0, 0) == 0xE220A8397B1DCDAF
+    assert O.splitmix64(0, 1) == 0x6E789E6AA1B965F4
+
+
+# ---------------------------------------------------------------- link times
+@pytest.mark.parametrize("k,expected", [(1, {21472}), (2, {3122, 5743}), (3, {1028, 1356, 2011}),
+                                        (4, {1328, 4622})])
+def test_link_time_closed_forms(k, expected):
+    # alpha + m / bandwidth (Sec. 4.6), 1 GB/s = 1 B/ns, rounded up to whole ns
+    wl = W.CONFIGS[k]()
+    r = run(wl) if k != 4 else O.run(wl.topo.n_npus, wl.topo.n_switches, wl.topo.src, wl.topo.dst,
+                                     wl.topo.alpha_ns, wl.topo.bw_GBps, 1, wl.coll.chunk_bytes,
+                                     np.zeros((512, 1), np.uint64), np.zeros((512, 1), np.uint64),
+                                     W.group_mask(512, range(512))[None, :])
+    assert set(int(x) for x in r.T) == expected
+
+
+# ---------------------------------------------------------------- distances
+@pytest.mark.parametrize("seed", range(12))
+def test_condition_distance_matches_floyd_warshall(seed):
+    wl = W.random_small(seed)
+    r = run(wl)
+    T = link_times(wl.topo, wl.coll.chunk_bytes)
+    D = wl.topo.n_devices
+    G = csr_matrix((T.astype(float), (wl.topo.src, wl.topo.dst)), shape=(D, D))
+    fw = floyd_warshall(G, directed=True)
+    dests = wl.coll.post & ~wl.coll.pre
+    for c in range(wl.coll.n_chunks):
+        s = int(r.chunk_src[c])
+        ds = [v for v in range(wl.topo.n_npus) if c in bits_of(dests, v)]
+        want = 0 if not ds else int(max(fw[s, v] for v in ds))
+        if s == 0xFFFFFFFF:
+            want = 0
+        assert int(r.chunk_dist[c]) == want
+
+
+# ---------------------------------------------------------------- priority
+@pytest.mark.parametrize("seed", range(6))
+def test_priority_order_properties(seed):
+    wl = W.random_small(seed, max_chunks=60)
+    r = run(wl)
+    C = wl.coll.n_chunks
+    assert sorted(r.rank.tolist()) == list(range(C))
+    order = np.argsort(r.rank)
+    keys = [O.splitmix64(wl.tie_seed, int(c)) for c in order]
+    for a, b in zip(range(C - 1), range(1, C)):
+        ca, cb = order[a], order[b]
+        assert r.chunk_dist[ca] >= r.chunk_dist[cb]
+        if r.chunk_dist[ca] == r.chunk_dist[cb]:
+            assert keys[a] < keys[b]
+
+
+def test_priority_longest_condition_goes_first():
+    # Alg. 3: conditions sorted by distance, descending.  Chunk a (0 -> 1)
+    # and chunk b (0 -> 2 through 1) compete for link 0->1: b (distance
+    # T01 + T12) goes first, a follows when the link is free again.
+    topo = W.make_topology(3, 0, [(0, 1), (1, 2)], [10, 10], [1, 1])
+    coll = W.collective_from_lists(3, 2, 5, [0, 0], [[1], [2]], [[0, 1, 2]])
+    r = run(wl_of(topo, coll, seed=7))
+    T = 15
+    np.testing.assert_array_equal(r.sends, [[0, 1, 0, 0], [0, 0, T, 0], [1, 1, T, 0]])
+    assert r.collective_time == 2 * T
+
+
+# ---------------------------------------------------------------- clash rule
+def test_clash_fastest_link_wins():
+    # Chunk 0 starts on NPU 0 and must reach {1, 2, 3}.  At t = 1 both 1 and
+    # 2 hold it and both links into 3 are free: the faster link 2->3 wins
+    # although 1->3 has the lower id; NPU 3 has it at 1 + 2 = 3, not 1 + 5.
+    pairs = [(0, 1), (0, 2), (1, 3), (2, 3)]
+    topo = W.make_topology(4, 0, pairs, [0, 0, 4, 1], [1, 1, 1, 1])
+    coll = single_chunk(4, 0, [1, 2, 3], chunk_bytes=1)
+    r = run(wl_of(topo, coll))
+    np.testing.assert_array_equal(r.sends, [[0, 0, 0, 0], [1, 0, 0, 0], [3, 0, 1, 0]])
+    assert r.collective_time == 3
+    assert r.stats["clashes"] == 1
+
+
+def test_clash_equal_times_lowest_link_id_wins():
+    pairs = [(0, 1), (0, 2), (2, 3), (1, 3)]
+    topo = W.make_topology(4, 0, pairs, [0, 0, 1, 1], [1, 1, 1, 1])
+    coll = single_chunk(4, 0, [1, 2, 3], chunk_bytes=1)
+    r = run(wl_of(topo, coll))
+    # links 2 (2->3) and 3 (1->3) tie on time; link 2 has the lower id
+    np.testing.assert_array_equal(r.sends, [[0, 0, 0, 0], [1, 0, 0, 0], [2, 0, 1, 0]])
+
+
+# ---------------------------------------------------------------- closed forms
+@pytest.mark.parametrize("p", [2, 3, 4, 5, 7, 8, 12, 16])
+def test_ring_allgather_closed_forms(p):
+    # Ring All-Gather takes p - 1 steps on a unidirectional ring (Sec. 2.3);
+    # on a bidirectional ring the greedy matching needs floor(p/2) steps.
+    T = 500 + (1 << 20) // 50 + 1
+    uni = run(wl_of(W.ring(p, bidirectional=False), W.all_gather(p, range(p), 1, 1 << 20)))
+    assert uni.collective_time == (p - 1) * T
+    assert len(uni.sends) == p * (p - 1)
+    assert uni.stats["clashes"] == 0
+    if p >= 3:
+        bi = run(wl_of(W.ring(p, bidirectional=True), W.all_gather(p, range(p), 1, 1 << 20)))
+        assert bi.collective_time == (p // 2) * T
+        assert len(bi.sends) == p * (p - 1)
+
+
+def test_config1_exact():
+    r = run(W.config1())
+    assert r.collective_time == 85888 and len(r.sends) == 56
+    # at the last step NPU i gets chunk i+4 from both neighbours: 8 clashes
+    assert r.stats["clashes"] == 8
+
+
+@pytest.mark.parametrize("n", [2, 3, 5, 8])
+def test_all_to_all_complete_graph(n):
+    pairs = [(i, j) for i in range(n) for j in range(n) if i != j]
+    topo = W.make_topology(n, 0, pairs, 100, 10)
+    r = run(wl_of(topo, W.all_to_all(n, range(n), 1000)))
+    assert r.collective_time == 200
+    assert len(r.sends) == n * (n - 1)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_broadcast_depth(seed):
+    # one chunk over a homogeneous graph: every NPU receives it at its hop
+    # distance times T, the collective time is the source's eccentricity
+    rng = W.SplitMix64(seed + 100)
+    n = 3 + rng.rand(8)
+    topo = W.mesh2d(n, 2, alpha=3, bw=1)
+    s = rng.rand(2 * n)
+    coll = single_chunk(2 * n, s, [v for v in range(2 * n) if v != s], chunk_bytes=4)
+    r = run(wl_of(topo, coll))
+    T = 7
+    D = 2 * n
+    G = csr_matrix((np.ones(topo.n_links), (topo.src, topo.dst)), shape=(D, D))
+    hops = floyd_warshall(G, directed=True, unweighted=True)[s]
+    arr = check_copy_schedule(topo, coll, r.sends, r.collective_time)
+    for v in range(D):
+        if v != s:
+            assert arr[(v, 0)] == hops[v] * T
+    assert r.collective_time == hops.max() * T
+
+
+def test_relay_through_non_member():
+    # path 0 -> 1 -> 2, process group {0, 2}: NPU 1 is outside the group but
+    # relays (Sec. 4.3 path filtering keeps intermediate devices)
+    topo = W.make_topology(3, 0, [(0, 1), (1, 2)], 5, 1)
+    coll = single_chunk(3, 0, [2], chunk_bytes=5, members=[0, 2])
+    r = run(wl_of(topo, coll))
+    np.testing.assert_array_equal(r.sends, [[0, 0, 0, 0], [1, 0, 10, 0]])
+    assert r.collective_time == 20
+
+
+def test_relay_through_switch():
+    # two NPUs behind one switch (Sec. 4.7): every chunk crosses the switch
+    topo = W.make_topology(2, 1, [(0, 2), (2, 0), (1, 2), (2, 1)], 1, 1)
+    coll = W.all_gather(2, [0, 1], 1, 1)
+    r = run(wl_of(topo, coll))
+    assert r.collective_time == 4
+    assert len(r.sends) == 4
+    check_copy_schedule(topo, coll, r.sends, r.collective_time)
+
+
+@pytest.mark.slow
+def test_config4_structure():
+    # 2-level rails: every inter-node chunk takes NPU -> its rail switch ->
+    # (destination node, same local index) -> destination; one holder per
+    # in-neighbour, so no clashes, no wasted relays, 745,472 transfers, and
+    # each uplink carries 504 chunks of 4,622 ns.
+    r = run(W.config4())
+    assert len(r.sends) == 745472
+    assert r.stats["clashes"] == 0 and r.stats["wasted"] == 0
+    assert r.collective_time >= 504 * 4622
+
+
+def test_allreduce_is_reversed_then_forward():
+    wl = W.config2()
+    r = run(wl)
+    coll_ag = W.config2().coll
+    coll_ag.op = W.OP_COPY
+    ag = run(wl_of(wl.topo, coll_ag))
+    assert r.collective_time == 2 * ag.collective_time
+    rs = r.sends[r.sends[:, 3] == 1]
+    fw = r.sends[r.sends[:, 3] == 0].copy()
+    fw[:, 2] -= ag.collective_time
+    np.testing.assert_array_equal(fw, ag.sends)
+    check_reversed_schedule(wl.topo, coll_ag, rs, ag.collective_time)
+
+
+# ---------------------------------------------------------------- process groups
+def test_mesh3x3_two_groups_invariants():
+    # Sec. 6.4: two process groups on a 3x3 mesh run independent collectives
+    wl = W.mesh3x3_two_groups()
+    r = run(wl)
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+
+
+@pytest.mark.xfail(strict=True, reason=(
+    "relay needs come from uncongested shortest-path trees (the link-parallel "
+    "reading of the path filtering step), so row-0 and row-2 traffic stays on "
+    "its rows; the detours through NPUs 3..5 in the paper's example come from "
+    "the condition-sequential BFS of Alg. 3 routing around links removed by "
+    "earlier conditions"))
+def test_mesh3x3_two_groups_detours_through_outside_npus():
+    wl = W.mesh3x3_two_groups()
+    r = run(wl)
+    touched = set(wl.topo.src[r.sends[:, 0]]) | set(wl.topo.dst[r.sends[:, 0]])
+    assert touched & {3, 4, 5}
+
+
+def test_process_group_relays_through_non_members():
+    # All-Gather between NPUs 0 and 6 of the 3x3 mesh: every shortest path
+    # crosses NPU 3, which is in no process group and relays both ways
+    topo = W.mesh2d(3, 3)
+    coll = W.all_gather(9, [0, 6], 1, 1 << 20)
+    r = run(wl_of(topo, coll))
+    check_copy_schedule(topo, coll, r.sends, r.collective_time)
+    relays = set(int(topo.dst[l]) for l in r.sends[:, 0]) - {0, 6}
+    assert relays == {3}
+    T = 500 + (1 << 20) // 50 + 1
+    assert r.collective_time == 2 * T
+
+
+# ---------------------------------------------------------------- invariants
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_invariants_configs(k):
+    wl = W.CONFIGS[k]()
+    r = run(wl)
+    if wl.coll.op == W.OP_ALLREDUCE:
+        return  # covered by test_allreduce_is_reversed_then_forward
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+    assert r.collective_time >= int(r.chunk_dist.max())
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_invariants_fuzz(seed):
+    wl = W.random_small(seed)
+    r = run(wl)
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+    assert r.collective_time >= int(r.chunk_dist.max(initial=0))
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_plain_and_idle_skip_modes_agree(seed):
+    wl = W.random_small(seed)
+    a, b = run(wl, O.MODE_PLAIN), run(wl, O.MODE_SKIP_IDLE)
+    np.testing.assert_array_equal(a.sends, b.sends)
+    assert a.stats["clashes"] == b.stats["clashes"] and a.stats["rounds"] == b.stats["rounds"]
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_plain_and_idle_skip_modes_agree_configs(k):
+    wl = W.CONFIGS[k]()
+    a, b = run(wl, O.MODE_PLAIN), run(wl, O.MODE_SKIP_IDLE)
+    np.testing.assert_array_equal(a.sends, b.sends)
+
+
+# ---------------------------------------------------------------- brute force
+def tiny_instance(seed):
+    rng = W.SplitMix64(seed + 5000)
+    D = 2 + rng.rand(3)
+    pairs = set()
+    order = rng.shuffle(range(D))
+    for k in range(D):
+        pairs.add((order[k], order[(k + 1) % D]))
+    while len(pairs) < min(6, D * (D - 1)) and rng.rand(3):
+        u, v = rng.rand(D), rng.rand(D)
+        if u != v:
+            pairs.add((u, v))
+    pairs = sorted(pairs)
+    alpha = [rng.rand(2) for _ in pairs]
+    topo = W.make_topology(D, 0, pairs, alpha, 1)
+    C = 1 + rng.rand(3)
+    src_of, dests_of = [], []
+    for c in range(C):
+        s = rng.rand(D)
+        ds = [v for v in range(D) if v != s and rng.rand(2)]
+        src_of.append(s)
+        dests_of.append(ds)
+    coll = W.collective_from_lists(D, C, 1, src_of, dests_of, [list(range(D))])
+    return wl_of(topo, coll, seed=seed)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_never_beats_exhaustive_optimum(seed):
+    wl = tiny_instance(seed)
+    r = run(wl)
+    opt = optimal_makespan(wl.topo, wl.coll)
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+    assert r.collective_time >= opt
+
+
+@pytest.mark.parametrize("p", [2, 3, 4])
+def test_forced_families_reach_optimum(p):
+    # unidirectional ring All-Gather and single-chunk broadcast on a
+    # bidirectional ring: the greedy matching is optimal on both
+    wl = wl_of(W.ring(p, bidirectional=False, alpha=1, bw=1), W.all_gather(p, range(p), 1, 1))
+    assert run(wl).collective_time == optimal_makespan(wl.topo, wl.coll)
+    if p >= 3:
+        coll = single_chunk(p, 0, list(range(1, p)), chunk_bytes=1)
+        wl2 = wl_of(W.ring(p, bidirectional=True, alpha=1, bw=1), coll)
+        assert run(wl2).collective_time == optimal_makespan(wl2.topo, wl2.coll)
+    if p == 2:
+        wl3 = wl_of(W.make_topology(2, 0, [(0, 1), (1, 0)], 1, 1), W.all_to_all(2, range(2), 1))
+        assert run(wl3).collective_time == optimal_makespan(wl3.topo, wl3.coll)
+
+
+# ---------------------------------------------------------------- failures
+def _err(wl):
+    return O.run_workload(wl).status_name
+
+
+def test_errors():
+    base = W.config1()
+    t = base.topo
+    # two holders
+    c = W.config1().coll
+    W.set_bit(c.pre, 1, 0)
+    assert _err(wl_of(t, c)) == "EINVAL"
+    # bit on a non-member
+    c = W.all_gather(8, range(4), 1, 1 << 20)
+    W.set_bit(c.post, 6, 0)
+    assert _err(wl_of(t, c)) == "EINVAL"
+    # needed but held by nobody
+    c = W.config1().coll
+    c.pre[0, 0] &= ~np.uint64(1)
+    assert _err(wl_of(t, c)) == "EINVAL"
+    # bit beyond the last chunk
+    c = W.config1().coll
+    W.set_bit(c.post, 0, 9)
+    assert _err(wl_of(t, c)) == "EINVAL"
+    # self loop, duplicate link, zero bandwidth
+    for pairs, bw in (([(0, 0), (0, 1)], 1), ([(0, 1), (0, 1)], 1), ([(0, 1), (1, 0)], 0)):
+        tp = W.make_topology(2, 0, pairs, 1, bw)
+        assert _err(wl_of(tp, W.all_gather(2, [0, 1], 1, 8))) == "EINVAL"
+    # unreachable destination
+    tp = W.make_topology(2, 0, [(1, 0)], 1, 1)
+    assert _err(wl_of(tp, W.all_gather(2, [0, 1], 1, 8))) == "EUNREACHABLE"
+    # link time beyond 32 bits
+    assert _err(wl_of(t, W.all_gather(8, range(8), 1, 1 << 40))) == "ERANGE"
+    # reduction over a link without a reverse link of equal time
+    tp = W.ring(4, bidirectional=False)
+    assert _err(wl_of(tp, W.all_gather(4, range(4), 1, 1 << 20, op=W.OP_ALLREDUCE))) == "EUNSUPPORTED"
+
+
+def test_empty_and_trivial_collectives():
+    t = W.config1().topo
+    c = W.collective_from_lists(8, 0, 1024, [], [], [list(range(8))])
+    r = run(wl_of(t, c))
+    assert len(r.sends) == 0 and r.collective_time == 0 and r.stats["events"] == 1
+    c = W.collective_from_lists(8, 3, 1024, [0, 1, None], [[], [1], []], [list(range(8))])
+    r = run(wl_of(t, c))
+    assert len(r.sends) == 0 and r.collective_time == 0
