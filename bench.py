@@ -1,0 +1,151 @@
+#!/usr/bin/env python3
+"""Benchmark of the synthesis matcher on one MI355X.
+
+One step = one full pccl_synthesize call on the 512-NPU All-to-All over the
+2-level rail-switch topology (64 nodes x 8 NPUs, 400 GB/s intra-node, 8
+switches at 50 GB/s, 128 KiB chunks): conditions, shortest paths, relays,
+priority order, the matching event loop and the canonical schedule, with the
+pre/postcondition bitmaps already resident in HBM.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config k] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+# Algorithmic bytes of the matching kernel, per launch:
+# 16 B per scanned word position (one 8-byte word of the source's holds row
+# and one of the destination's needs row) plus, per committed transfer, the
+# needs-word read-modify-write (16 B), the holds-word fold at arrival (16 B),
+# the send-log record (12 B), the link state written back (16 B) and the
+# snapshot entry (8 B): 68 B.
+BYTES_PER_SCANNED_WORD = 16
+BYTES_PER_MATCH = 68
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, budget_s: float = 30.0):
+    """The CPU oracle as it stands, single-threaded, on the same workload."""
+    from oracle import oracle as O
+    t0 = time.perf_counter()
+    r = O.run_workload(wl)
+    dt = time.perf_counter() - t0
+    if r.status != 0:
+        raise RuntimeError(r.message)
+    cpu = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": len(r.sends) / dt, "unit": "matches/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole {wl.name} synthesis, one run ({dt:.1f} s, 1 thread, "
+                      f"host {os.cpu_count()} threads of {cpu})",
+            "seconds": dt, "n_sends": len(r.sends), "collective_time_ns": r.collective_time}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: the synthesis matcher runs on one GPU; there is no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_07019_amd import workloads as W
+    from paper_2606_07019_amd.pccl import Synthesizer
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("no GPU visible")
+    wl = W.CONFIGS[args.config]()
+    log(f"[bench] workload {wl.name}: {wl.topo.n_devices} devices, {wl.topo.n_links} links, "
+        f"{wl.coll.n_chunks} chunks")
+    syn = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed, device=0)
+    for i in range(args.warmup):
+        syn.synthesize()
+        log(f"[bench] warmup {i}: {syn.n_sends} sends, collective time {syn.collective_time} ns")
+    torch.cuda.synchronize()
+    match_ms, setup_ms, output_ms = [], [], []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        syn.synthesize()
+        p = syn.profile()
+        match_ms.append(p["match_ms"])
+        setup_ms.append(p["setup_ms"])
+        output_ms.append(p["output_ms"])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    step_s = dt / max(args.steps, 1)
+    prof = syn.profile()
+    st = syn.stats()
+    n = syn.n_sends
+    log(f"[bench] {args.steps} steps in {dt:.3f} s; stages (ms, last step) {prof}")
+
+    avg_match_s = sum(match_ms) / len(match_ms) / 1e3
+    alg_bytes = BYTES_PER_SCANNED_WORD * prof["scan_words"] + BYTES_PER_MATCH * n
+    achieved = alg_bytes / avg_match_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 3), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 6), "traffic": None,
+                "kernel": "k_match", "kernel_ms": round(avg_match_s * 1e3, 4),
+                "alg_bytes_per_launch": alg_bytes, "scan_words": prof["scan_words"], "matches": n}
+
+    out = {
+        "metric": "synthesis wall time (s) + link-chunk matches/s, 512-NPU All-to-All; HBM GB/s",
+        "value": n / step_s,
+        "unit": "matches/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "npus": wl.topo.n_npus, "switches": wl.topo.n_switches,
+                   "links": wl.topo.n_links, "chunks": wl.coll.n_chunks, "chunk_bytes": wl.coll.chunk_bytes,
+                   "sends": n, "collective_time_ns": syn.collective_time, "windows": st["windows"],
+                   "events": st["events"], "rounds": st["rounds"], "clashes": st["clashes"]},
+        "synthesis_wall_s": step_s,
+        "stage_ms": {"setup": sum(setup_ms) / len(setup_ms), "match": sum(match_ms) / len(match_ms),
+                     "output": sum(output_ms) / len(output_ms)},
+        "roofline": roofline,
+        "context": {"paper_512npu_a2a_synthesis_s": 700.8, "paper_hardware": "not stated",
+                    "paper_topology": "2D Mesh / 3D Hypercube family (not this topology)"},
+    }
+    syn.close()
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on the same workload ...")
+        cb = cpu_baseline(wl)
+        if cb["n_sends"] != n or cb["collective_time_ns"] != out["config"]["collective_time_ns"]:
+            raise RuntimeError("GPU and oracle schedules differ in size or collective time")
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        out["cpu_baseline"]["seconds"] = cb["seconds"]
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

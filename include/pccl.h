@@ -1,0 +1,208 @@
+/*
+ * pccl.h -- C ABI of the MI355X synthesis matcher for PCCL
+ * ("PCCL: Process Group-Aware Scalable and Generic Collective Algorithm
+ * Synthesizer").
+ *
+ * The library synthesizes a collective algorithm -- a schedule of
+ * (link, chunk, start time) transfers -- for a modeled network topology, a
+ * collective given as NPU-centric pre/postconditions, and one or more process
+ * groups.  Everything from the derivation of the conditions to the canonical
+ * schedule runs on one AMD Instinct GPU (gfx950); the host side only checks
+ * and stages the small topology arrays and launches kernels.
+ *
+ * Call order: pccl_create -> pccl_load_topology -> pccl_set_collective ->
+ * pccl_workspace_bytes -> pccl_set_workspace -> pccl_synthesize (any number
+ * of times) -> pccl_get_schedule / pccl_get_stats / pccl_get_setup ->
+ * pccl_destroy.  A call made out of order returns PCCL_ESTATE.  A context is
+ * not thread-safe; use one per thread.
+ *
+ * Every function returns a pccl_status; no C++ exception crosses the ABI.
+ * pccl_last_error() returns a message for the last failed call.
+ */
+#ifndef PCCL_H
+#define PCCL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct pccl_ctx pccl_ctx;
+
+typedef enum {
+    PCCL_OK = 0,
+    PCCL_EINVAL = 1,        /* malformed topology or collective */
+    PCCL_EUNREACHABLE = 2,  /* a destination cannot be reached from its source */
+    PCCL_ERANGE = 3,        /* a time in ns does not fit in 32 bits */
+    PCCL_ENOMEM = 4,        /* workspace too small for this collective */
+    PCCL_EDEVICE = 5,       /* a HIP call failed */
+    PCCL_ESTATE = 6,        /* call out of order */
+    PCCL_EUNSUPPORTED = 7,  /* outside the supported envelope (see each call) */
+    PCCL_EDEADLOCK = 8,     /* needs remain but nothing is in flight (never on valid input) */
+    PCCL_EINTERNAL = 9      /* internal error (watchdog, caught exception) */
+} pccl_status;
+
+/*
+ * Collective operations (paper Sec. 4.5, "Reduction Operations").
+ *   PCCL_OP_COPY: non-reduction patterns (All-Gather, All-to-All(v),
+ *     Broadcast, Scatter, any generic pre/postcondition).
+ *   PCCL_OP_REDUCE_REVERSED: pre/post describe the dual copy pattern (e.g.
+ *     All-Gather for Reduce-Scatter, Broadcast for Reduce); the output is the
+ *     time reversal of the copy schedule: each send (l, c, t) becomes
+ *     (reverse(l), c, C* - t - T[l]) with the reduce flag, C* being the copy
+ *     schedule's collective time.  Every link needs a reverse link of equal
+ *     transfer time, else PCCL_EUNSUPPORTED.
+ *   PCCL_OP_ALLREDUCE: pre/post describe the All-Gather half; the output is
+ *     the reversed schedule (Reduce-Scatter) followed by the copy schedule
+ *     shifted by C*; collective time 2 C*.
+ */
+typedef enum {
+    PCCL_OP_COPY = 0,
+    PCCL_OP_REDUCE_REVERSED = 1,
+    PCCL_OP_ALLREDUCE = 2
+} pccl_op;
+
+/* One transfer of the schedule: `link` starts sending chunk `chunk` (the
+ * caller's chunk id) at `t_start_ns`; it occupies the link for T[link] ns.
+ * flags bit 0 = the receiver reduces (adds) instead of copying. */
+typedef struct {
+    uint32_t link;
+    uint32_t chunk;
+    uint32_t t_start_ns;
+    uint32_t flags;
+} pccl_send;
+
+#define PCCL_SEND_REDUCE 1u
+
+/*
+ * Creates a context bound to HIP device `hip_device`.  `tie_seed` seeds the
+ * tie-break among chunks of equal distance: chunks are ordered by distance
+ * descending (Alg. 3 sorts conditions by their distance, Sec. 4.4), then by
+ * the SplitMix64 output number c+1 of a generator started at `tie_seed`
+ * ascending.  Returns PCCL_EDEVICE if the device cannot be selected.
+ */
+pccl_status pccl_create(pccl_ctx **out, int hip_device, uint64_t tie_seed);
+
+/* Releases the context (not the caller's workspace).  NULL is ignored. */
+void pccl_destroy(pccl_ctx *ctx);
+
+/*
+ * Loads the network (paper Sec. 4.2 TEN; Sec. 4.6 alpha-beta links; Sec. 4.7
+ * switches).  Devices 0..n_npus-1 are NPUs, n_npus..n_npus+n_switches-1 are
+ * switches (relay-only devices).  Link l is directed link_src[l] ->
+ * link_dst[l] with latency alpha_ns[l] and bandwidth bw_GBps[l] (1 GB/s is one
+ * byte per ns).  All arrays are host memory of n_links entries and are copied.
+ * PCCL_EINVAL: endpoint out of range, self loop, duplicate (src, dst) pair,
+ * zero bandwidth, n_npus == 0.  PCCL_EUNSUPPORTED: more than 8000 devices
+ * (NPUs plus switches), more than 256 in-links on one device, or a device
+ * whose in-links' sources have more than 1024 in-links in total (the
+ * per-destination state of the matching kernel lives in 30 KB of LDS).
+ */
+pccl_status pccl_load_topology(pccl_ctx *ctx, uint32_t n_npus, uint32_t n_switches,
+                               uint32_t n_links, const uint32_t *link_src,
+                               const uint32_t *link_dst, const uint32_t *alpha_ns,
+                               const uint32_t *bw_GBps);
+
+/*
+ * Sets the collective (paper Sec. 2.1 pre/postconditions, Sec. 2.2 process
+ * groups, Sec. 4.1 conditions).
+ *   n_chunks, chunk_bytes: C chunks of m bytes each (m >= 1).
+ *   pre_bits, post_bits: DEVICE pointers to n_npus rows of ceil(C/64)
+ *     uint64 words, LSB first (chunk c is bit c%64 of word c/64).  Row v of
+ *     pre holds the chunks NPU v has before the collective, row v of post the
+ *     chunks it must have after.  They are read by pccl_synthesize, so they
+ *     must stay valid and unchanged until the last synthesize call.
+ *   group_masks: HOST pointer to n_groups rows of ceil(n_npus/64) words, the
+ *     members of each process group (copied).
+ *   chunk_group: DEVICE pointer to C uint16 group ids, or NULL when
+ *     n_groups == 1.
+ * Checked here: sizes and group masks (PCCL_EINVAL).  Checked on the device
+ * by pccl_synthesize (PCCL_EINVAL): each chunk with a postcondition bit has
+ * exactly one precondition holder, no chunk has two holders, pre/post bits
+ * only at members of the chunk's group, no bits beyond chunk C-1, group ids
+ * in range.  A link time alpha + ceil(m / bw) above 2^32-1 gives PCCL_ERANGE.
+ */
+pccl_status pccl_set_collective(pccl_ctx *ctx, uint32_t n_chunks, uint64_t chunk_bytes,
+                                const uint64_t *pre_bits, const uint64_t *post_bits,
+                                const uint64_t *group_masks, uint32_t n_groups,
+                                const uint16_t *chunk_group, pccl_op op);
+
+/*
+ * Device workspace needed by pccl_synthesize for at most `max_sends`
+ * copy-schedule transfers (0 = the safe bound C * (D - 1), D = all devices).
+ * The number of copy transfers equals the number of (device, chunk) pairs
+ * that must receive the chunk: destinations plus relays.
+ */
+pccl_status pccl_workspace_bytes(pccl_ctx *ctx, uint64_t max_sends, size_t *out_bytes);
+
+/*
+ * Hands over the device workspace (caller-owned, 256-byte aligned, at least
+ * the size pccl_workspace_bytes returned for `max_sends`) and the HIP stream
+ * to run on (NULL = the default stream).  The library allocates no device
+ * memory of its own.  The workspace must not be used by the caller while a
+ * synthesize call runs.  PCCL_ENOMEM if `bytes` is too small.
+ */
+pccl_status pccl_set_workspace(pccl_ctx *ctx, void *device_ptr, size_t bytes,
+                               uint64_t max_sends, void *hip_stream);
+
+/*
+ * Runs the whole synthesis on the device and waits for it: conditions,
+ * shortest-path distances and relay devices (Alg. 3 distances; the
+ * path-filtering step after Alg. 2), priority order (Alg. 3), the
+ * event-stepped link-parallel matching (the BFS step of Alg. 2 applied to all
+ * free links at once; link exclusivity of Sec. 4.4 and 4.6; chunk arrival
+ * times of Sec. 4.6; NextAvailableTime of Alg. 1), and the canonical schedule
+ * (sorted by start time, then link id; reversed for reduction ops).
+ * Outputs the number of sends and the collective time (latest transfer end).
+ * The schedule stays in the workspace until the next synthesize call.
+ * PCCL_ENOMEM if the collective needs more than max_sends transfers.
+ */
+pccl_status pccl_synthesize(pccl_ctx *ctx, uint64_t *n_sends, uint32_t *collective_time_ns);
+
+/* Copies the schedule (canonical order) to `out`, host or device memory,
+ * at most `capacity` entries.  PCCL_EINVAL if capacity is too small. */
+pccl_status pccl_get_schedule(pccl_ctx *ctx, pccl_send *out, uint64_t capacity);
+
+/*
+ * Statistics of the last synthesize call:
+ *   events  -- distinct event times visited by the event loop (time 0 plus
+ *              every transfer end up to the last transfer start),
+ *   rounds  -- (event, destination) pick rounds that made at least one pick,
+ *   clashes -- picks that lost a (destination, chunk) clash,
+ *   windows -- synchronous look-ahead windows the device loop ran.
+ * Any pointer may be NULL.
+ */
+pccl_status pccl_get_stats(pccl_ctx *ctx, uint64_t *events, uint64_t *rounds,
+                           uint64_t *clashes, uint64_t *windows);
+
+/*
+ * Setup products of the last synthesize call, copied to host arrays (any may
+ * be NULL): link_time_ns[L] = alpha + ceil(m / bw); chunk_src[C] (source NPU
+ * or 0xFFFFFFFF when the chunk is unused); chunk_dist[C] (max shortest-path
+ * distance in ns from the source to the destinations, 0 if none);
+ * chunk_rank[C] (position in the priority order).
+ */
+pccl_status pccl_get_setup(pccl_ctx *ctx, uint32_t *link_time_ns, uint32_t *chunk_src,
+                           uint64_t *chunk_dist, uint32_t *chunk_rank);
+
+/*
+ * Timing and work counters of the last synthesize call, measured with HIP
+ * events recorded on the library's stream around its three stages: setup
+ * (conditions to initial bitmaps), matching (the persistent event-loop
+ * kernel) and output (canonical sort and reversal).  scan_words counts the
+ * 64-bit words of the two rows the intersect read (from a link's cursor
+ * through the word holding its pick, or to the row end when it found
+ * none).  Any pointer may be NULL.
+ */
+pccl_status pccl_get_profile(pccl_ctx *ctx, double *setup_ms, double *match_ms, double *output_ms,
+                             uint64_t *scan_words);
+
+/* Message of the last failed call on this context ("" if none). */
+const char *pccl_last_error(const pccl_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PCCL_H */

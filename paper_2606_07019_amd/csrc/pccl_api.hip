@@ -1,0 +1,562 @@
+// C ABI of the synthesis matcher: argument checks, the workspace layout,
+// staging of the small topology arrays and the launch sequence.  All
+// per-chunk and per-send work runs in the kernels of pccl_setup.hip,
+// pccl_match.hip and pccl_sort.hip.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <exception>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "pccl.h"
+#include "pccl_internal.h"
+
+using namespace pccl;
+
+struct pccl_ctx {
+    int device = 0;
+    uint64_t seed = 0;
+    std::string err;
+    bool have_topo = false, have_coll = false, have_ws = false, uploaded = false, have_result = false;
+    // topology
+    uint32_t N = 0, S = 0, D = 0, L = 0;
+    std::vector<uint32_t> src, dst, alpha, bw;
+    std::vector<uint32_t> in_off, slot_link, slot_src, slot_cum, dest_pairs, rev;
+    // collective
+    uint32_t C = 0, G = 0;
+    uint64_t m = 0;
+    const uint64_t *pre = nullptr, *post = nullptr;
+    const uint16_t *chunk_group = nullptr;
+    std::vector<uint64_t> gmask;
+    int op = 0;
+    std::vector<uint32_t> T, slot_time;
+    uint32_t tmin = 0;
+    // workspace
+    char *ws = nullptr;
+    size_t ws_bytes = 0;
+    uint64_t max_sends = 0;
+    hipStream_t stream = nullptr;
+    Layout ly{};
+    Sizes sz{};
+    int grid = 0;
+    // stage timing
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    float stage_ms[3] = {0.f, 0.f, 0.f};
+    ~pccl_ctx()
+    {
+        for (hipEvent_t e : ev)
+            if (e) (void)hipEventDestroy(e);
+    }
+    // results
+    uint64_t n_sends = 0, n_copy = 0;
+    uint32_t coll_time = 0;
+    Control ctl_host{};
+};
+
+namespace {
+
+pccl_status fail(pccl_ctx *c, pccl_status st, const char *fmt, ...) __attribute__((format(printf, 3, 4)));
+pccl_status fail(pccl_ctx *c, pccl_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (c) c->err = buf;
+    return st;
+}
+
+pccl_status hip_fail(pccl_ctx *c, hipError_t e, const char *what)
+{
+    return fail(c, PCCL_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_OR_FAIL(ctx, expr)                                   \
+    do {                                                         \
+        hipError_t e_ = (expr);                                  \
+        if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr); \
+    } while (0)
+
+uint64_t words(uint64_t bits) { return (bits + 63) / 64; }
+
+// Workspace carving: every array 256-byte aligned, in a fixed order.
+struct Carver {
+    char *base;
+    size_t off = 0;
+    template <class X>
+    X *take(uint64_t count)
+    {
+        off = (off + 255) & ~size_t(255);
+        X *p = base ? reinterpret_cast<X *>(base + off) : nullptr;
+        off += sizeof(X) * (count ? count : 1);
+        return p;
+    }
+};
+
+void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, size_t &total)
+{
+    sz.N = c->N;
+    sz.S = c->S;
+    sz.D = c->D;
+    sz.L = c->L;
+    sz.C = c->C;
+    sz.G = c->G;
+    sz.W = words(c->C);
+    sz.Wp = std::max<uint64_t>(ROW_ALIGN_WORDS, (sz.W + ROW_ALIGN_WORDS - 1) / ROW_ALIGN_WORDS * ROW_ALIGN_WORDS);
+    sz.WN = words(c->N);
+    sz.max_sends = max_sends;
+    sz.tmin = c->tmin;
+    const uint64_t nsort = std::max<uint64_t>(c->C, max_sends);
+    sz.max_tiles = (uint32_t)((nsort + SORT_TILE - 1) / SORT_TILE);
+    if (sz.max_tiles == 0) sz.max_tiles = 1;
+    const uint64_t L = c->L, D = c->D, N = c->N, C = c->C;
+    Carver cv{base};
+    ly.ctl = cv.take<Control>(1);
+    ly.lsrc = cv.take<uint32_t>(L);
+    ly.ldst = cv.take<uint32_t>(L);
+    ly.ltime = cv.take<uint32_t>(L);
+    ly.lrev = cv.take<uint32_t>(L);
+    ly.in_off = cv.take<uint32_t>(D + 1);
+    ly.slot_link = cv.take<uint32_t>(L);
+    ly.slot_src = cv.take<uint32_t>(L);
+    ly.slot_time = cv.take<uint32_t>(L);
+    ly.slot_cum = cv.take<uint32_t>(L);
+    ly.dest_pairs = cv.take<uint32_t>(D);
+    ly.group_masks = cv.take<uint64_t>((uint64_t)c->G * sz.WN);
+    ly.chunk_src = cv.take<uint32_t>(C);
+    ly.holder_cnt = cv.take<uint32_t>(C);
+    ly.chunk_dist = cv.take<uint64_t>(C);
+    ly.rank = cv.take<uint32_t>(C);
+    ly.order = cv.take<uint32_t>(C);
+    ly.src_index = cv.take<uint32_t>(N);
+    ly.src_list = cv.take<uint32_t>(N);
+    ly.sp_dist = cv.take<uint64_t>(N * D);
+    ly.sp_parent = cv.take<uint32_t>(N * D);
+    ly.skey[0] = cv.take<uint64_t>(nsort);
+    ly.skey[1] = cv.take<uint64_t>(nsort);
+    ly.sval[0] = cv.take<uint32_t>(nsort);
+    ly.sval[1] = cv.take<uint32_t>(nsort);
+    ly.hist = cv.take<uint32_t>(256ull * sz.max_tiles);
+    ly.holds = cv.take<uint64_t>(D * sz.Wp);
+    ly.needs = cv.take<uint64_t>(D * sz.Wp);
+    ly.busy = cv.take<uint32_t>(L);
+    ly.infl = cv.take<uint32_t>(L);
+    ly.cur = cv.take<uint32_t>(L);
+    ly.lflags = cv.take<uint32_t>(L);
+    ly.snap = cv.take<uint64_t>(3 * L);
+    ly.out = cv.take<pccl_send>((c->op == PCCL_OP_ALLREDUCE ? 2 : 1) * max_sends);
+    total = (cv.off + 255) & ~size_t(255);
+}
+
+uint64_t safe_max_sends(const pccl_ctx *c)
+{
+    return (uint64_t)c->C * (c->D > 0 ? c->D - 1 : 0);
+}
+
+const char *einval_detail(uint32_t code)
+{
+    switch (code) {
+    case 1: return "a bit is set beyond the last chunk";
+    case 2: return "a pre/postcondition bit sits on an NPU outside the chunk's process group";
+    case 3: return "chunk group id out of range";
+    case 4: return "chunk has more than one precondition holder";
+    case 5: return "chunk is needed by a postcondition but held by no NPU";
+    default: return "invalid collective";
+    }
+}
+
+}  // namespace
+
+#define GUARD_BEGIN try {
+#define GUARD_END(ctx)                                                   \
+    }                                                                    \
+    catch (const std::exception &ex)                                     \
+    {                                                                    \
+        return fail((ctx), PCCL_EINTERNAL, "exception: %s", ex.what()); \
+    }                                                                    \
+    catch (...)                                                          \
+    {                                                                    \
+        return fail((ctx), PCCL_EINTERNAL, "unknown exception");         \
+    }
+
+extern "C" {
+
+pccl_status pccl_create(pccl_ctx **out, int hip_device, uint64_t tie_seed)
+{
+    if (!out) return PCCL_EINVAL;
+    *out = nullptr;
+    GUARD_BEGIN
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess || hip_device < 0 || hip_device >= n) return PCCL_EDEVICE;
+    if (hipSetDevice(hip_device) != hipSuccess) return PCCL_EDEVICE;
+    pccl_ctx *c = new pccl_ctx();
+    c->device = hip_device;
+    c->seed = tie_seed;
+    *out = c;
+    return PCCL_OK;
+    GUARD_END(nullptr)
+}
+
+void pccl_destroy(pccl_ctx *ctx) { delete ctx; }
+
+const char *pccl_last_error(const pccl_ctx *ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+pccl_status pccl_load_topology(pccl_ctx *c, uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
+                               const uint32_t *link_src, const uint32_t *link_dst, const uint32_t *alpha_ns,
+                               const uint32_t *bw_GBps)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    if (n_npus == 0) return fail(c, PCCL_EINVAL, "no NPUs");
+    if (n_links && (!link_src || !link_dst || !alpha_ns || !bw_GBps)) return fail(c, PCCL_EINVAL, "null link array");
+    const uint64_t D64 = (uint64_t)n_npus + n_switches;
+    if (D64 > MAX_DEVICES_SP) return fail(c, PCCL_EUNSUPPORTED, "%llu devices (limit %u)", (unsigned long long)D64, MAX_DEVICES_SP);
+    const uint32_t D = (uint32_t)D64, L = n_links;
+    std::unordered_map<uint64_t, uint32_t> seen;
+    seen.reserve(L * 2 + 1);
+    for (uint32_t l = 0; l < L; l++) {
+        if (link_src[l] >= D || link_dst[l] >= D) return fail(c, PCCL_EINVAL, "link %u endpoint out of range", l);
+        if (link_src[l] == link_dst[l]) return fail(c, PCCL_EINVAL, "link %u is a self loop", l);
+        if (bw_GBps[l] == 0) return fail(c, PCCL_EINVAL, "link %u has zero bandwidth", l);
+        const uint64_t key = ((uint64_t)link_src[l] << 32) | link_dst[l];
+        auto it = seen.find(key);
+        if (it != seen.end()) return fail(c, PCCL_EINVAL, "links %u and %u are duplicates", it->second, l);
+        seen.emplace(key, l);
+    }
+    // destination-major slots
+    std::vector<uint32_t> in_off(D + 1, 0), fill(D, 0), slot_link(L), slot_src(L), slot_cum(L), dest_pairs(D, 0);
+    for (uint32_t l = 0; l < L; l++) in_off[link_dst[l] + 1]++;
+    for (uint32_t v = 0; v < D; v++) in_off[v + 1] += in_off[v];
+    for (uint32_t l = 0; l < L; l++) {
+        const uint32_t d = link_dst[l], sl = in_off[d] + fill[d]++;
+        slot_link[sl] = l;
+        slot_src[sl] = link_src[l];
+    }
+    for (uint32_t d = 0; d < D; d++) {
+        const uint32_t indeg = in_off[d + 1] - in_off[d];
+        if (indeg > MAX_IN_LINKS)
+            return fail(c, PCCL_EUNSUPPORTED, "device %u has %u in-links (limit %u)", d, indeg, MAX_IN_LINKS);
+        uint64_t cum = 0;
+        for (uint32_t sl = in_off[d]; sl < in_off[d + 1]; sl++) {
+            slot_cum[sl] = (uint32_t)cum;
+            const uint32_t s = slot_src[sl];
+            cum += in_off[s + 1] - in_off[s];
+        }
+        if (cum > MAX_PAIRS)
+            return fail(c, PCCL_EUNSUPPORTED, "device %u: its in-links' sources have %llu in-links in total (limit %u)",
+                        d, (unsigned long long)cum, MAX_PAIRS);
+        dest_pairs[d] = (uint32_t)cum;
+    }
+    std::vector<uint32_t> rev(L, NONE32);
+    for (uint32_t l = 0; l < L; l++) {
+        auto it = seen.find(((uint64_t)link_dst[l] << 32) | link_src[l]);
+        if (it != seen.end()) rev[l] = it->second;
+    }
+    c->N = n_npus;
+    c->S = n_switches;
+    c->D = D;
+    c->L = L;
+    c->src.assign(link_src, link_src + L);
+    c->dst.assign(link_dst, link_dst + L);
+    c->alpha.assign(alpha_ns, alpha_ns + L);
+    c->bw.assign(bw_GBps, bw_GBps + L);
+    c->in_off.swap(in_off);
+    c->slot_link.swap(slot_link);
+    c->slot_src.swap(slot_src);
+    c->slot_cum.swap(slot_cum);
+    c->dest_pairs.swap(dest_pairs);
+    c->rev.swap(rev);
+    c->have_topo = true;
+    c->have_coll = c->have_ws = c->uploaded = c->have_result = false;
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_set_collective(pccl_ctx *c, uint32_t n_chunks, uint64_t chunk_bytes, const uint64_t *pre_bits,
+                                const uint64_t *post_bits, const uint64_t *group_masks, uint32_t n_groups,
+                                const uint16_t *chunk_group, pccl_op op)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    if (!c->have_topo) return fail(c, PCCL_ESTATE, "load a topology first");
+    if (chunk_bytes == 0) return fail(c, PCCL_EINVAL, "chunk size 0");
+    if (n_groups == 0 || !group_masks) return fail(c, PCCL_EINVAL, "no process group");
+    if (n_groups > 1 && !chunk_group) return fail(c, PCCL_EINVAL, "several groups need chunk_group");
+    if (n_groups > 65536) return fail(c, PCCL_EINVAL, "too many groups");
+    if (n_chunks && (!pre_bits || !post_bits)) return fail(c, PCCL_EINVAL, "null pre/post bitmap");
+    if (op != PCCL_OP_COPY && op != PCCL_OP_REDUCE_REVERSED && op != PCCL_OP_ALLREDUCE)
+        return fail(c, PCCL_EINVAL, "unknown op %d", (int)op);
+    if ((uint64_t)n_chunks + ROW_ALIGN_WORDS * 64ull >= 0xFFFFFFFFull)
+        return fail(c, PCCL_EUNSUPPORTED, "too many chunks");
+    const uint64_t WN = words(c->N);
+    for (uint32_t g = 0; g < n_groups; g++)
+        for (uint64_t v = c->N; v < WN * 64; v++)
+            if ((group_masks[g * WN + v / 64] >> (v % 64)) & 1ull)
+                return fail(c, PCCL_EINVAL, "group %u names a non-NPU", g);
+    std::vector<uint32_t> T(c->L);
+    uint32_t tmin = NONE32;
+    for (uint32_t l = 0; l < c->L; l++) {
+        const uint64_t beta = chunk_bytes / c->bw[l] + (chunk_bytes % c->bw[l] != 0);
+        const uint64_t t = (uint64_t)c->alpha[l] + beta;
+        if (beta > 0xFFFFFFFFull || t > 0xFFFFFFFFull)
+            return fail(c, PCCL_ERANGE, "link %u time does not fit in 32 bits", l);
+        T[l] = (uint32_t)t;
+        tmin = std::min(tmin, T[l]);
+    }
+    if (op != PCCL_OP_COPY) {
+        for (uint32_t l = 0; l < c->L; l++)
+            if (c->rev[l] == NONE32 || T[c->rev[l]] != T[l])
+                return fail(c, PCCL_EUNSUPPORTED, "link %u has no reverse link of equal time", l);
+    }
+    std::vector<uint32_t> slot_time(c->L);
+    for (uint32_t sl = 0; sl < c->L; sl++) slot_time[sl] = T[c->slot_link[sl]];
+    c->C = n_chunks;
+    c->m = chunk_bytes;
+    c->pre = pre_bits;
+    c->post = post_bits;
+    c->G = n_groups;
+    c->chunk_group = chunk_group;
+    c->gmask.assign(group_masks, group_masks + (size_t)n_groups * WN);
+    c->op = op;
+    c->T.swap(T);
+    c->slot_time.swap(slot_time);
+    c->tmin = c->L ? tmin : 1;
+    c->have_coll = true;
+    c->have_ws = c->uploaded = c->have_result = false;
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_workspace_bytes(pccl_ctx *c, uint64_t max_sends, size_t *out_bytes)
+{
+    if (!c || !out_bytes) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
+    Layout ly{};
+    Sizes sz{};
+    size_t total = 0;
+    carve(c, nullptr, max_sends ? max_sends : safe_max_sends(c), ly, sz, total);
+    *out_bytes = total;
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint64_t max_sends, void *hip_stream)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
+    if (!device_ptr) return fail(c, PCCL_EINVAL, "null workspace");
+    if (reinterpret_cast<uintptr_t>(device_ptr) & 255u) return fail(c, PCCL_EINVAL, "workspace not 256-byte aligned");
+    const uint64_t ms = max_sends ? max_sends : safe_max_sends(c);
+    Layout ly{};
+    Sizes sz{};
+    size_t need = 0;
+    carve(c, nullptr, ms, ly, sz, need);
+    if (bytes < need) return fail(c, PCCL_ENOMEM, "workspace has %zu bytes, needs %zu", bytes, need);
+    carve(c, static_cast<char *>(device_ptr), ms, c->ly, c->sz, need);
+    c->ws = static_cast<char *>(device_ptr);
+    c->ws_bytes = bytes;
+    c->max_sends = ms;
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    HIP_OR_FAIL(c, hipSetDevice(c->device));
+    c->grid = std::min<int>(match_max_grid(c->device), (int)std::max<uint32_t>(c->D, 1));
+    if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+    c->have_ws = true;
+    c->uploaded = c->have_result = false;
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+static pccl_status upload(pccl_ctx *c)
+{
+    const Layout &ly = c->ly;
+    hipStream_t st = c->stream;
+    auto put = [&](void *dst, const void *src, size_t bytes) -> hipError_t {
+        if (!bytes) return hipSuccess;
+        return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st);
+    };
+    const size_t L4 = sizeof(uint32_t) * c->L;
+    HIP_OR_FAIL(c, put(ly.lsrc, c->src.data(), L4));
+    HIP_OR_FAIL(c, put(ly.ldst, c->dst.data(), L4));
+    HIP_OR_FAIL(c, put(ly.ltime, c->T.data(), L4));
+    HIP_OR_FAIL(c, put(ly.lrev, c->rev.data(), L4));
+    HIP_OR_FAIL(c, put(ly.in_off, c->in_off.data(), sizeof(uint32_t) * (c->D + 1)));
+    HIP_OR_FAIL(c, put(ly.slot_link, c->slot_link.data(), L4));
+    HIP_OR_FAIL(c, put(ly.slot_src, c->slot_src.data(), L4));
+    HIP_OR_FAIL(c, put(ly.slot_time, c->slot_time.data(), L4));
+    HIP_OR_FAIL(c, put(ly.slot_cum, c->slot_cum.data(), L4));
+    HIP_OR_FAIL(c, put(ly.dest_pairs, c->dest_pairs.data(), sizeof(uint32_t) * c->D));
+    HIP_OR_FAIL(c, put(ly.group_masks, c->gmask.data(), sizeof(uint64_t) * c->gmask.size()));
+    HIP_OR_FAIL(c, hipStreamSynchronize(st));
+    c->uploaded = true;
+    return PCCL_OK;
+}
+
+static pccl_status device_error(pccl_ctx *c, const Control &h)
+{
+    switch (h.error) {
+    case ST_EINVAL:
+        return fail(c, PCCL_EINVAL, "%s (chunk %u, NPU %u)", einval_detail(h.error_arg[2]), h.error_arg[0],
+                    h.error_arg[1]);
+    case ST_EUNREACHABLE:
+        return fail(c, PCCL_EUNREACHABLE, "chunk %u: NPU %u is unreachable from NPU %u", h.error_arg[0],
+                    h.error_arg[1], h.error_arg[2]);
+    case ST_ERANGE:
+        return fail(c, PCCL_ERANGE, "chunk %u at device %u: %s does not fit in 32 bits", h.error_arg[0],
+                    h.error_arg[1], h.error_arg[2] == 1 ? "distance" : "time");
+    case ST_ENOMEM:
+        return fail(c, PCCL_ENOMEM, "collective needs %llu transfers, workspace holds %llu",
+                    (unsigned long long)h.needs_total, (unsigned long long)h.max_sends);
+    case ST_EDEADLOCK:
+        return fail(c, PCCL_EDEADLOCK, "%u deliveries remain but nothing is in flight", h.error_arg[0]);
+    default:
+        return fail(c, PCCL_EINTERNAL, "device error %u (%u %u %u)", h.error, h.error_arg[0], h.error_arg[1],
+                    h.error_arg[2]);
+    }
+}
+
+pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective_time_ns)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    c->have_result = false;
+    if (!c->have_ws) return fail(c, PCCL_ESTATE, "set a workspace first");
+    HIP_OR_FAIL(c, hipSetDevice(c->device));
+    if (!c->uploaded) {
+        pccl_status s = upload(c);
+        if (s != PCCL_OK) return s;
+    }
+    hipStream_t st = c->stream;
+    for (hipEvent_t &e : c->ev)
+        if (!e) HIP_OR_FAIL(c, hipEventCreate(&e));
+    HIP_OR_FAIL(c, hipEventRecord(c->ev[0], st));
+    HIP_OR_FAIL(c, launch_setup(c->ly, c->sz, c->pre, c->post, c->chunk_group, c->seed, st));
+    HIP_OR_FAIL(c, hipEventRecord(c->ev[1], st));
+    HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid));
+    HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
+    HIP_OR_FAIL(c, hipMemcpyAsync(&c->ctl_host, c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
+    HIP_OR_FAIL(c, hipStreamSynchronize(st));
+    const Control &h = c->ctl_host;
+    if (h.abort) return fail(c, PCCL_EINTERNAL, "matching kernel barrier timed out");
+    if (h.error) return device_error(c, h);
+    if (h.n_log != h.needs_total)
+        return fail(c, PCCL_EINTERNAL, "logged %llu transfers for %llu deliveries", (unsigned long long)h.n_log,
+                    (unsigned long long)h.needs_total);
+    const uint64_t n = h.n_log;
+    if (c->op == PCCL_OP_ALLREDUCE && 2ull * h.cstar > 0xFFFFFFFFull)
+        return fail(c, PCCL_ERANGE, "all-reduce time does not fit in 32 bits");
+    HIP_OR_FAIL(c, launch_output(c->ly, c->sz, c->op, n, st));
+    HIP_OR_FAIL(c, hipEventRecord(c->ev[3], st));
+    HIP_OR_FAIL(c, hipStreamSynchronize(st));
+    for (int i = 0; i < 3; i++) HIP_OR_FAIL(c, hipEventElapsedTime(&c->stage_ms[i], c->ev[i], c->ev[i + 1]));
+    c->n_copy = n;
+    c->n_sends = c->op == PCCL_OP_ALLREDUCE ? 2 * n : n;
+    c->coll_time = c->op == PCCL_OP_ALLREDUCE ? 2 * h.cstar : h.cstar;
+    c->have_result = true;
+    if (n_sends) *n_sends = c->n_sends;
+    if (collective_time_ns) *collective_time_ns = c->coll_time;
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_get_schedule(pccl_ctx *c, pccl_send *out, uint64_t capacity)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (capacity < c->n_sends) return fail(c, PCCL_EINVAL, "capacity %llu < %llu sends",
+                                          (unsigned long long)capacity, (unsigned long long)c->n_sends);
+    if (c->n_sends) {
+        if (!out) return fail(c, PCCL_EINVAL, "null output");
+        HIP_OR_FAIL(c, hipMemcpyAsync(out, c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDefault, c->stream));
+        HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+    }
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_get_stats(pccl_ctx *c, uint64_t *events, uint64_t *rounds, uint64_t *clashes, uint64_t *windows)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (rounds) *rounds = c->ctl_host.rounds;
+    if (clashes) *clashes = c->ctl_host.clashes;
+    if (windows) *windows = c->ctl_host.windows;
+    if (events) {
+        // time 0 plus every distinct transfer end up to the last transfer start,
+        // taken from the copy schedule
+        std::vector<pccl_send> s(c->n_sends);
+        if (c->n_sends) {
+            HIP_OR_FAIL(c, hipMemcpyAsync(s.data(), c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDeviceToHost,
+                                          c->stream));
+            HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+        }
+        const uint32_t cs = c->ctl_host.cstar;
+        std::vector<uint32_t> ends;
+        ends.reserve(c->n_copy);
+        uint32_t last = 0;
+        for (const pccl_send &x : s) {
+            uint32_t t = x.t_start_ns, l = x.link;
+            if (c->op == PCCL_OP_REDUCE_REVERSED) {
+                l = c->rev[x.link];
+                t = cs - x.t_start_ns - c->T[l];
+            } else if (c->op == PCCL_OP_ALLREDUCE) {
+                if (x.flags & PCCL_SEND_REDUCE) continue;
+                t -= cs;
+            }
+            last = std::max(last, t);
+            ends.push_back(t + c->T[l]);
+        }
+        std::sort(ends.begin(), ends.end());
+        ends.erase(std::unique(ends.begin(), ends.end()), ends.end());
+        uint64_t e = 1;
+        for (uint32_t x : ends)
+            if (x <= last) e++;
+        *events = e;
+    }
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_get_profile(pccl_ctx *c, double *setup_ms, double *match_ms, double *output_ms,
+                             uint64_t *scan_words)
+{
+    if (!c) return PCCL_EINVAL;
+    if (!c->have_result) return fail(c, PCCL_ESTATE, "no synthesis");
+    if (setup_ms) *setup_ms = c->stage_ms[0];
+    if (match_ms) *match_ms = c->stage_ms[1];
+    if (output_ms) *output_ms = c->stage_ms[2];
+    if (scan_words) *scan_words = c->ctl_host.scan_words;
+    return PCCL_OK;
+}
+
+pccl_status pccl_get_setup(pccl_ctx *c, uint32_t *link_time_ns, uint32_t *chunk_src, uint64_t *chunk_dist,
+                           uint32_t *chunk_rank)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!c->have_result) return fail(c, PCCL_ESTATE, "no synthesis");
+    if (link_time_ns && c->L) std::memcpy(link_time_ns, c->T.data(), sizeof(uint32_t) * c->L);
+    hipStream_t st = c->stream;
+    if (chunk_src && c->C)
+        HIP_OR_FAIL(c, hipMemcpyAsync(chunk_src, c->ly.chunk_src, sizeof(uint32_t) * c->C, hipMemcpyDeviceToHost, st));
+    if (chunk_dist && c->C)
+        HIP_OR_FAIL(c, hipMemcpyAsync(chunk_dist, c->ly.chunk_dist, sizeof(uint64_t) * c->C, hipMemcpyDeviceToHost, st));
+    if (chunk_rank && c->C)
+        HIP_OR_FAIL(c, hipMemcpyAsync(chunk_rank, c->ly.rank, sizeof(uint32_t) * c->C, hipMemcpyDeviceToHost, st));
+    HIP_OR_FAIL(c, hipStreamSynchronize(st));
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+}  // extern "C"

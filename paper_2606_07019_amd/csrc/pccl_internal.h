@@ -1,0 +1,133 @@
+// Internal definitions of the MI355X synthesis matcher (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pccl {
+
+constexpr uint32_t NONE32 = 0xFFFFFFFFu;
+constexpr uint64_t NONE64 = 0xFFFFFFFFFFFFFFFFull;
+
+// Row padding of the chunk bitmaps: 128 words (1 KiB), one wave64 sweep of
+// 16-byte loads, so a sweep never needs a tail check inside a row.
+constexpr uint32_t ROW_ALIGN_WORDS = 128;
+
+// Matching kernel envelope (checked on the host when a topology is loaded).
+constexpr uint32_t MATCH_THREADS = 256;   // one workgroup per destination device
+constexpr uint32_t MAX_IN_LINKS = 256;    // in-links of one device
+constexpr uint32_t MAX_PAIRS = 1024;      // sum over a device's in-links of their sources' in-degree
+constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
+
+// Status codes mirrored from the public header.
+enum : uint32_t {
+    ST_OK = 0, ST_EINVAL = 1, ST_EUNREACHABLE = 2, ST_ERANGE = 3, ST_ENOMEM = 4,
+    ST_EDEVICE = 5, ST_ESTATE = 6, ST_EUNSUPPORTED = 7, ST_EDEADLOCK = 8, ST_EINTERNAL = 9
+};
+
+// Device-side control block: error reporting, counters, window bookkeeping.
+struct Control {
+    uint32_t error;          // first error code recorded (0 = none)
+    uint32_t error_arg[3];   // chunk / device / detail of the first error
+    unsigned long long needs_total;      // (device, chunk) deliveries required
+    unsigned long long needs_remaining;  // still undelivered
+    unsigned long long n_log;            // sends logged so far
+    unsigned long long max_sends;        // capacity of the send log
+    unsigned long long rounds, clashes, windows;
+    unsigned long long scan_words;       // words of each row read by the intersect
+    uint32_t n_sources;      // distinct chunk sources
+    uint32_t barrier;        // grid barrier arrival counter (monotonic)
+    uint32_t abort;          // set when a barrier wait times out
+    uint32_t cstar;          // collective time of the copy schedule
+    // per-window slots, indexed by window number mod 3 so that a slot is
+    // never written while a slow workgroup may still read it
+    uint32_t win_t0[3];      // start of window k+1, accumulated by atomicMin in window k
+    uint32_t win_err[3];     // an error was recorded in window k
+    unsigned long long win_sent[3];  // transfers committed in window k
+    uint32_t sort_cur;       // radix sort: buffer holding the current order
+    uint32_t sort_src;       // radix sort: buffer read by the pending scatter
+    uint32_t sort_skip;      // radix sort: pending pass is a no-op
+    uint32_t pad[3];
+};
+
+__device__ inline void record_error(Control *ctl, uint32_t code, uint32_t a = 0, uint32_t b = 0,
+                                    uint32_t c = 0)
+{
+    if (atomicCAS(&ctl->error, 0u, code) == 0u) {
+        ctl->error_arg[0] = a;
+        ctl->error_arg[1] = b;
+        ctl->error_arg[2] = c;
+    }
+}
+
+__device__ inline uint64_t splitmix64_key(uint64_t seed, uint64_t c)
+{
+    // Output number c+1 of SplitMix64 started at state `seed`
+    // (Steele, Lea and Flood, "Fast splittable pseudorandom number
+    // generators", OOPSLA 2014): golden-gamma increment, then the
+    // variant-13 finalizer of the MurmurHash3 mixer.
+    uint64_t z = seed + (c + 1ull) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Pointers into the caller's workspace (all device memory).
+struct Layout {
+    // topology, link order
+    uint32_t *lsrc, *ldst, *ltime, *lrev;
+    // topology, destination-major "slot" order (in-links grouped by destination)
+    uint32_t *in_off;      // [D+1]
+    uint32_t *slot_link;   // [L] link id of slot
+    uint32_t *slot_src;    // [L] source device of slot
+    uint32_t *slot_time;   // [L]
+    uint32_t *slot_cum;    // [L] prefix of source in-degrees inside the destination
+    uint32_t *dest_pairs;  // [D] total of source in-degrees over the destination's in-links
+    uint64_t *group_masks; // [G * WN]
+    // chunk setup
+    uint32_t *chunk_src;   // [C]
+    uint32_t *holder_cnt;  // [C] bit 31: has a postcondition bit
+    uint64_t *chunk_dist;  // [C]
+    uint32_t *rank;        // [C] chunk -> priority position
+    uint32_t *order;       // [C] priority position -> chunk
+    uint32_t *src_index;   // [N] row of a source in the shortest-path tables
+    uint32_t *src_list;    // [N]
+    uint64_t *sp_dist;     // [N * D]
+    uint32_t *sp_parent;   // [N * D]
+    // sort buffers (chunk order first, then the send log)
+    uint64_t *skey[2];     // [max(C, 2*max_sends)]
+    uint32_t *sval[2];
+    uint32_t *hist;        // [256 * max_tiles]
+    // matching state
+    uint64_t *holds, *needs;  // [D * Wp]
+    uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
+    uint64_t *snap;           // [3 * L] by slot
+    // output
+    void *out;                // pccl_send [2 * max_sends]
+    Control *ctl;
+};
+
+struct Sizes {
+    uint32_t N, S, D, L, C, G;
+    uint64_t W;    // words per chunk row of the caller's pre/post bitmaps
+    uint64_t Wp;   // padded words per row of the device bitmaps
+    uint64_t WN;   // words per group mask
+    uint64_t max_sends;
+    uint32_t tmin; // smallest link time (window length)
+    uint32_t max_tiles;
+};
+
+// ---- launchers (each defined in the translation unit that holds its kernels)
+hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, const uint64_t *post,
+                        const uint16_t *chunk_group, uint64_t seed, hipStream_t st);
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
+int match_max_grid(int device);
+hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st);
+// LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;
+// the sorted order ends up in buffer ly.ctl->sort_cur (read it on the device).
+hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_hi, uint32_t max_tiles,
+                            bool reset_cur, hipStream_t st);
+constexpr uint32_t SORT_TILE = 4096;      // elements per radix-sort tile
+constexpr uint32_t SORT_THREADS = 256;
+
+}  // namespace pccl

@@ -1,0 +1,317 @@
+// Setup of one synthesis on the device: conditions from the pre/postcondition
+// bitmaps, shortest-path trees from every chunk source, condition distances,
+// the priority order, relay devices and the initial holds/needs bitmaps over
+// priority-ordered columns.
+#include "pccl_internal.h"
+
+namespace pccl {
+namespace {
+
+constexpr uint32_t FLAG_POST = 0x80000000u;  // holder_cnt: chunk has a postcondition bit
+constexpr uint32_t CNT_MASK = 0x7FFFFFFFu;
+
+// detail codes carried in error_arg[2] for PCCL_EINVAL
+enum : uint32_t { BAD_TAIL = 1, BAD_MEMBER = 2, BAD_GROUP = 3, TWO_HOLDERS = 4, NO_HOLDER = 5 };
+
+__global__ void k_fill32(uint32_t *p, uint64_t n, uint32_t v)
+{
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void k_fill64(uint64_t *p, uint64_t n, uint64_t v)
+{
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void k_ctl_reset(Control *ctl, unsigned long long max_sends)
+{
+    Control c = {};
+    c.max_sends = max_sends;
+    c.win_t0[0] = 0;
+    c.win_t0[1] = NONE32;
+    c.win_t0[2] = NONE32;
+    *ctl = c;
+}
+
+// Mask of valid bits in word k of a chunk row.
+__device__ inline uint64_t tail_mask(uint64_t k, const Sizes &sz)
+{
+    if (k + 1 < sz.W || (sz.C & 63u) == 0) return NONE64;
+    return (1ull << (sz.C & 63u)) - 1ull;
+}
+
+// Conditions (Sec. 4.1): for every set bit of the NPU-centric bitmaps,
+// count precondition holders per chunk, mark chunks that are needed
+// somewhere, and check that pre/post bits sit on members of the chunk's
+// process group.  Grid: x over words, y over NPU rows.
+__global__ void k_conditions(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t *post,
+                             const uint16_t *cg)
+{
+    const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t v = blockIdx.y;
+    if (k >= sz.W) return;
+    const uint64_t p = pre[(uint64_t)v * sz.W + k], q = post[(uint64_t)v * sz.W + k];
+    if (!(p | q)) return;
+    const uint64_t tm = tail_mask(k, sz);
+    if ((p | q) & ~tm) record_error(ly.ctl, ST_EINVAL, sz.C, v, BAD_TAIL);
+    for (uint64_t x = (p | q) & tm; x; x &= x - 1) {
+        const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+        const uint32_t g = cg ? cg[c] : 0u;
+        if (g >= sz.G) {
+            record_error(ly.ctl, ST_EINVAL, c, v, BAD_GROUP);
+            continue;
+        }
+        if (!((ly.group_masks[(uint64_t)g * sz.WN + (v >> 6)] >> (v & 63)) & 1ull))
+            record_error(ly.ctl, ST_EINVAL, c, v, BAD_MEMBER);
+    }
+    for (uint64_t x = p & tm; x; x &= x - 1) {
+        const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+        const uint32_t old = atomicAdd(&ly.holder_cnt[c], 1u);
+        if (old & CNT_MASK)
+            record_error(ly.ctl, ST_EINVAL, c, v, TWO_HOLDERS);
+        else
+            ly.chunk_src[c] = v;
+    }
+    for (uint64_t x = q & tm; x; x &= x - 1) {
+        const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+        atomicOr(&ly.holder_cnt[c], FLAG_POST);
+    }
+}
+
+__global__ void k_chunk_check(Layout ly, Sizes sz)
+{
+    const uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= sz.C) return;
+    const uint32_t h = ly.holder_cnt[c];
+    if ((h & FLAG_POST) && !(h & CNT_MASK)) record_error(ly.ctl, ST_EINVAL, (uint32_t)c, 0, NO_HOLDER);
+    if ((h & CNT_MASK) == 1u) ly.src_index[ly.chunk_src[c]] = 1u;
+}
+
+// Distinct sources -> dense rows of the shortest-path tables (one workgroup).
+__global__ void __launch_bounds__(1024) k_compact_sources(Layout ly, Sizes sz)
+{
+    __shared__ uint32_t part[1024];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t per = (sz.N + 1023) / 1024;
+    const uint32_t lo = tid * per, hi = min(lo + per, sz.N);
+    uint32_t s = 0;
+    for (uint32_t v = lo; v < hi; v++) s += ly.src_index[v];
+    part[tid] = s;
+    __syncthreads();
+    for (uint32_t off = 1; off < 1024; off <<= 1) {
+        uint32_t x = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += x;
+        __syncthreads();
+    }
+    uint32_t run = tid ? part[tid - 1] : 0;
+    for (uint32_t v = lo; v < hi; v++) {
+        if (ly.src_index[v]) {
+            ly.src_list[run] = v;
+            ly.src_index[v] = run++;
+        } else {
+            ly.src_index[v] = NONE32;
+        }
+    }
+    if (tid == 1023) ly.ctl->n_sources = part[1023];
+}
+
+// Shortest paths from one source per workgroup (Alg. 3 ShortestPath over
+// the alpha-beta link times): Bellman-Ford relaxation with the distances in
+// LDS, then the parent of each device = the smallest-id in-neighbour on a
+// shortest path (the tree the pruned BFS of Sec. 4.3 keeps).
+__global__ void __launch_bounds__(256) k_shortest_paths(Layout ly, Sizes sz)
+{
+    extern __shared__ unsigned long long dist[];
+    __shared__ uint32_t changed;
+    const uint32_t b = blockIdx.x, tid = threadIdx.x;
+    if (b >= ly.ctl->n_sources || ly.ctl->error) return;
+    const uint32_t s = ly.src_list[b];
+    for (uint32_t v = tid; v < sz.D; v += blockDim.x) dist[v] = v == s ? 0ull : NONE64;
+    __syncthreads();
+    for (uint32_t it = 0; it < sz.D; it++) {
+        if (tid == 0) changed = 0;
+        __syncthreads();
+        for (uint32_t e = tid; e < sz.L; e += blockDim.x) {
+            const unsigned long long du = dist[ly.lsrc[e]];
+            if (du == NONE64) continue;
+            const unsigned long long nd = du + ly.ltime[e];
+            const uint32_t v = ly.ldst[e];
+            if (nd < dist[v]) {
+                atomicMin(&dist[v], nd);
+                changed = 1;
+            }
+        }
+        __syncthreads();
+        const uint32_t again = changed;
+        __syncthreads();
+        if (!again) break;
+    }
+    for (uint32_t v = tid; v < sz.D; v += blockDim.x) {
+        const unsigned long long dv = dist[v];
+        ly.sp_dist[(uint64_t)b * sz.D + v] = dv;
+        uint32_t par = NONE32;
+        if (v != s && dv != NONE64) {
+            for (uint32_t i = ly.in_off[v]; i < ly.in_off[v + 1]; i++) {
+                const uint32_t u = ly.slot_src[i];
+                const unsigned long long du = dist[u];
+                if (du != NONE64 && du + ly.slot_time[i] == dv && u < par) par = u;
+            }
+        }
+        ly.sp_parent[(uint64_t)b * sz.D + v] = par;
+    }
+}
+
+// Condition distance = max over destinations of the shortest-path distance
+// (Alg. 3); destinations = postcondition and not precondition.
+__global__ void k_chunk_dist(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t *post)
+{
+    if (ly.ctl->error) return;
+    const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t v = blockIdx.y;
+    if (k >= sz.W) return;
+    const uint64_t x0 = post[(uint64_t)v * sz.W + k] & ~pre[(uint64_t)v * sz.W + k] & tail_mask(k, sz);
+    for (uint64_t x = x0; x; x &= x - 1) {
+        const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+        const uint32_t row = ly.src_index[ly.chunk_src[c]];
+        const unsigned long long dv = ly.sp_dist[(uint64_t)row * sz.D + v];
+        if (dv == NONE64)
+            record_error(ly.ctl, ST_EUNREACHABLE, c, v, ly.chunk_src[c]);
+        else if (dv >= 0xFFFFFFFFull)
+            record_error(ly.ctl, ST_ERANGE, c, v, 1);
+        else
+            atomicMax(&ly.chunk_dist[c], dv);
+    }
+}
+
+__global__ void k_keys_hash(Layout ly, Sizes sz, uint64_t seed)
+{
+    const uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= sz.C) return;
+    ly.skey[0][c] = splitmix64_key(seed, c);
+    ly.sval[0][c] = (uint32_t)c;
+}
+
+// After the stable sort by tie-break key: key = bitwise-not of the distance,
+// so an ascending stable sort gives distance descending, ties by key.
+__global__ void k_keys_dist(Layout ly, Sizes sz)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= sz.C) return;
+    const uint32_t cur = ly.ctl->sort_cur;
+    const uint32_t c = ly.sval[cur][i];
+    ly.skey[cur][i] = (uint64_t)(~(uint32_t)ly.chunk_dist[c]);
+}
+
+__global__ void k_rank(Layout ly, Sizes sz)
+{
+    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= sz.C) return;
+    const uint32_t c = ly.sval[ly.ctl->sort_cur][r];
+    ly.order[r] = c;
+    ly.rank[c] = (uint32_t)r;
+}
+
+__global__ void k_holds(Layout ly, Sizes sz)
+{
+    if (ly.ctl->error) return;
+    const uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= sz.C) return;
+    if ((ly.holder_cnt[c] & CNT_MASK) != 1u) return;
+    const uint32_t r = ly.rank[c];
+    atomicOr((unsigned long long *)&ly.holds[(uint64_t)ly.chunk_src[c] * sz.Wp + (r >> 6)], 1ull << (r & 63));
+}
+
+// needs = destinations plus the relays on their tree paths (the paths the
+// pruned BFS keeps, Sec. 4.3): walk parents from each destination up to the
+// source; a walk stops at a device whose bit another walk already set.
+__global__ void k_needs(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t *post)
+{
+    if (ly.ctl->error) return;
+    const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t v = blockIdx.y;
+    unsigned long long added = 0;
+    if (k < sz.W) {
+        const uint64_t x0 = post[(uint64_t)v * sz.W + k] & ~pre[(uint64_t)v * sz.W + k] & tail_mask(k, sz);
+        for (uint64_t x = x0; x; x &= x - 1) {
+            const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+            const uint32_t s = ly.chunk_src[c], row = ly.src_index[s], r = ly.rank[c];
+            const uint64_t bit = 1ull << (r & 63);
+            const uint32_t *par = ly.sp_parent + (uint64_t)row * sz.D;
+            uint32_t u = v;
+            for (uint32_t hop = 0; hop < sz.D && u != s && u < sz.D; hop++) {
+                const unsigned long long old =
+                    atomicOr((unsigned long long *)&ly.needs[(uint64_t)u * sz.Wp + (r >> 6)], bit);
+                if (old & bit) break;
+                added++;
+                u = par[u];
+            }
+        }
+    }
+    for (int off = 32; off; off >>= 1) added += __shfl_xor(added, off);
+    if ((threadIdx.x & 63) == 0 && added) atomicAdd(&ly.ctl->needs_total, added);
+}
+
+__global__ void k_init_match(Layout ly, Sizes sz)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < sz.L) {
+        ly.busy[i] = 0;
+        ly.infl[i] = NONE32;
+        ly.cur[i] = 0;
+        ly.lflags[i] = 0;
+        ly.snap[i] = NONE64;
+        ly.snap[sz.L + i] = NONE64;
+        ly.snap[2ull * sz.L + i] = NONE64;
+    }
+    if (i == 0) {
+        Control *ctl = ly.ctl;
+        ctl->needs_remaining = ctl->needs_total;
+        if (!ctl->error && ctl->needs_total > ctl->max_sends)
+            record_error(ctl, ST_ENOMEM, (uint32_t)(ctl->needs_total >> 32), (uint32_t)ctl->needs_total, 0);
+    }
+}
+
+inline uint32_t blocks_for(uint64_t n, uint32_t t) { return (uint32_t)((n + t - 1) / t); }
+
+}  // namespace
+
+hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, const uint64_t *post,
+                        const uint16_t *chunk_group, uint64_t seed, hipStream_t st)
+{
+    const uint32_t T = 256;
+    k_ctl_reset<<<1, 1, 0, st>>>(ly.ctl, sz.max_sends);
+    const uint64_t C = sz.C;
+    if (C) {
+        k_fill32<<<min(blocks_for(C, T), 4096u), T, 0, st>>>(ly.holder_cnt, C, 0);
+        k_fill32<<<min(blocks_for(C, T), 4096u), T, 0, st>>>(ly.chunk_src, C, NONE32);
+        k_fill64<<<min(blocks_for(C, T), 4096u), T, 0, st>>>(ly.chunk_dist, C, 0);
+    }
+    k_fill32<<<blocks_for(sz.N, T), T, 0, st>>>(ly.src_index, sz.N, 0);
+    const uint64_t bm = (uint64_t)sz.D * sz.Wp;
+    k_fill64<<<min(blocks_for(bm, T), 8192u), T, 0, st>>>(ly.holds, bm, 0);
+    k_fill64<<<min(blocks_for(bm, T), 8192u), T, 0, st>>>(ly.needs, bm, 0);
+    const dim3 gw(blocks_for(sz.W ? sz.W : 1, T), sz.N);
+    if (sz.W) k_conditions<<<gw, T, 0, st>>>(ly, sz, pre, post, chunk_group);
+    if (C) k_chunk_check<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
+    k_compact_sources<<<1, 1024, 0, st>>>(ly, sz);
+    k_shortest_paths<<<sz.N, 256, sizeof(unsigned long long) * sz.D, st>>>(ly, sz);
+    if (sz.W) k_chunk_dist<<<gw, T, 0, st>>>(ly, sz, pre, post);
+    if (C) {
+        k_keys_hash<<<blocks_for(C, T), T, 0, st>>>(ly, sz, seed);
+        hipError_t e = radix_sort_pairs(ly, C, 0, 8, sz.max_tiles, true, st);
+        if (e != hipSuccess) return e;
+        k_keys_dist<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
+        e = radix_sort_pairs(ly, C, 0, 4, sz.max_tiles, false, st);
+        if (e != hipSuccess) return e;
+        k_rank<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
+        k_holds<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
+    }
+    if (sz.W) k_needs<<<gw, T, 0, st>>>(ly, sz, pre, post);
+    k_init_match<<<blocks_for(sz.L ? sz.L : 1, T), T, 0, st>>>(ly, sz);
+    return hipGetLastError();
+}
+
+}  // namespace pccl

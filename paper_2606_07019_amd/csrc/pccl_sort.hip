@@ -1,0 +1,221 @@
+// Stable LSD radix sort of (uint64 key, uint32 value) pairs and the
+// schedule output pass (canonical order, caller chunk ids, reductions).
+#include "pccl_internal.h"
+
+namespace pccl {
+namespace {
+
+// Per-tile digit histogram, stored digit-major: hist[digit * tiles + tile].
+__global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles)
+{
+    __shared__ uint32_t cnt[256];
+    const uint32_t tid = threadIdx.x, tile = blockIdx.x;
+    cnt[tid] = 0;
+    __syncthreads();
+    const uint64_t *key = ly.skey[ly.ctl->sort_cur];
+    const uint64_t base = (uint64_t)tile * SORT_TILE;
+    for (uint32_t e = tid; e < SORT_TILE; e += SORT_THREADS) {
+        uint64_t i = base + e;
+        if (i < n) atomicAdd(&cnt[(key[i] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    ly.hist[(uint64_t)tid * tiles + tile] = cnt[tid];
+}
+
+// Exclusive scan of the histogram (one workgroup), and the skip decision:
+// a pass whose digit is the same for every element is a no-op.
+__global__ void __launch_bounds__(1024) k_scan(Layout ly, uint64_t n, uint32_t tiles)
+{
+    __shared__ uint32_t part[1024];
+    const uint32_t tid = threadIdx.x;
+    const uint64_t total = 256ull * tiles;
+    const uint64_t per = (total + 1023) / 1024;
+    const uint64_t lo = tid * per, hi = lo + per < total ? lo + per : total;
+    uint32_t s = 0;
+    for (uint64_t i = lo; i < hi; i++) s += ly.hist[i];
+    part[tid] = s;
+    __syncthreads();
+    for (uint32_t off = 1; off < 1024; off <<= 1) {
+        uint32_t v = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    uint32_t run = tid ? part[tid - 1] : 0;
+    for (uint64_t i = lo; i < hi; i++) {
+        uint32_t v = ly.hist[i];
+        ly.hist[i] = run;
+        run += v;
+    }
+    __syncthreads();
+    __shared__ uint32_t skip;
+    if (tid == 0) skip = 0;
+    __syncthreads();
+    if (tid < 256) {
+        uint32_t start = ly.hist[(uint64_t)tid * tiles];
+        uint32_t end = tid < 255 ? ly.hist[(uint64_t)(tid + 1) * tiles] : (uint32_t)n;
+        if (end - start == (uint32_t)n) skip = 1;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t cur = ly.ctl->sort_cur;
+        ly.ctl->sort_src = cur;
+        ly.ctl->sort_skip = skip;
+        ly.ctl->sort_cur = skip ? cur : cur ^ 1u;
+    }
+}
+
+// Stable scatter: a tile is consumed in order, 256 elements at a time; the
+// rank of an element among equal digits of its wave comes from 8 ballots
+// (one per digit bit), the offset of its wave from LDS counts.
+__global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n, int shift, uint32_t tiles)
+{
+    if (ly.ctl->sort_skip) return;
+    __shared__ uint32_t run[256];
+    __shared__ uint32_t wc[SORT_THREADS / 64][256];
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, tile = blockIdx.x;
+    const uint32_t src = ly.ctl->sort_src;
+    const uint64_t *kin = ly.skey[src];
+    const uint32_t *vin = ly.sval[src];
+    uint64_t *kout = ly.skey[src ^ 1u];
+    uint32_t *vout = ly.sval[src ^ 1u];
+    run[tid] = ly.hist[(uint64_t)tid * tiles + tile];
+    for (uint32_t w = 0; w < SORT_THREADS / 64; w++) wc[w][tid] = 0;
+    __syncthreads();
+    const uint64_t base = (uint64_t)tile * SORT_TILE;
+    const uint64_t lt = (1ull << lane) - 1ull;
+    for (uint32_t e0 = 0; e0 < SORT_TILE; e0 += SORT_THREADS) {
+        const uint64_t i = base + e0 + tid;
+        const bool valid = i < n;
+        uint64_t k = 0;
+        uint32_t v = 0, dg = 0;
+        if (valid) {
+            k = kin[i];
+            v = vin[i];
+            dg = (uint32_t)(k >> shift) & 255u;
+        }
+        uint64_t same = __ballot(valid);
+        for (int b = 0; b < 8; b++) {
+            const bool bit = (dg >> b) & 1u;
+            const uint64_t bb = __ballot(bit);
+            same &= bit ? bb : ~bb;
+        }
+        const uint32_t r = __popcll(same & lt);
+        if (valid && r == 0) wc[wave][dg] = __popcll(same);
+        __syncthreads();
+        if (valid) {
+            uint32_t pre = run[dg];
+            for (uint32_t w = 0; w < wave; w++) pre += wc[w][dg];
+            const uint32_t dst = pre + r;
+            kout[dst] = k;
+            vout[dst] = v;
+        }
+        __syncthreads();
+        uint32_t add = 0;
+        for (uint32_t w = 0; w < SORT_THREADS / 64; w++) {
+            add += wc[w][tid];
+            wc[w][tid] = 0;
+        }
+        run[tid] += add;
+        __syncthreads();
+        if (base + e0 + SORT_THREADS >= n) break;
+    }
+}
+
+__global__ void k_sort_reset(Layout ly) { ly.ctl->sort_cur = 0; }
+
+// Send log -> schedule.  Log key = t_start << 32 | link, value = rank.
+// `add_cstar` shifts start times by the copy schedule's collective time
+// (the All-Gather half of an All-Reduce).
+__global__ void k_out_copy(Layout ly, uint64_t n, uint64_t out_off, uint32_t add_cstar, uint32_t flags)
+{
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint32_t cur = ly.ctl->sort_cur;
+    const uint64_t k = ly.skey[cur][i];
+    const uint32_t r = ly.sval[cur][i];
+    uint4 rec;
+    rec.x = (uint32_t)k;
+    rec.y = ly.order[r];
+    rec.z = (uint32_t)(k >> 32) + (add_cstar ? ly.ctl->cstar : 0u);
+    rec.w = flags;
+    reinterpret_cast<uint4 *>(ly.out)[out_off + i] = rec;
+}
+
+// Forward log -> time-reversed keys (in place in the current buffer):
+// (l, c, t) -> (reverse(l), c, C* - t - T[l]).
+__global__ void k_reverse_keys(Layout ly, uint64_t n)
+{
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint32_t cur = ly.ctl->sort_cur;
+    const uint64_t k = ly.skey[cur][i];
+    const uint32_t l = (uint32_t)k, t = (uint32_t)(k >> 32);
+    const uint32_t tr = ly.ctl->cstar - t - ly.ltime[l];
+    ly.skey[cur][i] = ((uint64_t)tr << 32) | ly.lrev[l];
+}
+
+}  // namespace
+
+hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_hi, uint32_t max_tiles,
+                            bool reset_cur, hipStream_t st)
+{
+    if (reset_cur) {
+        k_sort_reset<<<1, 1, 0, st>>>(ly);
+    }
+    if (n == 0) return hipGetLastError();
+    const uint32_t tiles = (uint32_t)((n + SORT_TILE - 1) / SORT_TILE);
+    if (tiles > max_tiles) return hipErrorInvalidValue;
+    for (int b = byte_lo; b < byte_hi; b++) {
+        k_hist<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
+        k_scan<<<1, 1024, 0, st>>>(ly, n, tiles);
+        k_scatter<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
+    }
+    return hipGetLastError();
+}
+
+static int bytes_for(uint64_t maxval)
+{
+    int b = 0;
+    while (maxval) {
+        b++;
+        maxval >>= 8;
+    }
+    return b ? b : 1;
+}
+
+// Output stage: the send log (n entries, key t_start << 32 | link, value
+// rank) is in sort buffer 0.  Writes the canonical schedule to ly.out.
+hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st)
+{
+    const int link_bytes = bytes_for(sz.L ? sz.L - 1 : 0);
+    const int threads = 256;
+    const uint64_t blocks = (n + threads - 1) / threads;
+    hipError_t e;
+    if (op == 0 || op == 2) {
+        // forward schedule sorted by (t_start, link)
+        e = radix_sort_pairs(ly, n, 0, link_bytes, sz.max_tiles, true, st);
+        if (e != hipSuccess) return e;
+        e = radix_sort_pairs(ly, n, 4, 8, sz.max_tiles, false, st);
+        if (e != hipSuccess) return e;
+        if (n) {
+            if (op == 0)
+                k_out_copy<<<blocks, threads, 0, st>>>(ly, n, 0, 0, 0);
+            else
+                k_out_copy<<<blocks, threads, 0, st>>>(ly, n, n, 1, 0);
+        }
+    } else {
+        k_sort_reset<<<1, 1, 0, st>>>(ly);
+    }
+    if (op == 1 || op == 2) {
+        if (n) k_reverse_keys<<<blocks, threads, 0, st>>>(ly, n);
+        e = radix_sort_pairs(ly, n, 0, link_bytes, sz.max_tiles, false, st);
+        if (e != hipSuccess) return e;
+        e = radix_sort_pairs(ly, n, 4, 8, sz.max_tiles, false, st);
+        if (e != hipSuccess) return e;
+        if (n) k_out_copy<<<blocks, threads, 0, st>>>(ly, n, 0, 0, 1);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace pccl

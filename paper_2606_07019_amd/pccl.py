@@ -1,0 +1,237 @@
+"""Thin ctypes binding of libpccl.so (the C ABI in include/pccl.h).
+
+Argument marshalling only: every step of the synthesis runs in the library's
+HIP kernels.  PyTorch provides device memory (the workspace and the device
+copies of the bitmaps) and the stream.  There is no fallback: if the library
+is not built, or no GPU is present, the calls raise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpccl.so")
+
+STATUS = {0: "PCCL_OK", 1: "PCCL_EINVAL", 2: "PCCL_EUNREACHABLE", 3: "PCCL_ERANGE",
+          4: "PCCL_ENOMEM", 5: "PCCL_EDEVICE", 6: "PCCL_ESTATE", 7: "PCCL_EUNSUPPORTED",
+          8: "PCCL_EDEADLOCK", 9: "PCCL_EINTERNAL"}
+
+PCCL_OP_COPY = 0
+PCCL_OP_REDUCE_REVERSED = 1
+PCCL_OP_ALLREDUCE = 2
+
+
+class PcclError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+class pccl_send(ctypes.Structure):
+    _fields_ = [("link", ctypes.c_uint32), ("chunk", ctypes.c_uint32),
+                ("t_start_ns", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libpccl.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2606_07019_amd.build.build()")
+    lib = ctypes.CDLL(path)
+    P, U32, U64, I = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    sig = {
+        "pccl_create": ([PP, I, U64], I),
+        "pccl_destroy": ([P], None),
+        "pccl_load_topology": ([P, U32, U32, U32, P, P, P, P], I),
+        "pccl_set_collective": ([P, U32, U64, P, P, P, U32, P, I], I),
+        "pccl_workspace_bytes": ([P, U64, ctypes.POINTER(ctypes.c_size_t)], I),
+        "pccl_set_workspace": ([P, P, ctypes.c_size_t, U64, P], I),
+        "pccl_synthesize": ([P, ctypes.POINTER(U64), ctypes.POINTER(U32)], I),
+        "pccl_get_schedule": ([P, P, U64], I),
+        "pccl_get_stats": ([P, ctypes.POINTER(U64), ctypes.POINTER(U64), ctypes.POINTER(U64),
+                            ctypes.POINTER(U64)], I),
+        "pccl_get_setup": ([P, P, P, P, P], I),
+        "pccl_get_profile": ([P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                              ctypes.POINTER(ctypes.c_double), ctypes.POINTER(U64)], I),
+        "pccl_last_error": ([P], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _np_ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(h, st: int):
+    if st != 0:
+        msg = load_library().pccl_last_error(h)
+        raise PcclError(st, msg.decode() if msg else "")
+
+
+# ---- the C ABI, name for name ------------------------------------------------
+
+def pccl_create(hip_device: int = 0, tie_seed: int = 0) -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    st = load_library().pccl_create(ctypes.byref(h), hip_device, tie_seed & ((1 << 64) - 1))
+    if st != 0:
+        raise PcclError(st, f"cannot create a context on HIP device {hip_device}")
+    return h
+
+
+def pccl_destroy(h) -> None:
+    load_library().pccl_destroy(h)
+
+
+def pccl_last_error(h) -> str:
+    m = load_library().pccl_last_error(h)
+    return m.decode() if m else ""
+
+
+def pccl_load_topology(h, n_npus, n_switches, link_src, link_dst, alpha_ns, bw_GBps) -> None:
+    arrs = [np.ascontiguousarray(a, dtype=np.uint32) for a in (link_src, link_dst, alpha_ns, bw_GBps)]
+    L = int(arrs[0].shape[0])
+    _check(h, load_library().pccl_load_topology(h, n_npus, n_switches, L, *[_np_ptr(a) for a in arrs]))
+
+
+def pccl_set_collective(h, n_chunks, chunk_bytes, pre_bits_dev_ptr, post_bits_dev_ptr,
+                        group_masks, chunk_group_dev_ptr, op) -> None:
+    """pre/post/chunk_group are DEVICE pointers (ints); group_masks a host array."""
+    gm = np.ascontiguousarray(group_masks, dtype=np.uint64)
+    if gm.ndim == 1:
+        gm = gm[None, :]
+    _check(h, load_library().pccl_set_collective(
+        h, n_chunks, chunk_bytes, pre_bits_dev_ptr, post_bits_dev_ptr, _np_ptr(gm), gm.shape[0],
+        chunk_group_dev_ptr, op))
+
+
+def pccl_workspace_bytes(h, max_sends: int = 0) -> int:
+    out = ctypes.c_size_t()
+    _check(h, load_library().pccl_workspace_bytes(h, max_sends, ctypes.byref(out)))
+    return int(out.value)
+
+
+def pccl_set_workspace(h, device_ptr: int, nbytes: int, max_sends: int = 0, stream_ptr: int = 0) -> None:
+    _check(h, load_library().pccl_set_workspace(h, device_ptr, nbytes, max_sends, stream_ptr or None))
+
+
+def pccl_synthesize(h):
+    n = ctypes.c_uint64()
+    t = ctypes.c_uint32()
+    _check(h, load_library().pccl_synthesize(h, ctypes.byref(n), ctypes.byref(t)))
+    return int(n.value), int(t.value)
+
+
+def pccl_get_schedule(h, out_ptr: int, capacity: int) -> None:
+    _check(h, load_library().pccl_get_schedule(h, out_ptr, capacity))
+
+
+def pccl_get_stats(h) -> dict:
+    v = [ctypes.c_uint64() for _ in range(4)]
+    _check(h, load_library().pccl_get_stats(h, *[ctypes.byref(x) for x in v]))
+    return dict(zip(["events", "rounds", "clashes", "windows"], [int(x.value) for x in v]))
+
+
+def pccl_get_profile(h) -> dict:
+    d = [ctypes.c_double() for _ in range(3)]
+    w = ctypes.c_uint64()
+    _check(h, load_library().pccl_get_profile(h, *[ctypes.byref(x) for x in d], ctypes.byref(w)))
+    return {"setup_ms": d[0].value, "match_ms": d[1].value, "output_ms": d[2].value,
+            "scan_words": int(w.value)}
+
+
+def pccl_get_setup(h, n_links: int, n_chunks: int):
+    T = np.zeros(n_links, np.uint32)
+    src = np.zeros(n_chunks, np.uint32)
+    dist = np.zeros(n_chunks, np.uint64)
+    rank = np.zeros(n_chunks, np.uint32)
+    _check(h, load_library().pccl_get_setup(h, _np_ptr(T), _np_ptr(src), _np_ptr(dist), _np_ptr(rank)))
+    return T, src, dist, rank
+
+
+# ---- convenience wrapper (marshalling of a whole workload) --------------------
+
+class Synthesizer:
+    """Owns a context, the device copies of the bitmaps and the workspace.
+
+    `topo` / `coll` follow paper_2606_07019_amd.workloads (numpy arrays)."""
+
+    def __init__(self, topo, coll, tie_seed: int = 0, device: int = 0, max_sends: int = 0,
+                 stream=None):
+        import torch
+        self.torch = torch
+        self.dev = torch.device("cuda", device)
+        self.topo, self.coll = topo, coll
+        self.h = pccl_create(device, tie_seed)
+        pccl_load_topology(self.h, topo.n_npus, topo.n_switches, topo.src, topo.dst,
+                           topo.alpha_ns, topo.bw_GBps)
+        self.pre = torch.from_numpy(coll.pre.view(np.int64).copy()).to(self.dev)
+        self.post = torch.from_numpy(coll.post.view(np.int64).copy()).to(self.dev)
+        self.cg = None
+        if coll.chunk_group is not None:
+            self.cg = torch.from_numpy(coll.chunk_group.astype(np.int16).copy()).to(self.dev)
+        pccl_set_collective(self.h, coll.n_chunks, coll.chunk_bytes, self.pre.data_ptr(),
+                            self.post.data_ptr(), coll.group_masks,
+                            None if self.cg is None else self.cg.data_ptr(), coll.op)
+        self.max_sends = max_sends
+        nbytes = pccl_workspace_bytes(self.h, max_sends)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=self.dev)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.dev)
+        pccl_set_workspace(self.h, self.ws.data_ptr(), nbytes, max_sends, self.stream.cuda_stream)
+        self.n_sends = None
+        self.collective_time = None
+
+    def synthesize(self):
+        self.n_sends, self.collective_time = pccl_synthesize(self.h)
+        return self.n_sends, self.collective_time
+
+    def schedule(self) -> np.ndarray:
+        """(S, 4) uint32: link, chunk, t_start_ns, flags in canonical order."""
+        n = self.n_sends or 0
+        out = np.zeros((n, 4), dtype=np.uint32)
+        if n:
+            pccl_get_schedule(self.h, out.ctypes.data, n)
+        return out
+
+    def schedule_device(self):
+        n = self.n_sends or 0
+        out = self.torch.empty((max(n, 1), 4), dtype=self.torch.int32, device=self.dev)
+        if n:
+            pccl_get_schedule(self.h, out.data_ptr(), n)
+        return out[:n]
+
+    def stats(self) -> dict:
+        return pccl_get_stats(self.h)
+
+    def profile(self) -> dict:
+        return pccl_get_profile(self.h)
+
+    def setup(self):
+        return pccl_get_setup(self.h, self.topo.n_links, self.coll.n_chunks)
+
+    def close(self):
+        if self.h is not None:
+            pccl_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

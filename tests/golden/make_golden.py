@@ -1,0 +1,61 @@
+"""Writes tests/golden/config<k>.json from the CPU oracle (and nothing else).
+
+Each file holds, for one of the five benchmark-shaped workloads, the
+oracle's transfer count, collective time, statistics, the SHA-256 of its
+canonical schedule (uint32 little-endian rows: link, chunk, t_start, flags)
+and 512 evenly spaced schedule rows, so GPU tests at full size can compare
+element by element on the samples and bit-exactly through the digest.
+
+    python tests/golden/make_golden.py [k ...]
+"""
+
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+from oracle import oracle as O  # noqa: E402
+from paper_2606_07019_amd import workloads as W  # noqa: E402
+
+N_SAMPLES = 512
+
+
+def digest(sends: np.ndarray) -> str:
+    return hashlib.sha256(np.ascontiguousarray(sends, dtype="<u4").tobytes()).hexdigest()
+
+
+def make(k: int) -> dict:
+    wl = W.CONFIGS[k]()
+    t0 = time.time()
+    r = O.run_workload(wl)
+    dt = time.time() - t0
+    assert r.status == 0, r.message
+    n = len(r.sends)
+    idx = np.unique(np.linspace(0, max(n - 1, 0), num=min(N_SAMPLES, n)).astype(np.int64)) if n else []
+    return {
+        "workload": wl.name,
+        "config": k,
+        "n_sends": n,
+        "collective_time_ns": r.collective_time,
+        "stats": r.stats,
+        "sha256": digest(r.sends),
+        "sample_index": [int(i) for i in idx],
+        "sample_rows": [[int(x) for x in r.sends[i]] for i in idx],
+        "oracle_seconds": round(dt, 2),
+    }
+
+
+if __name__ == "__main__":
+    ks = [int(a) for a in sys.argv[1:]] or [1, 2, 3, 4, 5]
+    for k in ks:
+        g = make(k)
+        with open(os.path.join(HERE, f"config{k}.json"), "w") as f:
+            json.dump(g, f, indent=1)
+        print(k, g["workload"], g["n_sends"], g["collective_time_ns"], g["oracle_seconds"], "s", flush=True)
