@@ -96,9 +96,10 @@ void pccl_destroy(pccl_ctx *ctx);
  * byte per ns).  All arrays are host memory of n_links entries and are copied.
  * PCCL_EINVAL: endpoint out of range, self loop, duplicate (src, dst) pair,
  * zero bandwidth, n_npus == 0.  PCCL_EUNSUPPORTED: more than 8000 devices
- * (NPUs plus switches), more than 256 in-links on one device, or a device
- * whose in-links' sources have more than 1024 in-links in total (the
- * per-destination state of the matching kernel lives in 30 KB of LDS).
+ * (NPUs plus switches), more than 64 in-links on one device (one wavefront
+ * lane per in-link), or a device whose in-links' sources have more than 512
+ * in-links in total (the per-destination arrival lists live in ~10 KB of
+ * LDS per wavefront).
  */
 pccl_status pccl_load_topology(pccl_ctx *ctx, uint32_t n_npus, uint32_t n_switches,
                                uint32_t n_links, const uint32_t *link_src,

@@ -14,9 +14,9 @@ constexpr uint64_t NONE64 = 0xFFFFFFFFFFFFFFFFull;
 constexpr uint32_t ROW_ALIGN_WORDS = 128;
 
 // Matching kernel envelope (checked on the host when a topology is loaded).
-constexpr uint32_t MATCH_THREADS = 256;   // one workgroup per destination device
-constexpr uint32_t MAX_IN_LINKS = 256;    // in-links of one device
-constexpr uint32_t MAX_PAIRS = 1024;      // sum over a device's in-links of their sources' in-degree
+constexpr uint32_t MATCH_THREADS = 512;   // 8 wavefronts, one destination device each
+constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one device (one lane each)
+constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of their sources' in-degree
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
 
 // Status codes mirrored from the public header.
@@ -37,6 +37,7 @@ struct Control {
     unsigned long long scan_words;       // words of each row read by the intersect
     uint32_t n_sources;      // distinct chunk sources
     uint32_t barrier;        // grid barrier arrival counter (monotonic)
+    uint32_t release;        // grid barrier generation, bumped by the last arrival
     uint32_t abort;          // set when a barrier wait times out
     uint32_t cstar;          // collective time of the copy schedule
     // per-window slots, indexed by window number mod 3 so that a slot is
@@ -47,7 +48,7 @@ struct Control {
     uint32_t sort_cur;       // radix sort: buffer holding the current order
     uint32_t sort_src;       // radix sort: buffer read by the pending scatter
     uint32_t sort_skip;      // radix sort: pending pass is a no-op
-    uint32_t pad[3];
+    uint32_t pad[2];
 };
 
 __device__ inline void record_error(Control *ctl, uint32_t code, uint32_t a = 0, uint32_t b = 0,
@@ -102,6 +103,7 @@ struct Layout {
     uint64_t *holds, *needs;  // [D * Wp]
     uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
     uint64_t *snap;           // [3 * L] by slot
+    unsigned long long *dest_log;  // [D] next send-log slot of each destination
     // output
     void *out;                // pccl_send [2 * max_sends]
     Control *ctl;
@@ -122,6 +124,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
                         const uint16_t *chunk_group, uint64_t seed, hipStream_t st);
 hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
 int match_max_grid(int device);
+int match_waves_per_block();
 hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st);
 // LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;
 // the sorted order ends up in buffer ly.ctl->sort_cur (read it on the device).

@@ -15,8 +15,9 @@
 //  1. Within one event, picks into different destinations never interact:
 //     holds do not change during an event and a commit only clears a bit of
 //     its own destination's needs row.  So each destination device d is
-//     owned by one workgroup, which keeps d's in-links, d's needs row and
-//     the arrivals into d; clashes are resolved inside the workgroup.
+//     owned by one wavefront (lane i <-> in-link i), which keeps d's
+//     in-links, d's needs row and the arrivals into d; clashes are resolved
+//     inside the wavefront, with no workgroup barrier.
 //  2. A transfer started at time >= t0 ends no earlier than t0 + Tmin (the
 //     smallest link time).  So every arrival inside [t0, t0 + Tmin) comes
 //     from a transfer that started before t0 and is known when the window
@@ -31,7 +32,9 @@
 // candidate set was found empty stays empty until its source receives a
 // chunk its destination needs (needs only shrink), so it is not rescanned;
 // a busy link keeps a cursor below which it has no candidate (lowered when
-// its source receives a needed chunk), so its next scan starts there.
+// its source receives a needed chunk), so its next scan starts there.  Each
+// lane first probes the next few words of its own link's two rows; only the
+// scans that run past the probe are continued by the whole wavefront.
 #include "pccl_internal.h"
 
 namespace pccl {
@@ -39,50 +42,70 @@ namespace {
 
 constexpr uint32_t NT = MATCH_THREADS;
 constexpr uint32_t NWAVES = NT / 64;
-constexpr uint8_t M_IDLE = 0, M_FULL = 1, M_ARR = 2, M_ARR_WON = 3;
-constexpr uint32_t SPIN_LIMIT = 1u << 22;
+constexpr uint32_t MAXIN = MAX_IN_LINKS;  // one lane per in-link
+constexpr uint32_t PAIRS = MAX_PAIRS;
+constexpr uint32_t M_IDLE = 0, M_FULL = 1, M_ARR = 2, M_ARR_WON = 3;
+constexpr uint32_t K_NONE = 0, K_BUSY = 1, K_IDLE = 2;
+constexpr uint32_t SPIN_LIMIT = 1u << 24;
+constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
+constexpr uint32_t PROBE_STEPS = 4;  // lane-parallel probe steps before the whole wave helps
+constexpr uint32_t PAIR_GROUP = 4;   // arrival-list entries per lane whose loads are in flight together
 
-struct Shared {
-    uint32_t link[MAX_IN_LINKS], src[MAX_IN_LINKS], tim[MAX_IN_LINKS];
-    uint32_t busy[MAX_IN_LINKS], infl[MAX_IN_LINKS], cur[MAX_IN_LINKS], pick[MAX_IN_LINKS];
-    uint32_t cum[MAX_IN_LINKS + 1];
-    uint32_t full_list[MAX_IN_LINKS];
-    uint8_t mode[MAX_IN_LINKS], idle[MAX_IN_LINKS], win[MAX_IN_LINKS];
-    uint32_t arr_end[MAX_PAIRS], arr_c[MAX_PAIRS];
-    uint16_t arr_j[MAX_PAIRS];
-    uint32_t unf_c[MAX_PAIRS];
-    uint16_t unf_j[MAX_PAIRS];
-    uint32_t snd_link[MAX_IN_LINKS], snd_rank[MAX_IN_LINKS], snd_t[MAX_IN_LINKS];
-    uint32_t n_arr, n_unf, n_full, n_send, send_base;
-    uint32_t red[NWAVES];
+static_assert(MAXIN == 64, "one lane per in-link");
+
+// Per-wavefront scratch (one destination at a time).  When every wave owns
+// one destination for the whole run, the per-link part persists across
+// windows (no reload).
+struct WaveShared {
+    uint32_t src[MAXIN], srcoff[MAXIN], tim[MAXIN], link[MAXIN];
+    uint32_t cur[MAXIN], pick[MAXIN], mode[MAXIN], kind[MAXIN];
+    uint32_t cum[MAXIN + 1];
+    uint32_t arr_end[PAIRS], arr_c[PAIRS];
+    uint32_t unf_c[PAIRS];
+    uint8_t arr_j[PAIRS], unf_j[PAIRS], arr_need[PAIRS], unf_need[PAIRS];
+    uint32_t snd_link[MAXIN], snd_rank[MAXIN], snd_t[MAXIN];
+};
+
+struct BlockShared {
+    WaveShared w[NWAVES];
+    uint32_t red_tmin[NWAVES];
+    unsigned long long red_sent[NWAVES];
     uint32_t barrier_ok;
 };
+
+__device__ inline void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 __device__ inline bool need_bit(const uint64_t *nd, uint32_t c)
 {
     return (nd[c >> 6] >> (c & 63)) & 1ull;
 }
 
-__device__ inline uint32_t block_min(uint32_t v, Shared &sh)
+__device__ inline uint32_t wave_min(uint32_t v)
 {
     for (int off = 32; off; off >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, off));
-    if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = v;
-    __syncthreads();
-    uint32_t r = sh.red[0];
-    for (uint32_t w = 1; w < NWAVES; w++) r = min(r, sh.red[w]);
-    __syncthreads();
-    return r;
+    return v;
 }
 
-__device__ inline uint32_t block_or(uint32_t v, Shared &sh)
+__device__ inline uint32_t wave_max(uint32_t v)
 {
-    const uint32_t any = __ballot(v != 0) != 0ull;
-    if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = any;
-    __syncthreads();
-    uint32_t r = 0;
-    for (uint32_t w = 0; w < NWAVES; w++) r |= sh.red[w];
-    __syncthreads();
-    return r;
+    for (int off = 32; off; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off));
+    return v;
+}
+
+__device__ inline uint32_t wave_sum(uint32_t v)
+{
+    for (int off = 32; off; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off);
+    return v;
+}
+
+__device__ inline uint32_t lane_prefix(uint64_t mask, uint32_t lane)
+{
+    return (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
 }
 
 __device__ inline uint64_t shfl64(uint64_t v, int lane)
@@ -91,11 +114,15 @@ __device__ inline uint64_t shfl64(uint64_t v, int lane)
     return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
+__device__ inline uint64_t u4lo(uint4 v) { return ((uint64_t)v.y << 32) | v.x; }
+__device__ inline uint64_t u4hi(uint4 v) { return ((uint64_t)v.w << 32) | v.z; }
+
 // Bitset intersect + select for one link, by a whole wave: the first set bit
 // at position >= cur of holds[src] & needs[dst], in priority order.  Each
 // lane loads 16 bytes of each row per sweep (two sweeps in flight, 2 KiB per
 // row per wave), a ballot finds the first lane with a non-zero AND, and a
-// count-trailing-zeros gives the chunk.
+// count-trailing-zeros gives the chunk.  `words` counts the words per row the
+// scan needed (through the word holding the pick, or to the row end).
 __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
                                          uint32_t cur, uint64_t Wp, uint64_t &words)
 {
@@ -112,8 +139,8 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
             if (idx < Wp) {
                 const uint4 hv = *reinterpret_cast<const uint4 *>(h + idx);
                 const uint4 nv = *reinterpret_cast<const uint4 *>(nd + idx);
-                x = (((uint64_t)hv.y << 32) | hv.x) & (((uint64_t)nv.y << 32) | nv.x);
-                y = (((uint64_t)hv.w << 32) | hv.z) & (((uint64_t)nv.w << 32) | nv.z);
+                x = u4lo(hv) & u4lo(nv);
+                y = u4hi(hv) & u4hi(nv);
                 if (idx < w0) x = 0;
                 else if (idx == w0) x &= keep0;
                 if (idx + 1 < w0) y = 0;
@@ -139,9 +166,10 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
     return NONE32;
 }
 
-// Grid-wide barrier on a monotonic arrival counter.  Returns false when the
+// Grid-wide barrier: arrivals on a monotonic counter; the last arrival bumps
+// a separate release word that the others poll.  Returns false when the
 // wait timed out or another workgroup gave up (then the kernel ends).
-__device__ bool grid_barrier(Control *ctl, Shared &sh)
+__device__ bool grid_barrier(Control *ctl, BlockShared &sh, uint32_t gen)
 {
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -149,21 +177,24 @@ __device__ bool grid_barrier(Control *ctl, Shared &sh)
         uint32_t ok = 1;
         __threadfence();
         const uint32_t old = atomicAdd(&ctl->barrier, 1u);
-        const uint32_t target = (old / nb + 1u) * nb;
-        uint32_t spins = 0;
-        while (true) {
-            const uint32_t v = __hip_atomic_load(&ctl->barrier, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if ((int32_t)(v - target) >= 0) break;
-            if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                ok = 0;
-                break;
+        if (old + 1u == (gen + 1u) * nb) {
+            __hip_atomic_store(&ctl->release, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            uint32_t spins = 0;
+            while (true) {
+                const uint32_t v = __hip_atomic_load(&ctl->release, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((int32_t)(v - (gen + 1u)) >= 0) break;
+                if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                    ok = 0;
+                    break;
+                }
+                if (++spins > SPIN_LIMIT) {
+                    atomicExch(&ctl->abort, 1u);
+                    ok = 0;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
             }
-            if (++spins > SPIN_LIMIT) {
-                atomicExch(&ctl->abort, 1u);
-                ok = 0;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
         }
         __threadfence();
         sh.barrier_ok = ok;
@@ -178,20 +209,72 @@ __device__ inline void window_error(Control *ctl, uint32_t k, uint32_t code, uin
     atomicOr(&ctl->win_err[k % 3], 1u);
 }
 
+// Per-wavefront accumulators, kept identical on every lane.
 struct Acc {
-    uint32_t tmin;     // earliest end among transfers in flight (this thread's links)
-    uint32_t cstar;    // latest transfer end committed by this thread
-    uint32_t clashes;  // picks of this thread that lost a clash
-    uint64_t words;    // words per row scanned by this thread's wave (lane 0)
+    uint32_t tmin;     // earliest end among transfers in flight on this wave's links
+    uint32_t cstar;    // latest transfer end committed by this wave
+    unsigned long long sent, rounds, clashes, words;
 };
 
-// All events of window [t0, t1) for destination d.
-__device__ void process_destination(const Layout &ly, const Sizes &sz, Shared &sh, uint32_t d, uint32_t k,
-                                    uint32_t t0, uint64_t t1, Acc &acc, unsigned long long &rounds,
-                                    unsigned long long &sent)
+// One wavefront's destination: uniform values and this lane's in-link.
+struct Dest {
+    uint32_t d, base, n, pairs;
+    uint32_t src, tim;          // this lane's in-link (lane < n)
+    uint32_t busy, infl, idle;  // its state
+    unsigned long long log;     // next send-log slot of d
+};
+
+__device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds)
 {
-    const uint32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const uint32_t base = ly.in_off[d], n = ly.in_off[d + 1] - base;
+    const uint32_t lane = threadIdx.x & 63;
+    ds.d = d;
+    ds.base = ly.in_off[d];
+    ds.n = ly.in_off[d + 1] - ds.base;
+    ds.pairs = ly.dest_pairs[d];
+    ds.log = ly.dest_log[d];
+    ds.src = 0;
+    ds.tim = 0;
+    ds.busy = 0;
+    ds.infl = NONE32;
+    ds.idle = 0;
+    if (lane < ds.n) {
+        const uint32_t sl = ds.base + lane;
+        ds.src = ly.slot_src[sl];
+        ds.tim = ly.slot_time[sl];
+        ds.busy = ly.busy[sl];
+        ds.infl = ly.infl[sl];
+        ds.idle = ly.lflags[sl] & 1u;
+        ws.src[lane] = ds.src;
+        ws.srcoff[lane] = ly.in_off[ds.src];
+        ws.tim[lane] = ds.tim;
+        ws.link[lane] = ly.slot_link[sl];
+        ws.cur[lane] = ly.cur[sl];
+        ws.cum[lane] = ly.slot_cum[sl];
+    }
+    if (lane == 0) ws.cum[ds.n] = ds.pairs;
+    wave_sync();
+}
+
+__device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    if (lane < ds.n) {
+        const uint32_t sl = ds.base + lane;
+        ly.busy[sl] = ds.busy;
+        ly.infl[sl] = ds.infl;
+        ly.cur[sl] = ws.cur[lane];
+        ly.lflags[sl] = ds.idle;
+    }
+    if (lane == 0) ly.dest_log[ds.d] = ds.log;
+    wave_sync();
+}
+
+// All events of window [t0, t1) for one destination, by one wavefront.
+__device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws, Dest &ds, uint32_t k,
+                               uint32_t t0, uint64_t t1, Acc &acc)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t n = ds.n, d = ds.d;
     if (n == 0) return;
     const uint64_t Wp = sz.Wp, L = sz.L;
     const uint32_t END = (uint32_t)(Wp * 64);
@@ -200,19 +283,12 @@ __device__ void process_destination(const Layout &ly, const Sizes &sz, Shared &s
     const uint64_t *snap1 = ly.snap + (uint64_t)((k + 2) % 3) * L;  // in flight at the end of window k-1
     const uint64_t *snap2 = ly.snap + (uint64_t)((k + 1) % 3) * L;  // in flight at the end of window k-2
     uint64_t *snap0 = ly.snap + (uint64_t)(k % 3) * L;              // written for window k+1
+    const bool mine = lane < n;
+    const uint32_t sl = ds.base + lane;
 
-    // load this destination's in-links; fold the arrivals of window k-1
-    for (uint32_t i = tid; i < n; i += NT) {
-        const uint32_t sl = base + i;
-        sh.link[i] = ly.slot_link[sl];
-        sh.src[i] = ly.slot_src[sl];
-        sh.tim[i] = ly.slot_time[sl];
-        sh.busy[i] = ly.busy[sl];
-        sh.infl[i] = ly.infl[sl];
-        sh.cur[i] = ly.cur[sl];
-        sh.idle[i] = (uint8_t)(ly.lflags[sl] & 1u);
-        sh.cum[i] = ly.slot_cum[sl];
-        sh.mode[i] = M_IDLE;
+    // fold the arrivals of window k-1 into d's holds row
+    if (mine) {
+        ws.mode[lane] = M_IDLE;
         if (k >= 2) {
             const uint64_t e = snap2[sl];
             if (e != NONE64 && (uint32_t)e < t0) {
@@ -221,241 +297,314 @@ __device__ void process_destination(const Layout &ly, const Sizes &sz, Shared &s
             }
         }
     }
-    if (tid == 0) {
-        sh.n_arr = 0;
-        sh.n_unf = 0;
-        sh.n_send = 0;
-        sh.cum[n] = ly.dest_pairs[d];
-    }
-    __syncthreads();
 
     // arrivals at the sources of d's in-links that d needs: this window's
     // (snapshot k-1, ends in [t0, t1)) and last window's (snapshot k-2,
     // ends before t0; possibly not folded into the source's row yet)
-    const uint32_t pairs = sh.cum[n];
+    uint32_t n_arr = 0, n_unf = 0;
     if (k >= 1) {
-        for (uint32_t p = tid; p < pairs; p += NT) {
-            uint32_t lo = 0, hi = n;
-            while (hi - lo > 1) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if (sh.cum[mid] <= p) lo = mid;
-                else hi = mid;
-            }
-            const uint32_t s = sh.src[lo];
-            const uint32_t slot = ly.in_off[s] + (p - sh.cum[lo]);
-            const uint64_t e1 = snap1[slot];
-            if (e1 != NONE64 && (uint64_t)(uint32_t)e1 < t1) {
-                const uint32_t c = (uint32_t)(e1 >> 32);
-                if (need_bit(nd, c)) {
-                    const uint32_t q = atomicAdd(&sh.n_arr, 1u);
-                    sh.arr_end[q] = (uint32_t)e1;
-                    sh.arr_c[q] = c;
-                    sh.arr_j[q] = (uint16_t)lo;
-                }
-            }
-            if (k >= 2) {
-                const uint64_t e2 = snap2[slot];
-                if (e2 != NONE64 && (uint32_t)e2 < t0) {
-                    const uint32_t c = (uint32_t)(e2 >> 32);
-                    if (need_bit(nd, c)) {
-                        const uint32_t q = atomicAdd(&sh.n_unf, 1u);
-                        sh.unf_c[q] = c;
-                        sh.unf_j[q] = (uint16_t)lo;
+        for (uint32_t g0 = 0; g0 < ds.pairs; g0 += 64 * PAIR_GROUP) {
+            uint64_t e1[PAIR_GROUP], e2[PAIR_GROUP];
+            uint32_t jj[PAIR_GROUP];
+#pragma unroll
+            for (uint32_t u = 0; u < PAIR_GROUP; u++) {
+                const uint32_t p = g0 + 64 * u + lane;
+                e1[u] = NONE64;
+                e2[u] = NONE64;
+                jj[u] = 0;
+                if (p < ds.pairs) {
+                    uint32_t lo = 0, hi = n;
+                    while (hi - lo > 1) {
+                        const uint32_t mid = (lo + hi) >> 1;
+                        if (ws.cum[mid] <= p) lo = mid;
+                        else hi = mid;
                     }
+                    jj[u] = lo;
+                    const uint32_t slot = ws.srcoff[lo] + (p - ws.cum[lo]);
+                    e1[u] = snap1[slot];
+                    if (k >= 2) e2[u] = snap2[slot];
                 }
+            }
+            bool a_ok[PAIR_GROUP], u_ok[PAIR_GROUP];
+#pragma unroll
+            for (uint32_t u = 0; u < PAIR_GROUP; u++) {
+                a_ok[u] = e1[u] != NONE64 && (uint64_t)(uint32_t)e1[u] < t1 && need_bit(nd, (uint32_t)(e1[u] >> 32));
+                u_ok[u] = e2[u] != NONE64 && (uint32_t)e2[u] < t0 && need_bit(nd, (uint32_t)(e2[u] >> 32));
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < PAIR_GROUP; u++) {
+                const uint64_t ma = __ballot(a_ok[u]), mu = __ballot(u_ok[u]);
+                if (a_ok[u]) {
+                    const uint32_t q = n_arr + lane_prefix(ma, lane);
+                    ws.arr_end[q] = (uint32_t)e1[u];
+                    ws.arr_c[q] = (uint32_t)(e1[u] >> 32);
+                    ws.arr_j[q] = (uint8_t)jj[u];
+                    ws.arr_need[q] = 1;
+                }
+                if (u_ok[u]) {
+                    const uint32_t q = n_unf + lane_prefix(mu, lane);
+                    ws.unf_c[q] = (uint32_t)(e2[u] >> 32);
+                    ws.unf_j[q] = (uint8_t)jj[u];
+                    ws.unf_need[q] = 1;
+                }
+                n_arr += (uint32_t)__popcll(ma);
+                n_unf += (uint32_t)__popcll(mu);
             }
         }
     }
-    __syncthreads();
-    const uint32_t n_arr = sh.n_arr, n_unf = sh.n_unf;
+    wave_sync();
 
     // event times of this destination inside the window, in order
     int64_t t_prev = (int64_t)t0 - 1;
+    uint32_t n_send = 0;
     while (true) {
         uint32_t m = NONE32;
         if (k == 0) {
-            if (t_prev < 0 && tid == 0) m = 0;
+            if (t_prev < 0) m = 0;
         } else {
-            for (uint32_t i = tid; i < n; i += NT)
-                if (sh.infl[i] != NONE32 && (int64_t)sh.busy[i] > t_prev && (uint64_t)sh.busy[i] < t1)
-                    m = min(m, sh.busy[i]);
-            for (uint32_t q = tid; q < n_arr; q += NT)
-                if ((int64_t)sh.arr_end[q] > t_prev) m = min(m, sh.arr_end[q]);
+            if (mine && ds.infl != NONE32 && (int64_t)ds.busy > t_prev && (uint64_t)ds.busy < t1) m = ds.busy;
+            for (uint32_t q = lane; q < n_arr; q += 64)
+                if (ws.arr_need[q] && (int64_t)ws.arr_end[q] > t_prev) m = min(m, ws.arr_end[q]);
         }
-        const uint32_t t = block_min(m, sh);
+        const uint32_t t = wave_min(m);
         if (t == NONE32) break;
 
         // links whose transfer ends now are free and need a full scan
-        for (uint32_t i = tid; i < n; i += NT) {
-            uint8_t md = M_IDLE;
+        uint32_t md = M_IDLE;
+        if (mine) {
             if (k == 0) {
                 md = M_FULL;
-            } else if (sh.infl[i] != NONE32 && sh.busy[i] == t) {
+            } else if (ds.infl != NONE32 && ds.busy == t) {
                 md = M_FULL;
-                sh.infl[i] = NONE32;
+                ds.infl = NONE32;
             }
-            sh.mode[i] = md;
+            ws.mode[lane] = md;
+            ws.kind[lane] = (md == M_FULL || ds.infl != NONE32) ? K_BUSY : (ds.idle ? K_IDLE : K_NONE);
         }
-        __syncthreads();
+        wave_sync();
         // a needed chunk arriving at a link's source: busy or just-freed links
         // lower their cursor; an idle free link gets it as its candidate
-        for (uint32_t q = tid; q < n_arr; q += NT) {
-            if (sh.arr_end[q] != t) continue;
-            const uint32_t j = sh.arr_j[q], c = sh.arr_c[q];
-            if (!need_bit(nd, c)) continue;
-            if (sh.mode[j] == M_FULL || sh.infl[j] != NONE32)
-                atomicMin(&sh.cur[j], c);
-            else if (sh.idle[j])
-                sh.mode[j] = M_ARR;
+        for (uint32_t q = lane; q < n_arr; q += 64) {
+            if (ws.arr_end[q] != t || !ws.arr_need[q]) continue;
+            const uint32_t j = ws.arr_j[q], c = ws.arr_c[q];
+            const uint32_t kind = ws.kind[j];
+            if (kind == K_BUSY) atomicMin(&ws.cur[j], c);
+            else if (kind == K_IDLE) ws.mode[j] = M_ARR;
         }
-        __syncthreads();
+        wave_sync();
+        if (mine) md = ws.mode[lane];
 
         // pick rounds at time t
         while (true) {
-            for (uint32_t i = tid; i < n; i += NT) sh.pick[i] = NONE32;
-            if (tid == 0) sh.n_full = 0;
-            __syncthreads();
-            for (uint32_t i = tid; i < n; i += NT)
-                if (sh.mode[i] == M_FULL) sh.full_list[atomicAdd(&sh.n_full, 1u)] = i;
-            __syncthreads();
-            const uint32_t nf = sh.n_full;
-            for (uint32_t f = wave; f < nf; f += NWAVES) {
-                const uint32_t j = sh.full_list[f];
-                const uint32_t p =
-                    wave_first_candidate(ly.holds + (uint64_t)sh.src[j] * Wp, nd, sh.cur[j], Wp, acc.words);
-                if (lane == 0 && p != NONE32) atomicMin(&sh.pick[j], p);
+            // bitmap part of the full scans: lane-parallel probes of each
+            // link's own rows; scans that outlast them continue with the wave
+            uint32_t p = NONE32, scanned = 0;
+            bool scanning = false;
+            uint64_t pos = 0, w0 = 0, keep0 = 0;
+            if (mine && md == M_FULL) {
+                const uint32_t cur = ws.cur[lane];
+                w0 = cur >> 6;
+                keep0 = ~0ull << (cur & 63);
+                scanning = w0 < Wp;
+                pos = w0 & ~1ull;
             }
-            for (uint32_t q = tid; q < n_arr; q += NT) {
-                const uint32_t j = sh.arr_j[q], c = sh.arr_c[q], md = sh.mode[j];
-                if (md == M_FULL) {
-                    if (sh.arr_end[q] <= t && c >= sh.cur[j] && need_bit(nd, c)) atomicMin(&sh.pick[j], c);
-                } else if (md == M_ARR) {
-                    if (sh.arr_end[q] == t && need_bit(nd, c)) atomicMin(&sh.pick[j], c);
-                }
-            }
-            for (uint32_t q = tid; q < n_unf; q += NT) {
-                const uint32_t j = sh.unf_j[q], c = sh.unf_c[q];
-                if (sh.mode[j] == M_FULL && c >= sh.cur[j] && need_bit(nd, c)) atomicMin(&sh.pick[j], c);
-            }
-            __syncthreads();
-            uint32_t any = 0;
-            for (uint32_t i = tid; i < n; i += NT) {
-                if (sh.mode[i] == M_IDLE) continue;
-                if (sh.pick[i] == NONE32) {
-                    sh.mode[i] = M_IDLE;
-                    sh.idle[i] = 1;
-                    sh.cur[i] = END;
-                } else {
-                    any = 1;
-                }
-            }
-            if (!block_or(any, sh)) break;
-            // clash resolution among d's in-links: fastest link, then lowest id
-            for (uint32_t i = tid; i < n; i += NT) {
-                if (sh.mode[i] == M_IDLE) continue;
-                const uint32_t p = sh.pick[i], ti = sh.tim[i], li = sh.link[i];
-                uint8_t w = 1;
-                for (uint32_t j = 0; j < n; j++) {
-                    if (j == i || sh.mode[j] == M_IDLE || sh.pick[j] != p) continue;
-                    if (sh.tim[j] < ti || (sh.tim[j] == ti && sh.link[j] < li)) w = 0;
-                }
-                sh.win[i] = w;
-            }
-            __syncthreads();
-            for (uint32_t i = tid; i < n; i += NT) {
-                if (sh.mode[i] == M_IDLE) continue;
-                const uint32_t p = sh.pick[i];
-                if (sh.win[i]) {
-                    atomicAnd((unsigned long long *)&nd[p >> 6], ~(1ull << (p & 63)));
-                    const uint64_t end = (uint64_t)t + sh.tim[i];
-                    if (end > 0xFFFFFFFFull) window_error(ly.ctl, k, ST_ERANGE, p, d, 2);
-                    const uint32_t e32 = end > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)end;
-                    sh.infl[i] = p;
-                    sh.busy[i] = e32;
-                    sh.idle[i] = 0;
-                    const uint32_t q = atomicAdd(&sh.n_send, 1u);
-                    sh.snd_link[q] = sh.link[i];
-                    sh.snd_rank[q] = p;
-                    sh.snd_t[q] = t;
-                    acc.cstar = max(acc.cstar, e32);
-                    if (sh.mode[i] == M_FULL) {
-                        sh.cur[i] = p + 1;
-                        sh.mode[i] = M_IDLE;
-                    } else {
-                        sh.cur[i] = END;
-                        sh.mode[i] = M_ARR_WON;
+            const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
+            for (uint32_t step = 0; step < PROBE_STEPS; step++) {
+                if (!__ballot(scanning)) break;
+                if (scanning) {
+                    uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
+#pragma unroll
+                    for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                        const uint64_t idx = pos + 2 * u;
+                        if (idx < Wp) {
+                            hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
+                            nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
+                        } else {
+                            hv[u] = make_uint4(0, 0, 0, 0);
+                            nv[u] = make_uint4(0, 0, 0, 0);
+                        }
                     }
-                } else {
-                    acc.clashes++;
-                    if (sh.mode[i] == M_FULL) sh.cur[i] = p + 1;
+#pragma unroll
+                    for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                        const uint64_t idx = pos + 2 * u;
+                        uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
+                        if (idx < w0) x = 0;
+                        else if (idx == w0) x &= keep0;
+                        if (idx + 1 < w0) y = 0;
+                        else if (idx + 1 == w0) y &= keep0;
+                        if (p == NONE32) {
+                            if (x) {
+                                p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
+                                scanned = (uint32_t)(idx + 1 - w0);
+                            } else if (y) {
+                                p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
+                                scanned = (uint32_t)(idx + 2 - w0);
+                            }
+                        }
+                    }
+                    if (p != NONE32) {
+                        scanning = false;
+                    } else {
+                        pos += PROBE_WORDS;
+                        if (pos >= Wp) {
+                            scanning = false;
+                            scanned = (uint32_t)(Wp - w0);
+                        }
+                    }
                 }
             }
-            __syncthreads();
-            // a link that won an arrival keeps the other arrivals as its cursor
-            for (uint32_t q = tid; q < n_arr; q += NT) {
-                if (sh.arr_end[q] != t) continue;
-                const uint32_t j = sh.arr_j[q], c = sh.arr_c[q];
-                if (sh.mode[j] == M_ARR_WON && need_bit(nd, c)) atomicMin(&sh.cur[j], c);
+            if (scanning) scanned = (uint32_t)(pos - w0);
+            acc.words += wave_sum(scanned);
+            uint64_t cmask = __ballot(scanning);
+            while (cmask) {
+                const int j = __builtin_ffsll((long long)cmask) - 1;
+                cmask &= cmask - 1;
+                const uint32_t sj = (uint32_t)__shfl((int)ds.src, j);
+                const uint32_t from = (uint32_t)(shfl64(pos, j) * 64);
+                uint64_t w = 0;
+                const uint32_t pj = wave_first_candidate(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
+                acc.words += w;
+                if ((int)lane == j) p = pj;
             }
-            __syncthreads();
-            for (uint32_t i = tid; i < n; i += NT)
-                if (sh.mode[i] == M_ARR_WON) sh.mode[i] = M_IDLE;
-            if (tid == 0) rounds++;
-            __syncthreads();
+            // explicit candidates: arrivals not yet in the source's row
+            if (mine) ws.pick[lane] = (md == M_FULL) ? p : NONE32;
+            wave_sync();
+            for (uint32_t q = lane; q < n_arr; q += 64) {
+                if (!ws.arr_need[q]) continue;
+                const uint32_t j = ws.arr_j[q], c = ws.arr_c[q], mj = ws.mode[j];
+                if (mj == M_FULL) {
+                    if (ws.arr_end[q] <= t && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
+                } else if (mj == M_ARR) {
+                    if (ws.arr_end[q] == t) atomicMin(&ws.pick[j], c);
+                }
+            }
+            for (uint32_t q = lane; q < n_unf; q += 64) {
+                if (!ws.unf_need[q]) continue;
+                const uint32_t j = ws.unf_j[q], c = ws.unf_c[q];
+                if (ws.mode[j] == M_FULL && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
+            }
+            wave_sync();
+            uint32_t pk = NONE32;
+            if (mine && md != M_IDLE) {
+                pk = ws.pick[lane];
+                if (pk == NONE32) {
+                    md = M_IDLE;
+                    ds.idle = 1;
+                    ws.cur[lane] = END;
+                }
+                ws.mode[lane] = md;
+            }
+            const bool act = mine && md != M_IDLE;
+            if (!__ballot(act)) break;
+            // clash resolution among d's in-links: fastest link, then lowest id
+            if (mine) ws.pick[lane] = act ? pk : NONE32;
+            wave_sync();
+            bool win = false;
+            if (act) {
+                win = true;
+                const uint32_t li = ws.link[lane];
+                for (uint32_t j = 0; j < n; j++) {
+                    if (j == lane || ws.pick[j] != pk) continue;
+                    if (ws.tim[j] < ds.tim || (ws.tim[j] == ds.tim && ws.link[j] < li)) win = false;
+                }
+            }
+            const uint64_t wins = __ballot(win);
+            const uint64_t losers = __ballot(act && !win);
+            uint32_t ce = 0;
+            if (act) {
+                if (win) {
+                    atomicAnd((unsigned long long *)&nd[pk >> 6], ~(1ull << (pk & 63)));
+                    const uint64_t end = (uint64_t)t + ds.tim;
+                    if (end > 0xFFFFFFFFull) window_error(ly.ctl, k, ST_ERANGE, pk, d, 2);
+                    const uint32_t e32 = end > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)end;
+                    ds.infl = pk;
+                    ds.busy = e32;
+                    ds.idle = 0;
+                    ce = e32;
+                    const uint32_t q = n_send + lane_prefix(wins, lane);
+                    ws.snd_link[q] = ws.link[lane];
+                    ws.snd_rank[q] = pk;
+                    ws.snd_t[q] = t;
+                    if (md == M_FULL) {
+                        ws.cur[lane] = pk + 1;
+                        md = M_IDLE;
+                    } else {
+                        ws.cur[lane] = END;
+                        md = M_ARR_WON;
+                    }
+                } else if (md == M_FULL) {
+                    ws.cur[lane] = pk + 1;
+                }
+                ws.mode[lane] = md;
+            }
+            n_send += (uint32_t)__popcll(wins);
+            acc.clashes += (unsigned long long)__popcll(losers);
+            acc.cstar = max(acc.cstar, wave_max(ce));
+            wave_sync();
+            // the delivered chunks are no longer needed: clear their flags
+            for (uint64_t wm = wins; wm; wm &= wm - 1) {
+                const uint32_t c = ws.pick[__builtin_ffsll((long long)wm) - 1];
+                for (uint32_t q = lane; q < n_arr; q += 64)
+                    if (ws.arr_c[q] == c) ws.arr_need[q] = 0;
+                for (uint32_t q = lane; q < n_unf; q += 64)
+                    if (ws.unf_c[q] == c) ws.unf_need[q] = 0;
+            }
+            wave_sync();
+            // a link that won an arrival keeps the other arrivals as its cursor
+            if (__ballot(md == M_ARR_WON)) {
+                for (uint32_t q = lane; q < n_arr; q += 64) {
+                    if (ws.arr_end[q] != t || !ws.arr_need[q]) continue;
+                    const uint32_t j = ws.arr_j[q];
+                    if (ws.mode[j] == M_ARR_WON) atomicMin(&ws.cur[j], ws.arr_c[q]);
+                }
+                wave_sync();
+                if (md == M_ARR_WON) {
+                    md = M_IDLE;
+                    ws.mode[lane] = md;
+                }
+            }
+            acc.rounds++;
+            wave_sync();
         }
         t_prev = t;
     }
 
-    // write back link state and this window's snapshot
-    for (uint32_t i = tid; i < n; i += NT) {
-        const uint32_t sl = base + i;
-        ly.busy[sl] = sh.busy[i];
-        ly.infl[sl] = sh.infl[i];
-        ly.cur[sl] = sh.cur[i];
-        ly.lflags[sl] = sh.idle[i];
-        if (sh.infl[i] != NONE32) {
-            snap0[sl] = ((uint64_t)sh.infl[i] << 32) | sh.busy[i];
-            acc.tmin = min(acc.tmin, sh.busy[i]);
-        } else {
-            snap0[sl] = NONE64;
+    // this window's snapshot and sends
+    if (mine) snap0[sl] = ds.infl != NONE32 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64;
+    acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
+    if (n_send) {
+        if (lane < n_send) {
+            const unsigned long long pos = ds.log + lane;
+            ly.skey[0][pos] = ((uint64_t)ws.snd_t[lane] << 32) | ws.snd_link[lane];
+            ly.sval[0][pos] = ws.snd_rank[lane];
         }
+        ds.log += n_send;
+        acc.sent += n_send;
     }
-    __syncthreads();
-    const uint32_t ns = sh.n_send;
-    if (ns) {
-        if (tid == 0) sh.send_base = (uint32_t)atomicAdd(&ly.ctl->n_log, (unsigned long long)ns);
-        __syncthreads();
-        const unsigned long long b0 = sh.send_base;
-        for (uint32_t q = tid; q < ns; q += NT) {
-            const unsigned long long pos = b0 + q;
-            if (pos < ly.ctl->max_sends) {
-                ly.skey[0][pos] = ((uint64_t)sh.snd_t[q] << 32) | sh.snd_link[q];
-                ly.sval[0][pos] = sh.snd_rank[q];
-            } else {
-                window_error(ly.ctl, k, ST_ENOMEM, 0, 0, 0);
-            }
-        }
-        if (tid == 0) sent += ns;
-    }
-    __syncthreads();
+    wave_sync();
 }
 
 __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 {
-    __shared__ Shared sh;
+    __shared__ BlockShared sh;
     Control *ctl = ly.ctl;
     if (__hip_atomic_load(&ctl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
-    const uint32_t tid = threadIdx.x;
-    const unsigned long long max_windows = ctl->needs_total + 2ull;
-    Acc acc = {NONE32, 0u, 0u, 0ull};
-    unsigned long long rounds = 0;
-    uint32_t t0 = 0;
-    unsigned long long k = 0;
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t gwave = blockIdx.x * NWAVES + wave, nwaves = gridDim.x * NWAVES;
     if (ctl->needs_total == 0) {
         if (blockIdx.x == 0 && tid == 0) ctl->windows = 0;
         return;
     }
+    const unsigned long long max_windows = ctl->needs_total + 2ull;
+    // every wave owns at most one destination: its state stays on chip
+    const bool resident = sz.D <= nwaves;
+    WaveShared &ws = sh.w[wave];
+    Dest ds{};
+    if (resident && gwave < sz.D) load_dest(ly, ws, gwave, ds);
+    Acc acc = {NONE32, 0u, 0ull, 0ull, 0ull, 0ull};
     unsigned long long remaining = ctl->needs_total;
+    uint32_t t0 = 0;
+    unsigned long long k = 0;
     for (;; k++) {
         const uint64_t t1 = (uint64_t)t0 + sz.tmin;
         if (blockIdx.x == 0 && tid == 0) {
@@ -464,15 +613,32 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
             ctl->win_err[(k + 1) % 3] = 0;
         }
         acc.tmin = NONE32;
-        unsigned long long sent = 0;
-        for (uint32_t d = blockIdx.x; d < sz.D; d += gridDim.x)
-            process_destination(ly, sz, sh, d, (uint32_t)k, t0, t1, acc, rounds, sent);
-        const uint32_t bmin = block_min(acc.tmin, sh);
+        const unsigned long long sent0 = acc.sent;
+        if (resident) {
+            if (gwave < sz.D) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, acc);
+        } else {
+            for (uint32_t d = gwave; d < sz.D; d += nwaves) {
+                load_dest(ly, ws, d, ds);
+                process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, acc);
+                store_dest(ly, ws, ds);
+            }
+        }
+        if (lane == 0) {
+            sh.red_tmin[wave] = acc.tmin;
+            sh.red_sent[wave] = acc.sent - sent0;
+        }
+        __syncthreads();
         if (tid == 0) {
+            uint32_t bmin = NONE32;
+            unsigned long long sent = 0;
+            for (uint32_t w = 0; w < NWAVES; w++) {
+                bmin = min(bmin, sh.red_tmin[w]);
+                sent += sh.red_sent[w];
+            }
             if (bmin != NONE32) atomicMin(&ctl->win_t0[(k + 1) % 3], bmin);
             if (sent) atomicAdd(&ctl->win_sent[k % 3], sent);
         }
-        if (!grid_barrier(ctl, sh)) break;
+        if (!grid_barrier(ctl, sh, (uint32_t)k)) break;
         const uint32_t err = __hip_atomic_load(&ctl->win_err[k % 3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const unsigned long long done =
             __hip_atomic_load(&ctl->win_sent[k % 3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -489,20 +655,16 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         t0 = tn;
     }
-    if (blockIdx.x == 0 && tid == 0) ctl->needs_remaining = remaining;
-    // block totals
-    uint32_t c = acc.cstar;
-    for (int off = 32; off; off >>= 1) c = max(c, (uint32_t)__shfl_xor((int)c, off));
-    uint32_t cl = acc.clashes;
-    for (int off = 32; off; off >>= 1) cl += (uint32_t)__shfl_xor((int)cl, off);
-    if ((tid & 63) == 0) {
-        atomicMax(&ctl->cstar, c);
-        if (cl) atomicAdd(&ctl->clashes, (unsigned long long)cl);
-        if (acc.words) atomicAdd(&ctl->scan_words, (unsigned long long)acc.words);
+    if (blockIdx.x == 0 && tid == 0) {
+        ctl->needs_remaining = remaining;
+        ctl->windows = k + 1;
+        ctl->n_log = ctl->needs_total - remaining;
     }
-    if (tid == 0) {
-        if (rounds) atomicAdd(&ctl->rounds, rounds);
-        if (blockIdx.x == 0) ctl->windows = k + 1;
+    if (lane == 0) {
+        atomicMax(&ctl->cstar, acc.cstar);
+        if (acc.clashes) atomicAdd(&ctl->clashes, acc.clashes);
+        if (acc.rounds) atomicAdd(&ctl->rounds, acc.rounds);
+        if (acc.words) atomicAdd(&ctl->scan_words, acc.words);
     }
 }
 
@@ -515,6 +677,8 @@ int match_max_grid(int device)
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return 0;
     return per_cu * cus;
 }
+
+int match_waves_per_block() { return (int)NWAVES; }
 
 hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid)
 {

@@ -254,6 +254,47 @@ __global__ void k_needs(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t
     if ((threadIdx.x & 63) == 0 && added) atomicAdd(&ly.ctl->needs_total, added);
 }
 
+// Each destination gets a contiguous segment of the send log, as long as
+// the number of deliveries it needs (every delivery is one transfer into it).
+__global__ void __launch_bounds__(256) k_needs_count(Layout ly, Sizes sz)
+{
+    __shared__ unsigned long long part[4];
+    const uint32_t d = blockIdx.x, tid = threadIdx.x;
+    unsigned long long c = 0;
+    if (!ly.ctl->error) {
+        const uint64_t *row = ly.needs + (uint64_t)d * sz.Wp;
+        for (uint64_t w = tid; w < sz.Wp; w += 256) c += (unsigned long long)__popcll(row[w]);
+    }
+    for (int off = 32; off; off >>= 1) c += __shfl_xor(c, off);
+    if ((tid & 63) == 0) part[tid >> 6] = c;
+    __syncthreads();
+    if (tid == 0) ly.dest_log[d] = part[0] + part[1] + part[2] + part[3];
+}
+
+__global__ void __launch_bounds__(1024) k_log_offsets(Layout ly, Sizes sz)
+{
+    __shared__ unsigned long long part[1024];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t per = (sz.D + 1023) / 1024;
+    const uint32_t lo = tid * per, hi = min(lo + per, sz.D);
+    unsigned long long s = 0;
+    for (uint32_t v = lo; v < hi; v++) s += ly.dest_log[v];
+    part[tid] = s;
+    __syncthreads();
+    for (uint32_t off = 1; off < 1024; off <<= 1) {
+        unsigned long long x = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += x;
+        __syncthreads();
+    }
+    unsigned long long run = tid ? part[tid - 1] : 0;
+    for (uint32_t v = lo; v < hi; v++) {
+        const unsigned long long c = ly.dest_log[v];
+        ly.dest_log[v] = run;
+        run += c;
+    }
+}
+
 __global__ void k_init_match(Layout ly, Sizes sz)
 {
     const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -310,6 +351,8 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
         k_holds<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
     }
     if (sz.W) k_needs<<<gw, T, 0, st>>>(ly, sz, pre, post);
+    k_needs_count<<<sz.D, 256, 0, st>>>(ly, sz);
+    k_log_offsets<<<1, 1024, 0, st>>>(ly, sz);
     k_init_match<<<blocks_for(sz.L ? sz.L : 1, T), T, 0, st>>>(ly, sz);
     return hipGetLastError();
 }
