@@ -218,6 +218,7 @@ pccl_status pccl_load_topology(pccl_ctx *c, uint32_t n_npus, uint32_t n_switches
     const uint64_t D64 = (uint64_t)n_npus + n_switches;
     if (D64 > MAX_DEVICES_SP) return fail(c, PCCL_EUNSUPPORTED, "%llu devices (limit %u)", (unsigned long long)D64, MAX_DEVICES_SP);
     const uint32_t D = (uint32_t)D64, L = n_links;
+    if (L >= (1u << 24)) return fail(c, PCCL_EUNSUPPORTED, "%u links (limit 2^24 - 1)", L);
     std::unordered_map<uint64_t, uint32_t> seen;
     seen.reserve(L * 2 + 1);
     for (uint32_t l = 0; l < L; l++) {

@@ -50,6 +50,9 @@ constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
 constexpr uint32_t PROBE_STEPS = 4;  // lane-parallel probe steps before the whole wave helps
 constexpr uint32_t PAIR_GROUP = 4;   // arrival-list entries per lane whose loads are in flight together
+constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
+constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
+constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
 
 static_assert(MAXIN == 64, "one lane per in-link");
 
@@ -119,9 +122,9 @@ __device__ inline uint64_t u4hi(uint4 v) { return ((uint64_t)v.w << 32) | v.z; }
 
 // Bitset intersect + select for one link, by a whole wave: the first set bit
 // at position >= cur of holds[src] & needs[dst], in priority order.  Each
-// lane loads 16 bytes of each row per sweep (two sweeps in flight, 2 KiB per
-// row per wave), a ballot finds the first lane with a non-zero AND, and a
-// count-trailing-zeros gives the chunk.  `words` counts the words per row the
+// lane loads 16 bytes of each row per sweep (four sweeps in flight, 8 KiB
+// per row per wave), a ballot finds the first lane with a non-zero AND, and
+// a count-trailing-zeros gives the chunk.  `words` counts the words per row the
 // scan needed (through the word holding the pick, or to the row end).
 __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
                                          uint32_t cur, uint64_t Wp, uint64_t &words)
@@ -130,10 +133,10 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
     const uint64_t w0 = cur >> 6;
     if (w0 >= Wp) return NONE32;
     const uint64_t keep0 = ~0ull << (cur & 63);
-    for (uint64_t wb = w0 & ~1ull; wb < Wp; wb += 256) {
-        uint64_t a[2], b[2];
+    for (uint64_t wb = w0 & ~1ull; wb < Wp; wb += 128 * SWEEPS) {
+        uint64_t a[SWEEPS], b[SWEEPS];
 #pragma unroll
-        for (int u = 0; u < 2; u++) {
+        for (int u = 0; u < (int)SWEEPS; u++) {
             const uint64_t idx = wb + 128 * u + 2 * lane;
             uint64_t x = 0, y = 0;
             if (idx < Wp) {
@@ -150,7 +153,7 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
             b[u] = y;
         }
 #pragma unroll
-        for (int u = 0; u < 2; u++) {
+        for (int u = 0; u < (int)SWEEPS; u++) {
             const uint64_t m = __ballot((a[u] | b[u]) != 0ull);
             if (m) {
                 const int fl = __builtin_ffsll((long long)m) - 1;
@@ -222,6 +225,9 @@ struct Dest {
     uint32_t src, tim;          // this lane's in-link (lane < n)
     uint32_t busy, infl, idle;  // its state
     unsigned long long log;     // next send-log slot of d
+    // arrival pairs p = 64 u + lane: slot of the source's in-link, and the
+    // in-link of d it feeds (slot << 8 | j; NONE32 past the last pair)
+    uint32_t pair[PAIRS_PER_LANE];
 };
 
 __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds)
@@ -253,6 +259,20 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
     }
     if (lane == 0) ws.cum[ds.n] = ds.pairs;
     wave_sync();
+#pragma unroll
+    for (uint32_t u = 0; u < PAIRS_PER_LANE; u++) {
+        const uint32_t p = 64 * u + lane;
+        ds.pair[u] = NONE32;
+        if (p < ds.pairs) {
+            uint32_t lo = 0, hi = ds.n;
+            while (hi - lo > 1) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if (ws.cum[mid] <= p) lo = mid;
+                else hi = mid;
+            }
+            ds.pair[u] = ((ws.srcoff[lo] + (p - ws.cum[lo])) << 8) | lo;
+        }
+    }
 }
 
 __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
@@ -303,26 +323,18 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     // ends before t0; possibly not folded into the source's row yet)
     uint32_t n_arr = 0, n_unf = 0;
     if (k >= 1) {
-        for (uint32_t g0 = 0; g0 < ds.pairs; g0 += 64 * PAIR_GROUP) {
+#pragma unroll
+        for (uint32_t g = 0; g < PAIRS_PER_LANE; g += PAIR_GROUP) {
+            if (64 * g >= ds.pairs) break;
             uint64_t e1[PAIR_GROUP], e2[PAIR_GROUP];
-            uint32_t jj[PAIR_GROUP];
 #pragma unroll
             for (uint32_t u = 0; u < PAIR_GROUP; u++) {
-                const uint32_t p = g0 + 64 * u + lane;
                 e1[u] = NONE64;
                 e2[u] = NONE64;
-                jj[u] = 0;
-                if (p < ds.pairs) {
-                    uint32_t lo = 0, hi = n;
-                    while (hi - lo > 1) {
-                        const uint32_t mid = (lo + hi) >> 1;
-                        if (ws.cum[mid] <= p) lo = mid;
-                        else hi = mid;
-                    }
-                    jj[u] = lo;
-                    const uint32_t slot = ws.srcoff[lo] + (p - ws.cum[lo]);
-                    e1[u] = snap1[slot];
-                    if (k >= 2) e2[u] = snap2[slot];
+                const uint32_t pr = ds.pair[g + u];
+                if (pr != NONE32) {
+                    e1[u] = snap1[pr >> 8];
+                    if (k >= 2) e2[u] = snap2[pr >> 8];
                 }
             }
             bool a_ok[PAIR_GROUP], u_ok[PAIR_GROUP];
@@ -334,17 +346,18 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
 #pragma unroll
             for (uint32_t u = 0; u < PAIR_GROUP; u++) {
                 const uint64_t ma = __ballot(a_ok[u]), mu = __ballot(u_ok[u]);
+                const uint8_t j = (uint8_t)(ds.pair[g + u] & 0xFFu);
                 if (a_ok[u]) {
                     const uint32_t q = n_arr + lane_prefix(ma, lane);
                     ws.arr_end[q] = (uint32_t)e1[u];
                     ws.arr_c[q] = (uint32_t)(e1[u] >> 32);
-                    ws.arr_j[q] = (uint8_t)jj[u];
+                    ws.arr_j[q] = j;
                     ws.arr_need[q] = 1;
                 }
                 if (u_ok[u]) {
                     const uint32_t q = n_unf + lane_prefix(mu, lane);
                     ws.unf_c[q] = (uint32_t)(e2[u] >> 32);
-                    ws.unf_j[q] = (uint8_t)jj[u];
+                    ws.unf_j[q] = j;
                     ws.unf_need[q] = 1;
                 }
                 n_arr += (uint32_t)__popcll(ma);
@@ -409,7 +422,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 pos = w0 & ~1ull;
             }
             const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
-            for (uint32_t step = 0; step < PROBE_STEPS; step++) {
+            // with only a few scans, whole-wave scans are quicker than probes
+            const uint32_t steps = __popcll(__ballot(scanning)) <= FEW_SCANS ? 0u : PROBE_STEPS;
+            for (uint32_t step = 0; step < steps; step++) {
                 if (!__ballot(scanning)) break;
                 if (scanning) {
                     uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
@@ -453,14 +468,15 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     }
                 }
             }
-            if (scanning) scanned = (uint32_t)(pos - w0);
+            if (scanning) scanned = steps ? (uint32_t)(pos - w0) : 0u;
             acc.words += wave_sum(scanned);
             uint64_t cmask = __ballot(scanning);
             while (cmask) {
                 const int j = __builtin_ffsll((long long)cmask) - 1;
                 cmask &= cmask - 1;
                 const uint32_t sj = (uint32_t)__shfl((int)ds.src, j);
-                const uint32_t from = (uint32_t)(shfl64(pos, j) * 64);
+                // continue after the probed words (or from the cursor when nothing was probed)
+                const uint32_t from = steps ? (uint32_t)(shfl64(pos, j) * 64) : ws.cur[j];
                 uint64_t w = 0;
                 const uint32_t pj = wave_first_candidate(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
                 acc.words += w;
@@ -542,7 +558,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             acc.cstar = max(acc.cstar, wave_max(ce));
             wave_sync();
             // the delivered chunks are no longer needed: clear their flags
-            for (uint64_t wm = wins; wm; wm &= wm - 1) {
+            for (uint64_t wm = (n_arr | n_unf) ? wins : 0ull; wm; wm &= wm - 1) {
                 const uint32_t c = ws.pick[__builtin_ffsll((long long)wm) - 1];
                 for (uint32_t q = lane; q < n_arr; q += 64)
                     if (ws.arr_c[q] == c) ws.arr_need[q] = 0;
