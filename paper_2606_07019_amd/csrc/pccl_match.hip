@@ -49,7 +49,7 @@ constexpr uint32_t K_NONE = 0, K_BUSY = 1, K_IDLE = 2;
 constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
 constexpr uint32_t PROBE_STEPS = 4;  // lane-parallel probe steps before the whole wave helps
-constexpr uint32_t PAIR_GROUP = 4;   // arrival-list entries per lane whose loads are in flight together
+constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose loads are in flight together
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
 constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
@@ -59,7 +59,7 @@ static_assert(MAXIN == 64, "one lane per in-link");
 // Per-wavefront scratch (one destination at a time).  When every wave owns
 // one destination for the whole run, the per-link part persists across
 // windows (no reload).
-struct WaveShared {
+struct alignas(16) WaveShared {
     uint32_t src[MAXIN], srcoff[MAXIN], tim[MAXIN], link[MAXIN];
     uint32_t cur[MAXIN], pick[MAXIN], mode[MAXIN], kind[MAXIN];
     uint32_t cum[MAXIN + 1];
@@ -224,6 +224,8 @@ struct Dest {
     uint32_t d, base, n, pairs;
     uint32_t src, tim;          // this lane's in-link (lane < n)
     uint32_t busy, infl, idle;  // its state
+    uint32_t ready;             // the cursor points at a candidate found ahead of time
+    uint32_t fold;              // chunk delivered into d in the previous window, still to fold
     unsigned long long log;     // next send-log slot of d
     // arrival pairs p = 64 u + lane: slot of the source's in-link, and the
     // in-link of d it feeds (slot << 8 | j; NONE32 past the last pair)
@@ -243,6 +245,8 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
     ds.busy = 0;
     ds.infl = NONE32;
     ds.idle = 0;
+    ds.ready = 0;
+    ds.fold = NONE32;
     if (lane < ds.n) {
         const uint32_t sl = ds.base + lane;
         ds.src = ly.slot_src[sl];
@@ -250,6 +254,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
         ds.busy = ly.busy[sl];
         ds.infl = ly.infl[sl];
         ds.idle = ly.lflags[sl] & 1u;
+        ds.ready = (ly.lflags[sl] >> 1) & 1u;
         ws.src[lane] = ds.src;
         ws.srcoff[lane] = ly.in_off[ds.src];
         ws.tim[lane] = ds.tim;
@@ -283,7 +288,7 @@ __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
         ly.busy[sl] = ds.busy;
         ly.infl[sl] = ds.infl;
         ly.cur[sl] = ws.cur[lane];
-        ly.lflags[sl] = ds.idle;
+        ly.lflags[sl] = ds.idle | (ds.ready << 1);
     }
     if (lane == 0) ly.dest_log[ds.d] = ds.log;
     wave_sync();
@@ -291,7 +296,7 @@ __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
 
 // All events of window [t0, t1) for one destination, by one wavefront.
 __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws, Dest &ds, uint32_t k,
-                               uint32_t t0, uint64_t t1, Acc &acc)
+                               uint32_t t0, uint64_t t1, bool resident, Acc &acc)
 {
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t n = ds.n, d = ds.d;
@@ -306,16 +311,19 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     const bool mine = lane < n;
     const uint32_t sl = ds.base + lane;
 
-    // fold the arrivals of window k-1 into d's holds row
+    // fold the arrivals of window k-1 into d's holds row (a resident wave
+    // remembers them; otherwise they are the snapshot entries that ended)
     if (mine) {
         ws.mode[lane] = M_IDLE;
-        if (k >= 2) {
+        uint32_t r = NONE32;
+        if (resident) {
+            r = ds.fold;
+        } else if (k >= 2) {
             const uint64_t e = snap2[sl];
-            if (e != NONE64 && (uint32_t)e < t0) {
-                const uint32_t r = (uint32_t)(e >> 32);
-                atomicOr((unsigned long long *)&hd[r >> 6], 1ull << (r & 63));
-            }
+            if (e != NONE64 && (uint32_t)e < t0) r = (uint32_t)(e >> 32);
         }
+        if (r != NONE32) atomicOr((unsigned long long *)&hd[r >> 6], 1ull << (r & 63));
+        ds.fold = NONE32;
     }
 
     // arrivals at the sources of d's in-links that d needs: this window's
@@ -389,6 +397,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 md = M_FULL;
             } else if (ds.infl != NONE32 && ds.busy == t) {
                 md = M_FULL;
+                ds.fold = ds.infl;
                 ds.infl = NONE32;
             }
             ws.mode[lane] = md;
@@ -519,9 +528,16 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             if (act) {
                 win = true;
                 const uint32_t li = ws.link[lane];
-                for (uint32_t j = 0; j < n; j++) {
-                    if (j == lane || ws.pick[j] != pk) continue;
-                    if (ws.tim[j] < ds.tim || (ws.tim[j] == ds.tim && ws.link[j] < li)) win = false;
+                for (uint32_t j4 = 0; j4 < n; j4 += 4) {
+                    const uint4 pp = *reinterpret_cast<const uint4 *>(&ws.pick[j4]);
+                    const uint32_t pv[4] = {pp.x, pp.y, pp.z, pp.w};
+#pragma unroll
+                    for (uint32_t q = 0; q < 4; q++) {
+                        const uint32_t j = j4 + q;
+                        if (j < n && j != lane && pv[q] == pk &&
+                            (ws.tim[j] < ds.tim || (ws.tim[j] == ds.tim && ws.link[j] < li)))
+                            win = false;
+                    }
                 }
             }
             const uint64_t wins = __ballot(win);
@@ -536,6 +552,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     ds.infl = pk;
                     ds.busy = e32;
                     ds.idle = 0;
+                    ds.ready = 0;
                     ce = e32;
                     const uint32_t q = n_send + lane_prefix(wins, lane);
                     ws.snd_link[q] = ws.link[lane];
@@ -585,6 +602,79 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         t_prev = t;
     }
 
+    // look ahead for busy links: one probe step from the cursor (plus the
+    // listed arrivals), so that the scan at completion starts at the next
+    // candidate.  The cursor stays a lower bound: candidates only appear
+    // through arrivals, which lower it when they come.
+    {
+        bool pf = false;
+        uint32_t p = NONE32;
+        uint64_t pos = 0, w0 = 0;
+        if (mine && ds.infl != NONE32 && !ds.ready) {
+            const uint32_t cur = ws.cur[lane];
+            w0 = cur >> 6;
+            pf = w0 < Wp;
+            if (pf) {
+                pos = w0 & ~1ull;
+                const uint64_t keep0 = ~0ull << (cur & 63);
+                const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
+                uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
+#pragma unroll
+                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                    const uint64_t idx = pos + 2 * u;
+                    if (idx < Wp) {
+                        hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
+                        nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
+                    } else {
+                        hv[u] = make_uint4(0, 0, 0, 0);
+                        nv[u] = make_uint4(0, 0, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                    const uint64_t idx = pos + 2 * u;
+                    uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
+                    if (idx < w0) x = 0;
+                    else if (idx == w0) x &= keep0;
+                    if (idx + 1 < w0) y = 0;
+                    else if (idx + 1 == w0) y &= keep0;
+                    if (p == NONE32) {
+                        if (x) p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
+                        else if (y) p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
+                    }
+                }
+            }
+        }
+        if (__ballot(pf)) {
+            if (mine) ws.pick[lane] = pf ? p : NONE32;
+            ws.kind[lane] = pf ? 1u : 0u;
+            wave_sync();
+            for (uint32_t q = lane; q < n_arr; q += 64) {
+                const uint32_t j = ws.arr_j[q], c = ws.arr_c[q];
+                if (ws.arr_need[q] && ws.kind[j] && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
+            }
+            for (uint32_t q = lane; q < n_unf; q += 64) {
+                const uint32_t j = ws.unf_j[q], c = ws.unf_c[q];
+                if (ws.unf_need[q] && ws.kind[j] && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
+            }
+            wave_sync();
+            if (pf) {
+                // only the probed words are known empty: a listed arrival
+                // beyond them does not let the cursor skip unprobed words
+                const uint64_t end_w = pos + PROBE_WORDS;
+                const uint32_t probed = end_w >= Wp ? END : (uint32_t)(end_w * 64);
+                const uint32_t pk = ws.pick[lane];
+                if (pk < probed) {
+                    ws.cur[lane] = pk;
+                    ds.ready = 1;
+                } else {
+                    ws.cur[lane] = probed;
+                }
+            }
+            wave_sync();
+        }
+    }
+
     // this window's snapshot and sends
     if (mine) snap0[sl] = ds.infl != NONE32 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64;
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
@@ -631,11 +721,11 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         acc.tmin = NONE32;
         const unsigned long long sent0 = acc.sent;
         if (resident) {
-            if (gwave < sz.D) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, acc);
+            if (gwave < sz.D) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc);
         } else {
             for (uint32_t d = gwave; d < sz.D; d += nwaves) {
                 load_dest(ly, ws, d, ds);
-                process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, acc);
+                process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc);
                 store_dest(ly, ws, ds);
             }
         }
