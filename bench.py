@@ -33,6 +33,28 @@ BYTES_PER_SCANNED_WORD = 16
 BYTES_PER_MATCH = 68
 
 
+COUNTERS = os.path.join(ROOT, "profiles", "k_match_switch2level_512_a2a_hbm_counters.md")
+MATCH_SRC = os.path.join(ROOT, "paper_2606_07019_amd", "csrc", "pccl_match.hip")
+
+
+def measured_traffic(config: int):
+    """HBM bytes per k_match launch from the committed counter summary, or
+    None when the kernel source changed since the counters were taken."""
+    import hashlib
+    if config != 4 or not os.path.exists(COUNTERS):
+        return None
+    want, traffic = None, None
+    with open(COUNTERS) as f:
+        for line in f:
+            if "k_match source sha256:" in line:
+                want = line.split(":", 1)[1].strip()
+            elif "k_match traffic bytes per launch:" in line:
+                traffic = int(line.split(":", 1)[1].strip())
+    with open(MATCH_SRC, "rb") as f:
+        have = hashlib.sha256(f.read()).hexdigest()
+    return traffic if want == have else None
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -67,7 +89,19 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (to scale HBM counters)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration << 18  # int32 elements
+        src = torch.ones(n, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}), flush=True)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: the synthesis matcher runs on one GPU; there is no multi-GPU path "
@@ -108,7 +142,7 @@ def main():
     alg_bytes = BYTES_PER_SCANNED_WORD * prof["scan_words"] + BYTES_PER_MATCH * n
     achieved = alg_bytes / avg_match_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 3), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBPS, 6), "traffic": None,
+                "frac": round(achieved / PEAK_HBM_GBPS, 6), "traffic": measured_traffic(args.config),
                 "kernel": "k_match", "kernel_ms": round(avg_match_s * 1e3, 4),
                 "alg_bytes_per_launch": alg_bytes, "scan_words": prof["scan_words"], "matches": n}
 
