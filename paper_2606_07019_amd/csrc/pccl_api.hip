@@ -457,7 +457,7 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     const uint64_t n = h.n_log;
     if (c->op == PCCL_OP_ALLREDUCE && 2ull * h.cstar > 0xFFFFFFFFull)
         return fail(c, PCCL_ERANGE, "all-reduce time does not fit in 32 bits");
-    HIP_OR_FAIL(c, launch_output(c->ly, c->sz, c->op, n, st));
+    HIP_OR_FAIL(c, launch_output(c->ly, c->sz, c->op, n, h.cstar, st));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[3], st));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));
     for (int i = 0; i < 3; i++) HIP_OR_FAIL(c, hipEventElapsedTime(&c->stage_ms[i], c->ev[i], c->ev[i + 1]));

@@ -125,7 +125,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
 hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
 int match_max_grid(int device);
 int match_waves_per_block();
-hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st);
+hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st);
 // LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;
 // the sorted order ends up in buffer ly.ctl->sort_cur (read it on the device).
 hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_hi, uint32_t max_tiles,

@@ -226,32 +226,29 @@ __global__ void k_holds(Layout ly, Sizes sz)
 
 // needs = destinations plus the relays on their tree paths (the paths the
 // pruned BFS keeps, Sec. 4.3): walk parents from each destination up to the
-// source; a walk stops at a device whose bit another walk already set.
+// source.  A walk that meets a bit already set stops there: whoever set it
+// is a destination or a walk that continues upward.  Two walks may both
+// pass a device before either bit is visible; both then set it (harmless).
 __global__ void k_needs(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t *post)
 {
     if (ly.ctl->error) return;
     const uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t v = blockIdx.y;
-    unsigned long long added = 0;
-    if (k < sz.W) {
-        const uint64_t x0 = post[(uint64_t)v * sz.W + k] & ~pre[(uint64_t)v * sz.W + k] & tail_mask(k, sz);
-        for (uint64_t x = x0; x; x &= x - 1) {
-            const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
-            const uint32_t s = ly.chunk_src[c], row = ly.src_index[s], r = ly.rank[c];
-            const uint64_t bit = 1ull << (r & 63);
-            const uint32_t *par = ly.sp_parent + (uint64_t)row * sz.D;
-            uint32_t u = v;
-            for (uint32_t hop = 0; hop < sz.D && u != s && u < sz.D; hop++) {
-                const unsigned long long old =
-                    atomicOr((unsigned long long *)&ly.needs[(uint64_t)u * sz.Wp + (r >> 6)], bit);
-                if (old & bit) break;
-                added++;
-                u = par[u];
-            }
+    if (k >= sz.W) return;
+    const uint64_t x0 = post[(uint64_t)v * sz.W + k] & ~pre[(uint64_t)v * sz.W + k] & tail_mask(k, sz);
+    for (uint64_t x = x0; x; x &= x - 1) {
+        const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+        const uint32_t s = ly.chunk_src[c], row = ly.src_index[s], r = ly.rank[c];
+        const uint64_t bit = 1ull << (r & 63);
+        const uint32_t *par = ly.sp_parent + (uint64_t)row * sz.D;
+        uint32_t u = v;
+        for (uint32_t hop = 0; hop < sz.D && u != s && u < sz.D; hop++) {
+            unsigned long long *w = (unsigned long long *)&ly.needs[(uint64_t)u * sz.Wp + (r >> 6)];
+            if (hop > 0 && (*w & bit)) break;
+            atomicOr(w, bit);
+            u = par[u];
         }
     }
-    for (int off = 32; off; off >>= 1) added += __shfl_xor(added, off);
-    if ((threadIdx.x & 63) == 0 && added) atomicAdd(&ly.ctl->needs_total, added);
 }
 
 // Each destination gets a contiguous segment of the send log, as long as
@@ -293,6 +290,7 @@ __global__ void __launch_bounds__(1024) k_log_offsets(Layout ly, Sizes sz)
         ly.dest_log[v] = run;
         run += c;
     }
+    if (tid == 1023) ly.ctl->needs_total = part[1023];
 }
 
 __global__ void k_init_match(Layout ly, Sizes sz)

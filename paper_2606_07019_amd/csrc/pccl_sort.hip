@@ -5,7 +5,7 @@
 namespace pccl {
 namespace {
 
-// Per-tile digit histogram, stored digit-major: hist[digit * tiles + tile].
+// Per-tile digit histogram, stored tile-major: hist[tile * 256 + digit].
 __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles)
 {
     __shared__ uint32_t cnt[256];
@@ -19,46 +19,41 @@ __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, in
         if (i < n) atomicAdd(&cnt[(key[i] >> shift) & 255u], 1u);
     }
     __syncthreads();
-    ly.hist[(uint64_t)tid * tiles + tile] = cnt[tid];
+    ly.hist[(uint64_t)tile * 256 + tid] = cnt[tid];
 }
 
-// Exclusive scan of the histogram (one workgroup), and the skip decision:
-// a pass whose digit is the same for every element is a no-op.
-__global__ void __launch_bounds__(1024) k_scan(Layout ly, uint64_t n, uint32_t tiles)
+// Exclusive scan of the histogram (one workgroup, one thread per digit),
+// in (digit, tile) order, and the skip decision: a pass whose digit is the
+// same for every element is a no-op.
+__global__ void __launch_bounds__(256) k_scan(Layout ly, uint64_t n, uint32_t tiles)
 {
-    __shared__ uint32_t part[1024];
-    const uint32_t tid = threadIdx.x;
-    const uint64_t total = 256ull * tiles;
-    const uint64_t per = (total + 1023) / 1024;
-    const uint64_t lo = tid * per, hi = lo + per < total ? lo + per : total;
-    uint32_t s = 0;
-    for (uint64_t i = lo; i < hi; i++) s += ly.hist[i];
-    part[tid] = s;
+    __shared__ uint32_t part[256];
+    __shared__ uint32_t skip;
+    const uint32_t d = threadIdx.x;
+    uint32_t tot = 0;
+#pragma unroll 8
+    for (uint32_t t = 0; t < tiles; t++) tot += ly.hist[(uint64_t)t * 256 + d];
+    part[d] = tot;
+    if (d == 0) skip = 0;
     __syncthreads();
-    for (uint32_t off = 1; off < 1024; off <<= 1) {
-        uint32_t v = tid >= off ? part[tid - off] : 0;
+    if (tot == (uint32_t)n) skip = 1;
+    for (uint32_t off = 1; off < 256; off <<= 1) {
+        const uint32_t v = d >= off ? part[d - off] : 0;
         __syncthreads();
-        part[tid] += v;
+        part[d] += v;
         __syncthreads();
     }
-    uint32_t run = tid ? part[tid - 1] : 0;
-    for (uint64_t i = lo; i < hi; i++) {
-        uint32_t v = ly.hist[i];
+    uint32_t run = part[d] - tot;
+#pragma unroll 8
+    for (uint32_t t = 0; t < tiles; t++) {
+        const uint64_t i = (uint64_t)t * 256 + d;
+        const uint32_t v = ly.hist[i];
         ly.hist[i] = run;
         run += v;
     }
     __syncthreads();
-    __shared__ uint32_t skip;
-    if (tid == 0) skip = 0;
-    __syncthreads();
-    if (tid < 256) {
-        uint32_t start = ly.hist[(uint64_t)tid * tiles];
-        uint32_t end = tid < 255 ? ly.hist[(uint64_t)(tid + 1) * tiles] : (uint32_t)n;
-        if (end - start == (uint32_t)n) skip = 1;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        uint32_t cur = ly.ctl->sort_cur;
+    if (d == 0) {
+        const uint32_t cur = ly.ctl->sort_cur;
         ly.ctl->sort_src = cur;
         ly.ctl->sort_skip = skip;
         ly.ctl->sort_cur = skip ? cur : cur ^ 1u;
@@ -79,7 +74,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
     const uint32_t *vin = ly.sval[src];
     uint64_t *kout = ly.skey[src ^ 1u];
     uint32_t *vout = ly.sval[src ^ 1u];
-    run[tid] = ly.hist[(uint64_t)tid * tiles + tile];
+    run[tid] = ly.hist[(uint64_t)tile * 256 + tid];
     for (uint32_t w = 0; w < SORT_THREADS / 64; w++) wc[w][tid] = 0;
     __syncthreads();
     const uint64_t base = (uint64_t)tile * SORT_TILE;
@@ -168,7 +163,7 @@ hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_
     if (tiles > max_tiles) return hipErrorInvalidValue;
     for (int b = byte_lo; b < byte_hi; b++) {
         k_hist<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
-        k_scan<<<1, 1024, 0, st>>>(ly, n, tiles);
+        k_scan<<<1, 256, 0, st>>>(ly, n, tiles);
         k_scatter<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
     }
     return hipGetLastError();
@@ -186,9 +181,12 @@ static int bytes_for(uint64_t maxval)
 
 // Output stage: the send log (n entries, key t_start << 32 | link, value
 // rank) is in sort buffer 0.  Writes the canonical schedule to ly.out.
-hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st)
+hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st)
 {
+    // only the significant bytes of the link id (low word) and of the start
+    // time (high word, start times are below the collective time) are sorted
     const int link_bytes = bytes_for(sz.L ? sz.L - 1 : 0);
+    const int time_bytes = bytes_for(cstar);
     const int threads = 256;
     const uint64_t blocks = (n + threads - 1) / threads;
     hipError_t e;
@@ -196,7 +194,7 @@ hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, 
         // forward schedule sorted by (t_start, link)
         e = radix_sort_pairs(ly, n, 0, link_bytes, sz.max_tiles, true, st);
         if (e != hipSuccess) return e;
-        e = radix_sort_pairs(ly, n, 4, 8, sz.max_tiles, false, st);
+        e = radix_sort_pairs(ly, n, 4, 4 + time_bytes, sz.max_tiles, false, st);
         if (e != hipSuccess) return e;
         if (n) {
             if (op == 0)
@@ -211,7 +209,7 @@ hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, 
         if (n) k_reverse_keys<<<blocks, threads, 0, st>>>(ly, n);
         e = radix_sort_pairs(ly, n, 0, link_bytes, sz.max_tiles, false, st);
         if (e != hipSuccess) return e;
-        e = radix_sort_pairs(ly, n, 4, 8, sz.max_tiles, false, st);
+        e = radix_sort_pairs(ly, n, 4, 4 + time_bytes, sz.max_tiles, false, st);
         if (e != hipSuccess) return e;
         if (n) k_out_copy<<<blocks, threads, 0, st>>>(ly, n, 0, 0, 1);
     }
