@@ -149,6 +149,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.lflags = cv.take<uint32_t>(L);
     ly.snap = cv.take<uint64_t>(3 * L);
     ly.dest_log = cv.take<unsigned long long>(D);
+    ly.xslot = cv.take<uint64_t>(4ull * MAX_MATCH_GRID);
     ly.out = cv.take<pccl_send>((c->op == PCCL_OP_ALLREDUCE ? 2 : 1) * max_sends);
     total = (cv.off + 255) & ~size_t(255);
 }
@@ -370,7 +371,8 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     c->stream = static_cast<hipStream_t>(hip_stream);
     HIP_OR_FAIL(c, hipSetDevice(c->device));
     const int wpb = match_waves_per_block();
-    c->grid = std::min<int>(match_max_grid(c->device), (int)((std::max<uint32_t>(c->D, 1) + wpb - 1) / wpb));
+    c->grid = std::min<int>(std::min<int>(match_max_grid(c->device), (int)MAX_MATCH_GRID),
+                            (int)((std::max<uint32_t>(c->D, 1) + wpb - 1) / wpb));
     if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
     c->have_ws = true;
     c->uploaded = c->have_result = false;

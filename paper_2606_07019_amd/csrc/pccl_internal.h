@@ -18,6 +18,7 @@ constexpr uint32_t MATCH_THREADS = 512;   // 8 wavefronts, one destination devic
 constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one device (one lane each)
 constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of their sources' in-degree
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
+constexpr uint32_t MAX_MATCH_GRID = 1024; // workgroups of the matching kernel (window exchange slots)
 
 // Status codes mirrored from the public header.
 enum : uint32_t {
@@ -36,19 +37,12 @@ struct Control {
     unsigned long long rounds, clashes, windows;
     unsigned long long scan_words;       // words of each row read by the intersect
     uint32_t n_sources;      // distinct chunk sources
-    uint32_t barrier;        // grid barrier arrival counter (monotonic)
-    uint32_t release;        // grid barrier generation, bumped by the last arrival
-    uint32_t abort;          // set when a barrier wait times out
+    uint32_t abort;          // set when a window exchange wait times out
     uint32_t cstar;          // collective time of the copy schedule
-    // per-window slots, indexed by window number mod 3 so that a slot is
-    // never written while a slow workgroup may still read it
-    uint32_t win_t0[3];      // start of window k+1, accumulated by atomicMin in window k
-    uint32_t win_err[3];     // an error was recorded in window k
-    unsigned long long win_sent[3];  // transfers committed in window k
     uint32_t sort_cur;       // radix sort: buffer holding the current order
     uint32_t sort_src;       // radix sort: buffer read by the pending scatter
     uint32_t sort_skip;      // radix sort: pending pass is a no-op
-    uint32_t pad[2];
+    uint32_t pad[1];
 };
 
 __device__ inline void record_error(Control *ctl, uint32_t code, uint32_t a = 0, uint32_t b = 0,
@@ -104,6 +98,7 @@ struct Layout {
     uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
     uint64_t *snap;           // [3 * L] by slot
     unsigned long long *dest_log;  // [D] next send-log slot of each destination
+    uint64_t *xslot;          // [2 * MAX_MATCH_GRID * 2] window exchange slots of the matching kernel
     // output
     void *out;                // pccl_send [2 * max_sends]
     Control *ctl;

@@ -69,12 +69,7 @@ struct alignas(16) WaveShared {
     uint32_t snd_link[MAXIN], snd_rank[MAXIN], snd_t[MAXIN];
 };
 
-struct BlockShared {
-    WaveShared w[NWAVES];
-    uint32_t red_tmin[NWAVES];
-    unsigned long long red_sent[NWAVES];
-    uint32_t barrier_ok;
-};
+
 
 __device__ inline void wave_sync()
 {
@@ -103,6 +98,16 @@ __device__ inline uint32_t wave_max(uint32_t v)
 __device__ inline uint32_t wave_sum(uint32_t v)
 {
     for (int off = 32; off; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off);
+    return v;
+}
+
+__device__ inline unsigned long long wave_sum64(unsigned long long v)
+{
+    for (int off = 32; off; off >>= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off);
+        v += ((unsigned long long)hi << 32) | lo;
+    }
     return v;
 }
 
@@ -172,50 +177,96 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
 // Grid-wide barrier: arrivals on a monotonic counter; the last arrival bumps
 // a separate release word that the others poll.  Returns false when the
 // wait timed out or another workgroup gave up (then the kernel ends).
-__device__ bool grid_barrier(Control *ctl, BlockShared &sh, uint32_t gen)
+// Grid-wide exchange at the end of window `gen`, which is also the grid
+// barrier: every workgroup publishes its results in its own two 64-bit
+// slots, each tagged with gen+1 (16 bits): (tag, error flag, earliest
+// transfer end) and (tag, transfers committed).  Wave 0 of every workgroup
+// then polls all slots, one per lane, until each carries the tag, and
+// reduces them itself.  Slots alternate with the window parity: a workgroup
+// can run at most one window ahead of the slowest poller, so it never
+// overwrites a slot that is still being read.  No atomic read-modify-write
+// and no second round trip to release the waiters.
+struct Exchange {
+    uint32_t tn;              // start of the next window (earliest transfer end), NONE32 if none
+    uint32_t err;             // some workgroup recorded an error
+    unsigned long long sent;  // transfers committed in the window, grid-wide
+    uint32_t ok;              // 0 if the wait was abandoned
+};
+
+struct BlockShared {
+    WaveShared w[NWAVES];
+    uint32_t red_tmin[NWAVES], red_err[NWAVES];
+    unsigned long long red_sent[NWAVES];
+    Exchange ex;
+};
+
+__device__ bool window_exchange(Control *ctl, uint64_t *xslot, BlockShared &sh, uint32_t gen, uint32_t tmin,
+                                unsigned long long sent, uint32_t err, Exchange &ex)
 {
+    const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
+    const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFFu) << 48;
+    uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * 2;
+    // every wave's global writes of this window are complete before the workgroup publishes
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t nb = gridDim.x;
-        uint32_t ok = 1;
+    if (threadIdx.x < 64) {
         __threadfence();
-        const uint32_t old = atomicAdd(&ctl->barrier, 1u);
-        if (old + 1u == (gen + 1u) * nb) {
-            __hip_atomic_store(&ctl->release, gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            uint32_t spins = 0;
-            while (true) {
-                const uint32_t v = __hip_atomic_load(&ctl->release, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if ((int32_t)(v - (gen + 1u)) >= 0) break;
-                if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                    ok = 0;
-                    break;
-                }
-                if (++spins > SPIN_LIMIT) {
-                    atomicExch(&ctl->abort, 1u);
-                    ok = 0;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
+        // the L2 write-back of the fence has completed before the slots are written
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (lane == 0) {
+            __hip_atomic_store(&slot[2 * blockIdx.x], tag | ((uint64_t)(err ? 1u : 0u) << 47) | tmin,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&slot[2 * blockIdx.x + 1], tag | sent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        uint32_t spins = 0, ok = 1;
+        uint32_t tn = NONE32, e = 0;
+        unsigned long long s = 0;
+        while (true) {
+            bool all = true;
+            tn = NONE32;
+            e = 0;
+            s = 0;
+            for (uint32_t b = lane; b < nb; b += 64) {
+                const uint64_t a = __hip_atomic_load(&slot[2 * b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint64_t c = __hip_atomic_load(&slot[2 * b + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((a & (0xFFFFull << 48)) != tag || (c & (0xFFFFull << 48)) != tag) all = false;
+                tn = min(tn, (uint32_t)a);
+                e |= (uint32_t)(a >> 47) & 1u;
+                s += c & ((1ull << 47) - 1ull);
             }
+            if (__ballot(!all) == 0) break;
+            if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                ok = 0;
+                break;
+            }
+            if (++spins > SPIN_LIMIT) {
+                if (lane == 0) atomicExch(&ctl->abort, 1u);
+                ok = 0;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
         }
         __threadfence();
-        sh.barrier_ok = ok;
+        tn = wave_min(tn);
+        e = __ballot(e != 0) ? 1u : 0u;
+        s = wave_sum64(s);
+        if (lane == 0) {
+            sh.ex.tn = tn;
+            sh.ex.err = e;
+            sh.ex.sent = s;
+            sh.ex.ok = ok;
+        }
     }
     __syncthreads();
-    return sh.barrier_ok != 0;
-}
-
-__device__ inline void window_error(Control *ctl, uint32_t k, uint32_t code, uint32_t a, uint32_t b, uint32_t c)
-{
-    record_error(ctl, code, a, b, c);
-    atomicOr(&ctl->win_err[k % 3], 1u);
+    ex = sh.ex;
+    return ex.ok != 0;
 }
 
 // Per-wavefront accumulators, kept identical on every lane.
 struct Acc {
     uint32_t tmin;     // earliest end among transfers in flight on this wave's links
     uint32_t cstar;    // latest transfer end committed by this wave
+    uint32_t err;      // this wave recorded an error
     unsigned long long sent, rounds, clashes, words;
 };
 
@@ -543,11 +594,15 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             const uint64_t wins = __ballot(win);
             const uint64_t losers = __ballot(act && !win);
             uint32_t ce = 0;
+            bool overflow = false;
             if (act) {
                 if (win) {
                     atomicAnd((unsigned long long *)&nd[pk >> 6], ~(1ull << (pk & 63)));
                     const uint64_t end = (uint64_t)t + ds.tim;
-                    if (end > 0xFFFFFFFFull) window_error(ly.ctl, k, ST_ERANGE, pk, d, 2);
+                    if (end > 0xFFFFFFFFull) {
+                        record_error(ly.ctl, ST_ERANGE, pk, d, 2);
+                        overflow = true;
+                    }
                     const uint32_t e32 = end > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)end;
                     ds.infl = pk;
                     ds.busy = e32;
@@ -573,6 +628,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             n_send += (uint32_t)__popcll(wins);
             acc.clashes += (unsigned long long)__popcll(losers);
             acc.cstar = max(acc.cstar, wave_max(ce));
+            if (__ballot(overflow)) acc.err = 1;
             wave_sync();
             // the delivered chunks are no longer needed: clear their flags
             for (uint64_t wm = (n_arr | n_unf) ? wins : 0ull; wm; wm &= wm - 1) {
@@ -707,17 +763,12 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     WaveShared &ws = sh.w[wave];
     Dest ds{};
     if (resident && gwave < sz.D) load_dest(ly, ws, gwave, ds);
-    Acc acc = {NONE32, 0u, 0ull, 0ull, 0ull, 0ull};
+    Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull};
     unsigned long long remaining = ctl->needs_total;
     uint32_t t0 = 0;
     unsigned long long k = 0;
     for (;; k++) {
         const uint64_t t1 = (uint64_t)t0 + sz.tmin;
-        if (blockIdx.x == 0 && tid == 0) {
-            ctl->win_t0[(k + 2) % 3] = NONE32;
-            ctl->win_sent[(k + 1) % 3] = 0;
-            ctl->win_err[(k + 1) % 3] = 0;
-        }
         acc.tmin = NONE32;
         const unsigned long long sent0 = acc.sent;
         if (resident) {
@@ -731,27 +782,22 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         if (lane == 0) {
             sh.red_tmin[wave] = acc.tmin;
+            sh.red_err[wave] = acc.err;
             sh.red_sent[wave] = acc.sent - sent0;
         }
         __syncthreads();
-        if (tid == 0) {
-            uint32_t bmin = NONE32;
-            unsigned long long sent = 0;
-            for (uint32_t w = 0; w < NWAVES; w++) {
-                bmin = min(bmin, sh.red_tmin[w]);
-                sent += sh.red_sent[w];
-            }
-            if (bmin != NONE32) atomicMin(&ctl->win_t0[(k + 1) % 3], bmin);
-            if (sent) atomicAdd(&ctl->win_sent[k % 3], sent);
+        uint32_t bmin = NONE32, berr = 0;
+        unsigned long long bsent = 0;
+        for (uint32_t w = 0; w < NWAVES; w++) {
+            bmin = min(bmin, sh.red_tmin[w]);
+            berr |= sh.red_err[w];
+            bsent += sh.red_sent[w];
         }
-        if (!grid_barrier(ctl, sh, (uint32_t)k)) break;
-        const uint32_t err = __hip_atomic_load(&ctl->win_err[k % 3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned long long done =
-            __hip_atomic_load(&ctl->win_sent[k % 3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const uint32_t tn = __hip_atomic_load(&ctl->win_t0[(k + 1) % 3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        remaining -= done;
-        if (err || remaining == 0) break;
-        if (tn == NONE32) {
+        Exchange ex;
+        if (!window_exchange(ctl, ly.xslot, sh, (uint32_t)k, bmin, bsent, berr, ex)) break;
+        remaining -= ex.sent;
+        if (ex.err || remaining == 0) break;
+        if (ex.tn == NONE32) {
             record_error(ctl, ST_EDEADLOCK, (uint32_t)remaining, 0, 0);
             break;
         }
@@ -759,7 +805,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
             record_error(ctl, ST_EINTERNAL, 1, 0, 0);
             break;
         }
-        t0 = tn;
+        t0 = ex.tn;
     }
     if (blockIdx.x == 0 && tid == 0) {
         ctl->needs_remaining = remaining;

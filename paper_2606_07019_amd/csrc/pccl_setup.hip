@@ -29,9 +29,6 @@ __global__ void k_ctl_reset(Control *ctl, unsigned long long max_sends)
 {
     Control c = {};
     c.max_sends = max_sends;
-    c.win_t0[0] = 0;
-    c.win_t0[1] = NONE32;
-    c.win_t0[2] = NONE32;
     *ctl = c;
 }
 
@@ -305,6 +302,7 @@ __global__ void k_init_match(Layout ly, Sizes sz)
         ly.snap[sz.L + i] = NONE64;
         ly.snap[2ull * sz.L + i] = NONE64;
     }
+    if (i < 4ull * MAX_MATCH_GRID) ly.xslot[i] = 0;
     if (i == 0) {
         Control *ctl = ly.ctl;
         ctl->needs_remaining = ctl->needs_total;
@@ -351,7 +349,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
     if (sz.W) k_needs<<<gw, T, 0, st>>>(ly, sz, pre, post);
     k_needs_count<<<sz.D, 256, 0, st>>>(ly, sz);
     k_log_offsets<<<1, 1024, 0, st>>>(ly, sz);
-    k_init_match<<<blocks_for(sz.L ? sz.L : 1, T), T, 0, st>>>(ly, sz);
+    k_init_match<<<blocks_for(std::max<uint64_t>(sz.L, 4ull * MAX_MATCH_GRID), T), T, 0, st>>>(ly, sz);
     return hipGetLastError();
 }
 
