@@ -25,6 +25,7 @@ struct pccl_ctx {
     uint32_t N = 0, S = 0, D = 0, L = 0;
     std::vector<uint32_t> src, dst, alpha, bw;
     std::vector<uint32_t> in_off, slot_link, slot_src, slot_cum, dest_pairs, rev;
+    std::vector<uint32_t> wave_dest;  // destination of (pass, wave) in the matching kernel
     // collective
     uint32_t C = 0, G = 0;
     uint64_t m = 0;
@@ -150,8 +151,31 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.snap = cv.take<uint64_t>(3 * L);
     ly.dest_log = cv.take<unsigned long long>(D);
     ly.xslot = cv.take<uint64_t>(4ull * MAX_MATCH_GRID);
+    ly.wave_dest = cv.take<uint32_t>(D + (uint64_t)MATCH_WAVES * MAX_MATCH_GRID);
     ly.out = cv.take<pccl_send>((c->op == PCCL_OP_ALLREDUCE ? 2 : 1) * max_sends);
     total = (cv.off + 255) & ~size_t(255);
+}
+
+// Destinations of the matching kernel's waves: heaviest first (most arrival
+// pairs, then most in-links), dealt across workgroups before filling any
+// workgroup's second wave, so that heavy destinations (switches) do not share
+// a compute unit and its memory pipeline.  Pass r of wave w handles entry
+// r * nwaves + w.
+void deal_destinations(pccl_ctx *c)
+{
+    const uint32_t D = c->D, nb = (uint32_t)c->grid, nw = nb * MATCH_WAVES;
+    std::vector<uint32_t> byweight(D);
+    for (uint32_t v = 0; v < D; v++) byweight[v] = v;
+    std::stable_sort(byweight.begin(), byweight.end(), [&](uint32_t a, uint32_t b) {
+        if (c->dest_pairs[a] != c->dest_pairs[b]) return c->dest_pairs[a] > c->dest_pairs[b];
+        return c->in_off[a + 1] - c->in_off[a] > c->in_off[b + 1] - c->in_off[b];
+    });
+    const uint32_t passes = (D + nw - 1) / nw;
+    c->wave_dest.assign((size_t)std::max(passes, 1u) * nw, NONE32);
+    for (uint32_t i = 0; i < D; i++) {
+        const uint32_t r = i / nw, j = i % nw, w = (j % nb) * MATCH_WAVES + j / nb;
+        c->wave_dest[(size_t)r * nw + w] = byweight[i];
+    }
 }
 
 uint64_t safe_max_sends(const pccl_ctx *c)
@@ -374,6 +398,7 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     c->grid = std::min<int>(std::min<int>(match_max_grid(c->device), (int)MAX_MATCH_GRID),
                             (int)((std::max<uint32_t>(c->D, 1) + wpb - 1) / wpb));
     if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+    deal_destinations(c);
     c->have_ws = true;
     c->uploaded = c->have_result = false;
     return PCCL_OK;
@@ -399,6 +424,7 @@ static pccl_status upload(pccl_ctx *c)
     HIP_OR_FAIL(c, put(ly.slot_time, c->slot_time.data(), L4));
     HIP_OR_FAIL(c, put(ly.slot_cum, c->slot_cum.data(), L4));
     HIP_OR_FAIL(c, put(ly.dest_pairs, c->dest_pairs.data(), sizeof(uint32_t) * c->D));
+    HIP_OR_FAIL(c, put(ly.wave_dest, c->wave_dest.data(), sizeof(uint32_t) * c->wave_dest.size()));
     HIP_OR_FAIL(c, put(ly.group_masks, c->gmask.data(), sizeof(uint64_t) * c->gmask.size()));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));
     c->uploaded = true;

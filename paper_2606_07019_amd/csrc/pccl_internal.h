@@ -15,6 +15,7 @@ constexpr uint32_t ROW_ALIGN_WORDS = 128;
 
 // Matching kernel envelope (checked on the host when a topology is loaded).
 constexpr uint32_t MATCH_THREADS = 512;   // 8 wavefronts, one destination device each
+constexpr uint32_t MATCH_WAVES = MATCH_THREADS / 64;
 constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one device (one lane each)
 constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of their sources' in-degree
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
@@ -99,6 +100,7 @@ struct Layout {
     uint64_t *snap;           // [3 * L] by slot
     unsigned long long *dest_log;  // [D] next send-log slot of each destination
     uint64_t *xslot;          // [2 * MAX_MATCH_GRID * 2] window exchange slots of the matching kernel
+    uint32_t *wave_dest;      // [D + MATCH_WAVES * MAX_MATCH_GRID] destination of (pass, wave), NONE32 if none
     // output
     void *out;                // pccl_send [2 * max_sends]
     Control *ctl;

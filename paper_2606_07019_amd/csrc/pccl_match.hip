@@ -762,7 +762,9 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const bool resident = sz.D <= nwaves;
     WaveShared &ws = sh.w[wave];
     Dest ds{};
-    if (resident && gwave < sz.D) load_dest(ly, ws, gwave, ds);
+    const uint32_t passes = (sz.D + nwaves - 1) / nwaves;
+    const uint32_t mine_d = resident ? ly.wave_dest[gwave] : NONE32;
+    if (mine_d != NONE32) load_dest(ly, ws, mine_d, ds);
     Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull};
     unsigned long long remaining = ctl->needs_total;
     uint32_t t0 = 0;
@@ -772,9 +774,11 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         acc.tmin = NONE32;
         const unsigned long long sent0 = acc.sent;
         if (resident) {
-            if (gwave < sz.D) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc);
+            if (mine_d != NONE32) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc);
         } else {
-            for (uint32_t d = gwave; d < sz.D; d += nwaves) {
+            for (uint32_t r = 0; r < passes; r++) {
+                const uint32_t d = ly.wave_dest[(uint64_t)r * nwaves + gwave];
+                if (d == NONE32) continue;
                 load_dest(ly, ws, d, ds);
                 process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc);
                 store_dest(ly, ws, ds);
