@@ -186,6 +186,12 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
 // can run at most one window ahead of the slowest poller, so it never
 // overwrites a slot that is still being read.  No atomic read-modify-write
 // and no second round trip to release the waiters.
+// Memory ordering: the writes of a window that other workgroups read (the
+// snapshot entries and the holds folds) are agent-scope atomics, coherent
+// without an L2 write-back; every wave waits for their completion before the
+// workgroup barrier, so they are performed before the slots are written.
+// After the wait, an acquire fence makes this compute unit's later plain
+// loads miss any line cached before the other workgroups wrote it.
 struct Exchange {
     uint32_t tn;              // start of the next window (earliest transfer end), NONE32 if none
     uint32_t err;             // some workgroup recorded an error
@@ -206,13 +212,10 @@ __device__ bool window_exchange(Control *ctl, uint64_t *xslot, BlockShared &sh, 
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
     const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFFu) << 48;
     uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * 2;
-    // every wave's global writes of this window are complete before the workgroup publishes
+    // every wave's global writes and atomics of this window have completed
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     __syncthreads();
     if (threadIdx.x < 64) {
-        __threadfence();
-        // the L2 write-back of the fence has completed before the slots are written
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         if (lane == 0) {
             __hip_atomic_store(&slot[2 * blockIdx.x], tag | ((uint64_t)(err ? 1u : 0u) << 47) | tmin,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -246,7 +249,8 @@ __device__ bool window_exchange(Control *ctl, uint64_t *xslot, BlockShared &sh, 
             }
             __builtin_amdgcn_s_sleep(1);
         }
-        __threadfence();
+        // acquire: this compute unit's caches drop lines other workgroups wrote
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         tn = wave_min(tn);
         e = __ballot(e != 0) ? 1u : 0u;
         s = wave_sum64(s);
@@ -373,7 +377,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             const uint64_t e = snap2[sl];
             if (e != NONE64 && (uint32_t)e < t0) r = (uint32_t)(e >> 32);
         }
-        if (r != NONE32) atomicOr((unsigned long long *)&hd[r >> 6], 1ull << (r & 63));
+        if (r != NONE32)
+            __hip_atomic_fetch_or(&hd[r >> 6], 1ull << (r & 63), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ds.fold = NONE32;
     }
 
@@ -732,7 +737,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     }
 
     // this window's snapshot and sends
-    if (mine) snap0[sl] = ds.infl != NONE32 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64;
+    if (mine)
+        __hip_atomic_store(&snap0[sl], ds.infl != NONE32 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
     if (n_send) {
         if (lane < n_send) {

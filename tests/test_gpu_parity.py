@@ -63,3 +63,22 @@ def test_reduction_ops_parity(op):
     wl = W.config2()
     wl.coll.op = op
     _compare(wl, f"torus reduce op {op}")
+
+
+@pytest.mark.parametrize("seed", list(range(100, 112)))
+def test_random_medium_parity(seed):
+    """Random topologies of 40..129 NPUs plus switches: several workgroups,
+    so the window exchange between workgroups is on the path."""
+    wl = W.random_small(seed, n_npus=40 + (seed * 37) % 90, n_switches=seed % 4, max_chunks=3000)
+    _compare(wl, f"medium fuzz seed {seed}")
+
+
+def test_more_destinations_than_waves_parity():
+    """A 50 x 44 mesh (2200 devices): more destinations than the matching
+    kernel has wavefronts on one MI355X (256 workgroups of 8), so waves
+    take several destinations per window and keep their state in memory."""
+    topo = W.mesh2d(50, 44)
+    rng = W.SplitMix64(7)
+    members = sorted(rng.shuffle(range(2200))[:16])
+    coll = W.all_gather(2200, members, 4, 1 << 16)
+    _compare(W.Workload("mesh50x44_allgather16", topo, coll, 11), "non-resident mesh")
