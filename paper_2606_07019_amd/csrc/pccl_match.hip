@@ -53,6 +53,7 @@ constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose load
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
 constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
+constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
 
 static_assert(MAXIN == 64, "one lane per in-link");
 
@@ -67,6 +68,8 @@ struct alignas(16) WaveShared {
     uint32_t unf_c[PAIRS];
     uint8_t arr_j[PAIRS], unf_j[PAIRS], arr_need[PAIRS], unf_need[PAIRS];
     uint32_t snd_link[MAXIN], snd_rank[MAXIN], snd_t[MAXIN];
+    // clash detection: lane that last wrote a hashed pick, and slots written twice
+    uint8_t clash_lane[CLASH_SLOTS], clash_hit[CLASH_SLOTS];
 };
 
 
@@ -107,6 +110,16 @@ __device__ inline unsigned long long wave_sum64(unsigned long long v)
         const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off);
         const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off);
         v += ((unsigned long long)hi << 32) | lo;
+    }
+    return v;
+}
+
+__device__ inline uint64_t wave_min64(uint64_t v)
+{
+    for (int off = 32; off; off >>= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off);
+        v = min(v, ((uint64_t)hi << 32) | lo);
     }
     return v;
 }
@@ -577,23 +590,35 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             }
             const bool act = mine && md != M_IDLE;
             if (!__ballot(act)) break;
-            // clash resolution among d's in-links: fastest link, then lowest id
+            // clash resolution among d's in-links: fastest link, then lowest id.
+            // Picks are hashed into a table of lane ids; a lane alone in its
+            // slot has no rival and wins.  Lanes sharing a slot are grouped by
+            // equal pick, and each group keeps its smallest (time, link id).
             if (mine) ws.pick[lane] = act ? pk : NONE32;
+            const uint32_t hs = act ? (pk * 2654435761u) >> 22 : 0u;
+            if (act) ws.clash_lane[hs] = (uint8_t)lane;
             wave_sync();
-            bool win = false;
-            if (act) {
-                win = true;
-                const uint32_t li = ws.link[lane];
-                for (uint32_t j4 = 0; j4 < n; j4 += 4) {
-                    const uint4 pp = *reinterpret_cast<const uint4 *>(&ws.pick[j4]);
-                    const uint32_t pv[4] = {pp.x, pp.y, pp.z, pp.w};
-#pragma unroll
-                    for (uint32_t q = 0; q < 4; q++) {
-                        const uint32_t j = j4 + q;
-                        if (j < n && j != lane && pv[q] == pk &&
-                            (ws.tim[j] < ds.tim || (ws.tim[j] == ds.tim && ws.link[j] < li)))
-                            win = false;
-                    }
+            bool rival = false;
+            if (act && ws.clash_lane[hs] != lane) {
+                rival = true;
+                ws.clash_hit[hs] = 1;
+            }
+            wave_sync();
+            if (act && ws.clash_hit[hs]) rival = true;
+            bool win = act && !rival;
+            uint64_t contested = __ballot(rival);
+            if (contested) {
+                wave_sync();
+                if (rival) ws.clash_hit[hs] = 0;
+                const uint64_t key = act ? (((uint64_t)ds.tim << 32) | ws.link[lane]) : NONE64;
+                while (contested) {
+                    const int j = __builtin_ffsll((long long)contested) - 1;
+                    const uint32_t v = (uint32_t)__shfl((int)pk, j);
+                    const uint64_t g = __ballot(act && pk == v);
+                    const bool in_g = (g >> lane) & 1ull;
+                    const uint64_t kmin = wave_min64(in_g ? key : NONE64);
+                    if (in_g) win = key == kmin;
+                    contested &= ~g;
                 }
             }
             const uint64_t wins = __ballot(win);
@@ -769,6 +794,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const bool resident = sz.D <= nwaves;
     WaveShared &ws = sh.w[wave];
     Dest ds{};
+    for (uint32_t i = lane; i < CLASH_SLOTS; i += 64) ws.clash_hit[i] = 0;
     const uint32_t passes = (sz.D + nwaves - 1) / nwaves;
     const uint32_t mine_d = resident ? ly.wave_dest[gwave] : NONE32;
     if (mine_d != NONE32) load_dest(ly, ws, mine_d, ds);
