@@ -362,9 +362,102 @@ __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
     wave_sync();
 }
 
+// Look-ahead for busy links: one probe step of PROBE_WORDS words from the
+// cursor, combined with the window's listed arrivals, so that the scan at
+// completion starts at the next candidate.  The cursor stays a lower bound:
+// candidates only appear through arrivals, which lower it when they come.
+// The loads are issued at the end of a window and, when the wave keeps its
+// destination, consumed at the start of the next one, so their round trip
+// overlaps the window exchange.  The lists of the issuing window stay in
+// LDS until then.
+struct LookAhead {
+    uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];  // the two rows' words from the even word below the cursor
+    uint32_t cur;           // cursor the words were loaded from, NONE32 if none
+    uint32_t n_arr, n_unf;  // list lengths of the issuing window
+};
+
+__device__ inline void look_ahead_issue(const Layout &ly, uint64_t Wp, const WaveShared &ws, const Dest &ds,
+                                        const uint64_t *nd, bool mine, uint32_t n_arr, uint32_t n_unf,
+                                        LookAhead &la)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    la.cur = NONE32;
+    la.n_arr = n_arr;
+    la.n_unf = n_unf;
+    if (!(mine && ds.infl != NONE32 && !ds.ready)) return;
+    const uint32_t cur = ws.cur[lane];
+    if ((cur >> 6) >= Wp) return;
+    la.cur = cur;
+    const uint64_t pos = (cur >> 6) & ~1u;
+    const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
+#pragma unroll
+    for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+        const uint64_t idx = pos + 2 * u;
+        if (idx < Wp) {
+            la.hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
+            la.nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
+        } else {
+            la.hv[u] = make_uint4(0, 0, 0, 0);
+            la.nv[u] = make_uint4(0, 0, 0, 0);
+        }
+    }
+}
+
+__device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, bool mine, LookAhead &la)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    const bool pf = mine && la.cur != NONE32;
+    if (!__ballot(pf)) return;
+    uint32_t p = NONE32;
+    const uint64_t w0 = la.cur >> 6, pos = w0 & ~1ull;
+    if (pf) {
+        const uint64_t keep0 = ~0ull << (la.cur & 63);
+#pragma unroll
+        for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+            const uint64_t idx = pos + 2 * u;
+            uint64_t x = u4lo(la.hv[u]) & u4lo(la.nv[u]), y = u4hi(la.hv[u]) & u4hi(la.nv[u]);
+            if (idx < w0) x = 0;
+            else if (idx == w0) x &= keep0;
+            if (idx + 1 < w0) y = 0;
+            else if (idx + 1 == w0) y &= keep0;
+            if (p == NONE32) {
+                if (x) p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
+                else if (y) p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
+            }
+        }
+    }
+    if (mine) ws.pick[lane] = pf ? p : NONE32;
+    ws.kind[lane] = pf ? 1u : 0u;
+    wave_sync();
+    for (uint32_t q = lane; q < la.n_arr; q += 64) {
+        const uint32_t j = ws.arr_j[q], c = ws.arr_c[q];
+        if (ws.arr_need[q] && ws.kind[j] && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
+    }
+    for (uint32_t q = lane; q < la.n_unf; q += 64) {
+        const uint32_t j = ws.unf_j[q], c = ws.unf_c[q];
+        if (ws.unf_need[q] && ws.kind[j] && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
+    }
+    wave_sync();
+    if (pf) {
+        // only the probed words are known empty: a listed arrival beyond
+        // them does not let the cursor skip unprobed words
+        const uint64_t end_w = pos + PROBE_WORDS;
+        const uint32_t probed = end_w >= Wp ? (uint32_t)(Wp * 64) : (uint32_t)(end_w * 64);
+        const uint32_t pk = ws.pick[lane];
+        if (pk < probed) {
+            ws.cur[lane] = pk;
+            ds.ready = 1;
+        } else {
+            ws.cur[lane] = probed;
+        }
+    }
+    la.cur = NONE32;
+    wave_sync();
+}
+
 // All events of window [t0, t1) for one destination, by one wavefront.
 __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws, Dest &ds, uint32_t k,
-                               uint32_t t0, uint64_t t1, bool resident, Acc &acc)
+                               uint32_t t0, uint64_t t1, bool resident, Acc &acc, LookAhead &la)
 {
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t n = ds.n, d = ds.d;
@@ -378,6 +471,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     uint64_t *snap0 = ly.snap + (uint64_t)(k % 3) * L;              // written for window k+1
     const bool mine = lane < n;
     const uint32_t sl = ds.base + lane;
+    // the look-ahead issued at the end of the last window
+    if (resident) look_ahead_finish(Wp, ws, ds, mine, la);
 
     // fold the arrivals of window k-1 into d's holds row (a resident wave
     // remembers them; otherwise they are the snapshot entries that ended)
@@ -688,78 +783,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         t_prev = t;
     }
 
-    // look ahead for busy links: one probe step from the cursor (plus the
-    // listed arrivals), so that the scan at completion starts at the next
-    // candidate.  The cursor stays a lower bound: candidates only appear
-    // through arrivals, which lower it when they come.
-    {
-        bool pf = false;
-        uint32_t p = NONE32;
-        uint64_t pos = 0, w0 = 0;
-        if (mine && ds.infl != NONE32 && !ds.ready) {
-            const uint32_t cur = ws.cur[lane];
-            w0 = cur >> 6;
-            pf = w0 < Wp;
-            if (pf) {
-                pos = w0 & ~1ull;
-                const uint64_t keep0 = ~0ull << (cur & 63);
-                const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
-                uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
-#pragma unroll
-                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
-                    const uint64_t idx = pos + 2 * u;
-                    if (idx < Wp) {
-                        hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
-                        nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
-                    } else {
-                        hv[u] = make_uint4(0, 0, 0, 0);
-                        nv[u] = make_uint4(0, 0, 0, 0);
-                    }
-                }
-#pragma unroll
-                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
-                    const uint64_t idx = pos + 2 * u;
-                    uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
-                    if (idx < w0) x = 0;
-                    else if (idx == w0) x &= keep0;
-                    if (idx + 1 < w0) y = 0;
-                    else if (idx + 1 == w0) y &= keep0;
-                    if (p == NONE32) {
-                        if (x) p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
-                        else if (y) p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
-                    }
-                }
-            }
-        }
-        if (__ballot(pf)) {
-            if (mine) ws.pick[lane] = pf ? p : NONE32;
-            ws.kind[lane] = pf ? 1u : 0u;
-            wave_sync();
-            for (uint32_t q = lane; q < n_arr; q += 64) {
-                const uint32_t j = ws.arr_j[q], c = ws.arr_c[q];
-                if (ws.arr_need[q] && ws.kind[j] && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
-            }
-            for (uint32_t q = lane; q < n_unf; q += 64) {
-                const uint32_t j = ws.unf_j[q], c = ws.unf_c[q];
-                if (ws.unf_need[q] && ws.kind[j] && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
-            }
-            wave_sync();
-            if (pf) {
-                // only the probed words are known empty: a listed arrival
-                // beyond them does not let the cursor skip unprobed words
-                const uint64_t end_w = pos + PROBE_WORDS;
-                const uint32_t probed = end_w >= Wp ? END : (uint32_t)(end_w * 64);
-                const uint32_t pk = ws.pick[lane];
-                if (pk < probed) {
-                    ws.cur[lane] = pk;
-                    ds.ready = 1;
-                } else {
-                    ws.cur[lane] = probed;
-                }
-            }
-            wave_sync();
-        }
-    }
+    look_ahead_issue(ly, Wp, ws, ds, nd, mine, n_arr, n_unf, la);
+    if (!resident) look_ahead_finish(Wp, ws, ds, mine, la);
 
     // this window's snapshot and sends
     if (mine)
@@ -799,6 +824,9 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const uint32_t mine_d = resident ? ly.wave_dest[gwave] : NONE32;
     if (mine_d != NONE32) load_dest(ly, ws, mine_d, ds);
     Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull};
+    LookAhead la;
+    la.cur = NONE32;
+    la.n_arr = la.n_unf = 0;
     unsigned long long remaining = ctl->needs_total;
     uint32_t t0 = 0;
     unsigned long long k = 0;
@@ -807,13 +835,13 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         acc.tmin = NONE32;
         const unsigned long long sent0 = acc.sent;
         if (resident) {
-            if (mine_d != NONE32) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc);
+            if (mine_d != NONE32) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc, la);
         } else {
             for (uint32_t r = 0; r < passes; r++) {
                 const uint32_t d = ly.wave_dest[(uint64_t)r * nwaves + gwave];
                 if (d == NONE32) continue;
                 load_dest(ly, ws, d, ds);
-                process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc);
+                process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc, la);
                 store_dest(ly, ws, ds);
             }
         }
