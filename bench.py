@@ -8,6 +8,7 @@ priority order, the matching event loop and the canonical schedule, with the
 pre/postcondition bitmaps already resident in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config k] [--no-cpu-baseline]
+    python bench.py --sweep   # chunk-count sweep: 64-NPU All-to-All, 1..64 chunks per pair
 """
 
 from __future__ import annotations
@@ -82,6 +83,45 @@ def cpu_baseline(wl, budget_s: float = 30.0):
             "seconds": dt, "n_sends": len(r.sends), "collective_time_ns": r.collective_time}
 
 
+def sweep(args, W, Synthesizer, torch):
+    """Synthesis wall time against the number of 128 KiB chunks per pair
+    (the collective-size experiment of Sec. 7) on both 64-NPU topologies."""
+    steps = max(1, min(args.steps, 5))
+    points = []
+    for name, make in W.SWEEP_TOPOLOGIES.items():
+        for k in W.SWEEP_K:
+            wl = make(k)
+            syn = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed, device=0)
+            syn.synthesize()
+            torch.cuda.synchronize()
+            match_ms = []
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                syn.synthesize()
+                match_ms.append(syn.profile()["match_ms"])
+            torch.cuda.synchronize()
+            step_s = (time.perf_counter() - t0) / steps
+            st = syn.stats()
+            pt = {"topology": name, "chunks_per_pair": k, "chunks": wl.coll.n_chunks,
+                  "buffer_MiB_per_npu": 64 * k * wl.coll.chunk_bytes / 2 ** 20, "sends": syn.n_sends,
+                  "collective_time_ns": syn.collective_time, "windows": st["windows"],
+                  "synthesis_ms": step_s * 1e3, "match_ms": sum(match_ms) / len(match_ms),
+                  "matches_per_s": syn.n_sends / step_s}
+            syn.close()
+            log(f"[sweep] {wl.name}: {pt['synthesis_ms']:.2f} ms, {pt['sends']} sends, {pt['windows']} windows")
+            points.append(pt)
+    last = points[-1]
+    print(json.dumps({
+        "metric": "synthesis wall time vs chunks per pair, 64-NPU All-to-All (Sec. 7 collective size)",
+        "value": last["matches_per_s"], "unit": "matches/s", "n_gpus": 1, "steps": steps, "warmup": 1,
+        "ms_per_step": last["synthesis_ms"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": "grid4x4x4_a2a_k64 (last point)", "points": len(points)},
+        "points": points,
+        "context": {"paper_hypercube_512MiB_a2a_synthesis_s": 109.8, "paper_hardware": "not stated"},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -89,6 +129,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the chunk-count sweep (8x8 mesh and 4x4x4 grid All-to-All, k = 1..64)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (to scale HBM counters)")
     args = ap.parse_args()
@@ -114,6 +156,9 @@ def main():
 
     if not torch.cuda.is_available():
         raise RuntimeError("no GPU visible")
+    if args.sweep:
+        sweep(args, W, Synthesizer, torch)
+        return
     wl = W.CONFIGS[args.config]()
     log(f"[bench] workload {wl.name}: {wl.topo.n_devices} devices, {wl.topo.n_links} links, "
         f"{wl.coll.n_chunks} chunks")

@@ -422,6 +422,61 @@ def mesh3x3_two_groups(chunk_bytes=1 << 20) -> Workload:
 CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
 
 
+# --------------------------------------------------------------------------
+# Chunk-count sweep (Sec. 7, collective size): All-to-All on 64-NPU meshes
+# with k chunks of 128 KiB per (source, destination) pair
+# --------------------------------------------------------------------------
+
+def grid3d(dims=(4, 4, 4), alpha: int = 500, bw: int = 50) -> Topology:
+    """3-D grid without wraparound, id = x + X*(y + Y*z); per node the links
+    +x, -x, +y, -y, +z, -z that exist.  Stands in for the paper's 64-NPU
+    "3D Hypercube", whose wiring is not given."""
+    X, Y, Z = dims
+    pairs = []
+    for z in range(Z):
+        for y in range(Y):
+            for x in range(X):
+                v = x + X * (y + Y * z)
+                for (dx, dy, dz) in ((1, 0, 0), (-1, 0, 0), (0, 1, 0), (0, -1, 0), (0, 0, 1), (0, 0, -1)):
+                    a, b, c = x + dx, y + dy, z + dz
+                    if 0 <= a < X and 0 <= b < Y and 0 <= c < Z:
+                        pairs.append((v, a + X * (b + Y * c)))
+    return make_topology(X * Y * Z, 0, pairs, alpha, bw)
+
+
+def a2a_k_bitmaps(n: int, k: int, chunk_bytes: int) -> Collective:
+    """All-to-All over all n NPUs with k chunks per ordered pair: chunk
+    c = (n*i + j)*k + r (r < k) is held by i and needed by j; the diagonal
+    chunks stay where they are."""
+    C = n * n * k
+    W = words(C)
+    pre = np.zeros((n, W), dtype=np.uint64)
+    post = np.zeros((n, W), dtype=np.uint64)
+    r = np.arange(k)
+    for i in range(n):
+        cs = ((i * n + np.arange(n))[:, None] * k + r[None, :]).ravel()
+        np.bitwise_or.at(pre[i], cs >> 6, np.uint64(1) << (cs & 63).astype(np.uint64))
+    for j in range(n):
+        cs = ((np.arange(n) * n + j)[:, None] * k + r[None, :]).ravel()
+        np.bitwise_or.at(post[j], cs >> 6, np.uint64(1) << (cs & 63).astype(np.uint64))
+    gm = group_mask(n, range(n))[None, :]
+    return Collective(C, chunk_bytes, pre, post, gm, None, OP_COPY)
+
+
+def sweep_mesh8x8(k: int) -> Workload:
+    """8x8 mesh (alpha 500 ns, 50 GB/s), All-to-All, k x 128 KiB per pair."""
+    return Workload(f"mesh8x8_a2a_k{k}", mesh2d(8, 8), a2a_k_bitmaps(64, k, 128 << 10), 0)
+
+
+def sweep_grid4x4x4(k: int) -> Workload:
+    """4x4x4 grid (alpha 500 ns, 50 GB/s), All-to-All, k x 128 KiB per pair."""
+    return Workload(f"grid4x4x4_a2a_k{k}", grid3d((4, 4, 4)), a2a_k_bitmaps(64, k, 128 << 10), 0)
+
+
+SWEEP_TOPOLOGIES = {"mesh8x8": sweep_mesh8x8, "grid4x4x4": sweep_grid4x4x4}
+SWEEP_K = (1, 2, 4, 8, 16, 32, 64)
+
+
 def random_small(seed: int, n_npus=None, n_switches=None, max_chunks=40) -> Workload:
     """Small random strongly connected topology plus a random generic
     collective, for seeded fuzzing.  Reverse links of equal cost exist for

@@ -391,3 +391,30 @@ def test_empty_and_trivial_collectives():
     c = W.collective_from_lists(8, 3, 1024, [0, 1, None], [[], [1], []], [list(range(8))])
     r = run(wl_of(t, c))
     assert len(r.sends) == 0 and r.collective_time == 0
+
+
+# ---------------------------------------------------------------- chunk-count sweep
+def _hop_sum(topo):
+    D = topo.n_devices
+    G = csr_matrix((np.ones(topo.n_links), (topo.src, topo.dst)), shape=(D, D))
+    return int(floyd_warshall(G, unweighted=True).sum())
+
+
+@pytest.mark.parametrize("k", [1, 2])
+@pytest.mark.parametrize("name", ["mesh8x8", "grid4x4x4"])
+def test_sweep_a2a_transfers_equal_total_hop_count(name, k):
+    # Homogeneous links: every chunk follows one shortest path of its static
+    # tree, each device on it receives the chunk once and nobody else does,
+    # so the transfers are k x the sum of pairwise hop distances.  Closed
+    # forms: one dimension of n nodes sums (n^3 - n)/3 over ordered pairs, so
+    # the 8x8 mesh gives 2 * 64 * 168 = 21,504 and the 4x4x4 grid
+    # 3 * 16 * 16 * 20 = 15,360.
+    wl = W.SWEEP_TOPOLOGIES[name](k)
+    closed = {"mesh8x8": 2 * 64 * (8 ** 3 - 8) // 3, "grid4x4x4": 3 * 16 * 16 * (4 ** 3 - 4) // 3}[name]
+    assert _hop_sum(wl.topo) == closed
+    r = run(wl)
+    assert len(r.sends) == k * closed
+    assert r.stats["wasted"] == 0
+    if k == 1:
+        check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+        assert r.collective_time >= int(r.chunk_dist.max())
