@@ -42,7 +42,7 @@ struct pccl_ctx {
     hipStream_t stream = nullptr;
     Layout ly{};
     Sizes sz{};
-    int grid = 0;
+    int grid = 0, wpb = 0;  // matching kernel: workgroups, waves per workgroup
     // stage timing
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     float stage_ms[3] = {0.f, 0.f, 0.f};
@@ -163,7 +163,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
 // r * nwaves + w.
 void deal_destinations(pccl_ctx *c)
 {
-    const uint32_t D = c->D, nb = (uint32_t)c->grid, nw = nb * MATCH_WAVES;
+    const uint32_t D = c->D, nb = (uint32_t)c->grid, wpb = (uint32_t)c->wpb, nw = nb * wpb;
     std::vector<uint32_t> byweight(D);
     for (uint32_t v = 0; v < D; v++) byweight[v] = v;
     std::stable_sort(byweight.begin(), byweight.end(), [&](uint32_t a, uint32_t b) {
@@ -173,7 +173,7 @@ void deal_destinations(pccl_ctx *c)
     const uint32_t passes = (D + nw - 1) / nw;
     c->wave_dest.assign((size_t)std::max(passes, 1u) * nw, NONE32);
     for (uint32_t i = 0; i < D; i++) {
-        const uint32_t r = i / nw, j = i % nw, w = (j % nb) * MATCH_WAVES + j / nb;
+        const uint32_t r = i / nw, j = i % nw, w = (j % nb) * wpb + j / nb;
         c->wave_dest[(size_t)r * nw + w] = byweight[i];
     }
 }
@@ -394,9 +394,15 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     c->max_sends = ms;
     c->stream = static_cast<hipStream_t>(hip_stream);
     HIP_OR_FAIL(c, hipSetDevice(c->device));
-    const int wpb = match_waves_per_block();
-    c->grid = std::min<int>(std::min<int>(match_max_grid(c->device), (int)MAX_MATCH_GRID),
-                            (int)((std::max<uint32_t>(c->D, 1) + wpb - 1) / wpb));
+    // waves per workgroup: as few as keep the grid near MATCH_TARGET_GRID
+    // workgroups, so that few destinations still spread over many compute
+    // units while many destinations do not make the window exchange poll
+    // too many slots
+    const uint32_t D1 = std::max<uint32_t>(c->D, 1);
+    const int wpb = (int)std::min<uint32_t>(MATCH_WAVES, std::max<uint32_t>(1, (D1 + MATCH_TARGET_GRID - 1) / MATCH_TARGET_GRID));
+    c->wpb = wpb;
+    c->grid = std::min<int>(std::min<int>(match_max_grid(c->device, wpb), (int)MAX_MATCH_GRID),
+                            (int)((D1 + wpb - 1) / wpb));
     if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
     deal_destinations(c);
     c->have_ws = true;
@@ -472,7 +478,7 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     HIP_OR_FAIL(c, hipEventRecord(c->ev[0], st));
     HIP_OR_FAIL(c, launch_setup(c->ly, c->sz, c->pre, c->post, c->chunk_group, c->seed, st));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[1], st));
-    HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid));
+    HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
     HIP_OR_FAIL(c, hipMemcpyAsync(&c->ctl_host, c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));

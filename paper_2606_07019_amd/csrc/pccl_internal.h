@@ -14,12 +14,13 @@ constexpr uint64_t NONE64 = 0xFFFFFFFFFFFFFFFFull;
 constexpr uint32_t ROW_ALIGN_WORDS = 128;
 
 // Matching kernel envelope (checked on the host when a topology is loaded).
-constexpr uint32_t MATCH_THREADS = 512;   // 8 wavefronts, one destination device each
+constexpr uint32_t MATCH_THREADS = 512;   // at most 8 wavefronts per workgroup, one destination device each
 constexpr uint32_t MATCH_WAVES = MATCH_THREADS / 64;
 constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one device (one lane each)
 constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of their sources' in-degree
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
 constexpr uint32_t MAX_MATCH_GRID = 1024; // workgroups of the matching kernel (window exchange slots)
+constexpr uint32_t MATCH_TARGET_GRID = 128; // workgroups the matching kernel aims for (measured on MI355X)
 
 // Status codes mirrored from the public header.
 enum : uint32_t {
@@ -119,9 +120,8 @@ struct Sizes {
 // ---- launchers (each defined in the translation unit that holds its kernels)
 hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, const uint64_t *post,
                         const uint16_t *chunk_group, uint64_t seed, hipStream_t st);
-hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
-int match_max_grid(int device);
-int match_waves_per_block();
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block);
+int match_max_grid(int device, int waves_per_block);
 hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st);
 // LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;
 // the sorted order ends up in buffer ly.ctl->sort_cur (read it on the device).

@@ -49,6 +49,7 @@ constexpr uint32_t K_NONE = 0, K_BUSY = 1, K_IDLE = 2;
 constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
 constexpr uint32_t PROBE_STEPS = 4;  // lane-parallel probe steps before the whole wave helps
+constexpr uint32_t LA_WORDS = 8;     // words per row of one look-ahead step
 constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose loads are in flight together
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
@@ -362,7 +363,7 @@ __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
     wave_sync();
 }
 
-// Look-ahead for busy links: one probe step of PROBE_WORDS words from the
+// Look-ahead for busy links: one probe step of LA_WORDS words from the
 // cursor, combined with the window's listed arrivals, so that the scan at
 // completion starts at the next candidate.  The cursor stays a lower bound:
 // candidates only appear through arrivals, which lower it when they come.
@@ -371,7 +372,7 @@ __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
 // overlaps the window exchange.  The lists of the issuing window stay in
 // LDS until then.
 struct LookAhead {
-    uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];  // the two rows' words from the even word below the cursor
+    uint4 hv[LA_WORDS / 2], nv[LA_WORDS / 2];  // the two rows' words from the even word below the cursor
     uint32_t cur;           // cursor the words were loaded from, NONE32 if none
     uint32_t n_arr, n_unf;  // list lengths of the issuing window
 };
@@ -391,7 +392,7 @@ __device__ inline void look_ahead_issue(const Layout &ly, uint64_t Wp, const Wav
     const uint64_t pos = (cur >> 6) & ~1u;
     const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
 #pragma unroll
-    for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+    for (uint32_t u = 0; u < LA_WORDS / 2; u++) {
         const uint64_t idx = pos + 2 * u;
         if (idx < Wp) {
             la.hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
@@ -413,7 +414,7 @@ __device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, 
     if (pf) {
         const uint64_t keep0 = ~0ull << (la.cur & 63);
 #pragma unroll
-        for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+        for (uint32_t u = 0; u < LA_WORDS / 2; u++) {
             const uint64_t idx = pos + 2 * u;
             uint64_t x = u4lo(la.hv[u]) & u4lo(la.nv[u]), y = u4hi(la.hv[u]) & u4hi(la.nv[u]);
             if (idx < w0) x = 0;
@@ -441,7 +442,7 @@ __device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, 
     if (pf) {
         // only the probed words are known empty: a listed arrival beyond
         // them does not let the cursor skip unprobed words
-        const uint64_t end_w = pos + PROBE_WORDS;
+        const uint64_t end_w = pos + LA_WORDS;
         const uint32_t probed = end_w >= Wp ? (uint32_t)(Wp * 64) : (uint32_t)(end_w * 64);
         const uint32_t pk = ws.pick[lane];
         if (pk < probed) {
@@ -809,7 +810,8 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     Control *ctl = ly.ctl;
     if (__hip_atomic_load(&ctl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint32_t gwave = blockIdx.x * NWAVES + wave, nwaves = gridDim.x * NWAVES;
+    const uint32_t wpb = blockDim.x >> 6;  // waves in this workgroup (1..NWAVES)
+    const uint32_t gwave = blockIdx.x * wpb + wave, nwaves = gridDim.x * wpb;
     if (ctl->needs_total == 0) {
         if (blockIdx.x == 0 && tid == 0) ctl->windows = 0;
         return;
@@ -853,7 +855,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         __syncthreads();
         uint32_t bmin = NONE32, berr = 0;
         unsigned long long bsent = 0;
-        for (uint32_t w = 0; w < NWAVES; w++) {
+        for (uint32_t w = 0; w < wpb; w++) {
             bmin = min(bmin, sh.red_tmin[w]);
             berr |= sh.red_err[w];
             bsent += sh.red_sent[w];
@@ -887,22 +889,23 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 
 }  // namespace
 
-int match_max_grid(int device)
+int match_max_grid(int device, int waves_per_block)
 {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_match, NT, 0) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_match, 64 * waves_per_block, 0) != hipSuccess)
+        return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return 0;
     return per_cu * cus;
 }
 
-int match_waves_per_block() { return (int)NWAVES; }
-
-hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid)
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block)
 {
+    if (waves_per_block < 1 || waves_per_block > (int)NWAVES) return hipErrorInvalidValue;
     Layout l = ly;
     Sizes s = sz;
     void *args[] = {&l, &s};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_match), dim3(grid), dim3(NT), args, 0, st);
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_match), dim3(grid),
+                                      dim3(64 * waves_per_block), args, 0, st);
 }
 
 }  // namespace pccl
