@@ -295,6 +295,7 @@ struct Dest {
     uint32_t busy, infl, idle;  // its state
     uint32_t ready;             // the cursor points at a candidate found ahead of time
     uint32_t fold;              // chunk delivered into d in the previous window, still to fold
+    uint32_t n_arr_prev;        // length of the previous window's arrival list (kept in LDS)
     unsigned long long log;     // next send-log slot of d
     // arrival pairs p = 64 u + lane: slot of the source's in-link, and the
     // in-link of d it feeds (slot << 8 | j; NONE32 past the last pair)
@@ -316,6 +317,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
     ds.idle = 0;
     ds.ready = 0;
     ds.fold = NONE32;
+    ds.n_arr_prev = 0;
     if (lane < ds.n) {
         const uint32_t sl = ds.base + lane;
         ds.src = ly.slot_src[sl];
@@ -468,7 +470,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     uint64_t *nd = ly.needs + (uint64_t)d * Wp;
     uint64_t *hd = ly.holds + (uint64_t)d * Wp;
     const uint64_t *snap1 = ly.snap + (uint64_t)((k + 2) % 3) * L;  // in flight at the end of window k-1
-    const uint64_t *snap2 = ly.snap + (uint64_t)((k + 1) % 3) * L;  // in flight at the end of window k-2
+    const uint64_t *snap2 = ly.snap + (uint64_t)((k + 1) % 3) * L;  // in flight at the end of window k-2 (unless carried)
     uint64_t *snap0 = ly.snap + (uint64_t)(k % 3) * L;              // written for window k+1
     const bool mine = lane < n;
     const uint32_t sl = ds.base + lane;
@@ -493,8 +495,34 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
 
     // arrivals at the sources of d's in-links that d needs: this window's
     // (snapshot k-1, ends in [t0, t1)) and last window's (snapshot k-2,
-    // ends before t0; possibly not folded into the source's row yet)
+    // ends before t0; possibly not folded into the source's row yet).
+    // Every snapshot k-2 entry that ends before t0 ended in the last window,
+    // so when the wave keeps its destination, last window's list, with the
+    // flags of the chunks delivered since cleared, is exactly this window's
+    // second list: it is carried over in LDS instead of reloaded.
     uint32_t n_arr = 0, n_unf = 0;
+    const bool carry = resident && k >= 2;
+    if (carry) {
+        for (uint32_t q0 = 0; q0 < ds.n_arr_prev; q0 += 64) {
+            const uint32_t q = q0 + lane;
+            const bool keep = q < ds.n_arr_prev && ws.arr_need[q];
+            uint32_t c = 0;
+            uint8_t j = 0;
+            if (keep) {
+                c = ws.arr_c[q];
+                j = ws.arr_j[q];
+            }
+            const uint64_t m = __ballot(keep);
+            if (keep) {
+                const uint32_t u = n_unf + lane_prefix(m, lane);
+                ws.unf_c[u] = c;
+                ws.unf_j[u] = j;
+                ws.unf_need[u] = 1;
+            }
+            n_unf += (uint32_t)__popcll(m);
+        }
+        wave_sync();
+    }
     if (k >= 1) {
 #pragma unroll
         for (uint32_t g = 0; g < PAIRS_PER_LANE; g += PAIR_GROUP) {
@@ -507,7 +535,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint32_t pr = ds.pair[g + u];
                 if (pr != NONE32) {
                     e1[u] = snap1[pr >> 8];
-                    if (k >= 2) e2[u] = snap2[pr >> 8];
+                    if (k >= 2 && !carry) e2[u] = snap2[pr >> 8];
                 }
             }
             bool a_ok[PAIR_GROUP], u_ok[PAIR_GROUP];
@@ -785,6 +813,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     }
 
     look_ahead_issue(ly, Wp, ws, ds, nd, mine, n_arr, n_unf, la);
+    ds.n_arr_prev = n_arr;
     if (!resident) look_ahead_finish(Wp, ws, ds, mine, la);
 
     // this window's snapshot and sends
