@@ -48,7 +48,7 @@ constexpr uint32_t M_IDLE = 0, M_FULL = 1, M_ARR = 2, M_ARR_WON = 3;
 constexpr uint32_t K_NONE = 0, K_BUSY = 1, K_IDLE = 2;
 constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
-constexpr uint32_t PROBE_STEPS = 4;  // lane-parallel probe steps before the whole wave helps
+constexpr uint32_t SEG_STEPS = 3;    // lane-group probe steps before the whole wave helps
 constexpr uint32_t LA_WORDS = 8;     // words per row of one look-ahead step
 constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose loads are in flight together
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
@@ -69,6 +69,7 @@ struct alignas(16) WaveShared {
     uint32_t unf_c[PAIRS];
     uint8_t arr_j[PAIRS], unf_j[PAIRS], arr_need[PAIRS], unf_need[PAIRS];
     uint32_t snd_link[MAXIN], snd_rank[MAXIN], snd_t[MAXIN];
+    uint32_t seg_j[MAXIN], seg_p[MAXIN], seg_pos[MAXIN];  // probe groups: link, result, continuation word
     // clash detection: lane that last wrote a hashed pick, and slots written twice
     uint8_t clash_lane[CLASH_SLOTS], clash_hit[CLASH_SLOTS];
 };
@@ -611,8 +612,15 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
 
         // pick rounds at time t
         while (true) {
-            // bitmap part of the full scans: lane-parallel probes of each
-            // link's own rows; scans that outlast them continue with the wave
+            // bitmap part of the full scans.  First every scanning lane
+            // probes PROBE_WORDS words of its own link's two rows (most scans
+            // end there: the look-ahead put the cursor on the candidate);
+            // when three or more links are still scanning, the wave is split
+            // among them, G = 64 / next_pow2(k) lanes each, every lane
+            // reading PROBE_WORDS words per step, and a min over each lane
+            // group gives the link's first candidate.  Scans that are left
+            // (at most two, or after SEG_STEPS group steps) continue with the
+            // whole wave, one link at a time.
             uint32_t p = NONE32, scanned = 0;
             bool scanning = false;
             uint64_t pos = 0, w0 = 0, keep0 = 0;
@@ -624,61 +632,139 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 pos = w0 & ~1ull;
             }
             const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
-            // with only a few scans, whole-wave scans are quicker than probes
-            const uint32_t steps = __popcll(__ballot(scanning)) <= FEW_SCANS ? 0u : PROBE_STEPS;
-            for (uint32_t step = 0; step < steps; step++) {
-                if (!__ballot(scanning)) break;
-                if (scanning) {
-                    uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
+            if (__popcll(__ballot(scanning)) > FEW_SCANS && scanning) {
+                uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
 #pragma unroll
-                    for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
-                        const uint64_t idx = pos + 2 * u;
-                        if (idx < Wp) {
-                            hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
-                            nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
-                        } else {
-                            hv[u] = make_uint4(0, 0, 0, 0);
-                            nv[u] = make_uint4(0, 0, 0, 0);
-                        }
-                    }
-#pragma unroll
-                    for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
-                        const uint64_t idx = pos + 2 * u;
-                        uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
-                        if (idx < w0) x = 0;
-                        else if (idx == w0) x &= keep0;
-                        if (idx + 1 < w0) y = 0;
-                        else if (idx + 1 == w0) y &= keep0;
-                        if (p == NONE32) {
-                            if (x) {
-                                p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
-                                scanned = (uint32_t)(idx + 1 - w0);
-                            } else if (y) {
-                                p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
-                                scanned = (uint32_t)(idx + 2 - w0);
-                            }
-                        }
-                    }
-                    if (p != NONE32) {
-                        scanning = false;
+                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                    const uint64_t idx = pos + 2 * u;
+                    if (idx < Wp) {
+                        hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
+                        nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
                     } else {
-                        pos += PROBE_WORDS;
-                        if (pos >= Wp) {
-                            scanning = false;
-                            scanned = (uint32_t)(Wp - w0);
+                        hv[u] = make_uint4(0, 0, 0, 0);
+                        nv[u] = make_uint4(0, 0, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                    const uint64_t idx = pos + 2 * u;
+                    uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
+                    if (idx < w0) x = 0;
+                    else if (idx == w0) x &= keep0;
+                    if (idx + 1 < w0) y = 0;
+                    else if (idx + 1 == w0) y &= keep0;
+                    if (p == NONE32) {
+                        if (x) {
+                            p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
+                            scanned = (uint32_t)(idx + 1 - w0);
+                        } else if (y) {
+                            p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
+                            scanned = (uint32_t)(idx + 2 - w0);
                         }
                     }
                 }
+                if (p != NONE32) {
+                    scanning = false;
+                } else {
+                    pos += PROBE_WORDS;
+                    if (pos >= Wp) {
+                        scanning = false;
+                        scanned = (uint32_t)(Wp - w0);
+                    }
+                }
             }
-            if (scanning) scanned = steps ? (uint32_t)(pos - w0) : 0u;
+            if (scanning) scanned = pos > w0 ? (uint32_t)(pos - w0) : 0u;  // so far; the group steps add theirs
+            const uint64_t smask = __ballot(scanning);
+            const uint32_t ks = (uint32_t)__popcll(smask);
+            // one or two scans left: the whole-wave scan below is quicker
+            if (ks > FEW_SCANS) {
+                if (scanning) {
+                    ws.seg_j[lane_prefix(smask, lane)] = lane;
+                    ws.seg_pos[lane] = (uint32_t)pos;
+                }
+                wave_sync();
+                const uint32_t lg = (31u - (uint32_t)__builtin_clz(ks)) + ((ks & (ks - 1u)) ? 1u : 0u);
+                const uint32_t G = 64u >> lg;  // lanes per link still scanning
+                const uint32_t g = lane >> (6u - lg), sub = lane & (G - 1u);
+                const bool act = g < ks;
+                uint32_t j = 0;
+                uint64_t gw0 = 0, gkeep0 = 0, gpos = 0, gstart = 0;
+                const uint64_t *hj = ly.holds;
+                if (act) {
+                    j = ws.seg_j[g];
+                    const uint32_t cj = ws.cur[j];
+                    gw0 = cj >> 6;
+                    gkeep0 = ~0ull << (cj & 63);
+                    gpos = gstart = ws.seg_pos[j];
+                    hj = ly.holds + (uint64_t)ws.src[j] * Wp;
+                }
+                bool live = act;
+                uint32_t gp = NONE32;
+                for (uint32_t step = 0; step < SEG_STEPS; step++) {
+                    if (!__ballot(live)) break;
+                    uint32_t lp = NONE32;
+                    if (live) {
+                        const uint64_t base = gpos + (uint64_t)sub * PROBE_WORDS;
+                        uint4 hv[PROBE_WORDS / 2], nv[PROBE_WORDS / 2];
+#pragma unroll
+                        for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                            const uint64_t idx = base + 2 * u;
+                            if (idx < Wp) {
+                                hv[u] = *reinterpret_cast<const uint4 *>(hj + idx);
+                                nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
+                            } else {
+                                hv[u] = make_uint4(0, 0, 0, 0);
+                                nv[u] = make_uint4(0, 0, 0, 0);
+                            }
+                        }
+#pragma unroll
+                        for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
+                            const uint64_t idx = base + 2 * u;
+                            uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
+                            if (idx < gw0) x = 0;
+                            else if (idx == gw0) x &= gkeep0;
+                            if (idx + 1 < gw0) y = 0;
+                            else if (idx + 1 == gw0) y &= gkeep0;
+                            if (lp == NONE32) {
+                                if (x) lp = (uint32_t)(idx * 64 + __builtin_ctzll(x));
+                                else if (y) lp = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
+                            }
+                        }
+                    }
+                    for (uint32_t off = 1; off < G; off <<= 1) lp = min(lp, (uint32_t)__shfl_xor((int)lp, off));
+                    if (live) {
+                        if (lp != NONE32) {
+                            gp = lp;
+                            live = false;
+                        } else {
+                            gpos += (uint64_t)G * PROBE_WORDS;
+                            if (gpos >= Wp) live = false;
+                        }
+                    }
+                }
+                if (act && sub == 0) {
+                    // word positions these steps passed: through the pick's word, or the probed range
+                    ws.seg_p[j] = gp;
+                    ws.seg_pos[j] = live ? (uint32_t)gpos : NONE32;
+                    ws.pick[j] = (uint32_t)((gp != NONE32 ? (uint64_t)(gp >> 6) + 1 : min(gpos, Wp)) - max(gstart, gw0));
+                }
+                wave_sync();
+                if (scanning) {
+                    p = ws.seg_p[lane];
+                    scanned += ws.pick[lane];
+                    const uint32_t sp = ws.seg_pos[lane];
+                    scanning = sp != NONE32;
+                    pos = sp;
+                }
+            }
             acc.words += wave_sum(scanned);
             uint64_t cmask = __ballot(scanning);
             while (cmask) {
                 const int j = __builtin_ffsll((long long)cmask) - 1;
                 cmask &= cmask - 1;
                 const uint32_t sj = (uint32_t)__shfl((int)ds.src, j);
-                // continue after the probed words (or from the cursor when nothing was probed)
-                const uint32_t from = steps ? (uint32_t)(shfl64(pos, j) * 64) : ws.cur[j];
+                // continue after the probed words (from the cursor when none were probed)
+                const uint32_t from = max((uint32_t)(shfl64(pos, j) * 64), ws.cur[j]);
                 uint64_t w = 0;
                 const uint32_t pj = wave_first_candidate(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
                 acc.words += w;
