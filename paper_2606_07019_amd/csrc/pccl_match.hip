@@ -88,42 +88,67 @@ __device__ inline bool need_bit(const uint64_t *nd, uint32_t c)
     return (nd[c >> 6] >> (c & 63)) & 1ull;
 }
 
-__device__ inline uint32_t wave_min(uint32_t v)
+// Wave-wide reductions with DPP row operations (no LDS round trip): two quad
+// permutations, row shifts by 4 and 8, then the row broadcasts of lanes 15
+// and 31 leave the result over all 64 lanes in lane 63, which is read back as
+// a uniform value.  Lanes without a DPP source contribute the identity.
+template <class Op>
+__device__ inline uint32_t dpp_reduce(uint32_t v, uint32_t id, Op op)
 {
-    for (int off = 32; off; off >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, off));
-    return v;
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0xb1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x4e, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x114, 0xf, 0xf, false));  // row_shr 4
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x118, 0xf, 0xf, false));  // row_shr 8
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x142, 0xa, 0xf, false));  // row_bcast 15
+    v = op(v, (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, 0x143, 0xc, 0xf, false));  // row_bcast 31
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-__device__ inline uint32_t wave_max(uint32_t v)
+template <class Op>
+__device__ inline uint64_t dpp_reduce64(uint64_t v, uint64_t id, Op op)
 {
-    for (int off = 32; off; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off));
-    return v;
-}
-
-__device__ inline uint32_t wave_sum(uint32_t v)
-{
-    for (int off = 32; off; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off);
-    return v;
-}
-
-__device__ inline unsigned long long wave_sum64(unsigned long long v)
-{
-    for (int off = 32; off; off >>= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off);
-        v += ((unsigned long long)hi << 32) | lo;
+#define PCCL_DPP64(ctrl, rmask)                                                                          \
+    {                                                                                                    \
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)id, (int)(uint32_t)v,  \
+                                                                  ctrl, rmask, 0xf, false);              \
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(id >> 32),            \
+                                                                  (int)(uint32_t)(v >> 32), ctrl, rmask, \
+                                                                  0xf, false);                           \
+        v = op(v, ((uint64_t)hi << 32) | lo);                                                            \
     }
-    return v;
+    PCCL_DPP64(0xb1, 0xf)
+    PCCL_DPP64(0x4e, 0xf)
+    PCCL_DPP64(0x114, 0xf)
+    PCCL_DPP64(0x118, 0xf)
+    PCCL_DPP64(0x142, 0xa)
+    PCCL_DPP64(0x143, 0xc)
+#undef PCCL_DPP64
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ inline uint64_t wave_min64(uint64_t v)
+struct OpMin { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return min(a, b); } };
+struct OpMax { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return max(a, b); } };
+struct OpAdd { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; } };
+struct OpMin64 { __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a < b ? a : b; } };
+struct OpAdd64 { __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; } };
+
+__device__ inline uint32_t wave_min(uint32_t v) { return dpp_reduce(v, NONE32, OpMin()); }
+__device__ inline uint32_t wave_max(uint32_t v) { return dpp_reduce(v, 0u, OpMax()); }
+__device__ inline uint32_t wave_sum(uint32_t v) { return dpp_reduce(v, 0u, OpAdd()); }
+__device__ inline unsigned long long wave_sum64(unsigned long long v) { return dpp_reduce64(v, 0ull, OpAdd64()); }
+__device__ inline uint64_t wave_min64(uint64_t v) { return dpp_reduce64(v, NONE64, OpMin64()); }
+
+// The value of `v` in lane `lane`, which must be the same in every lane.
+__device__ inline uint32_t readlane32(uint32_t v, uint32_t lane)
 {
-    for (int off = 32; off; off >>= 1) {
-        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off);
-        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off);
-        v = min(v, ((uint64_t)hi << 32) | lo);
-    }
-    return v;
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)lane);
+}
+
+__device__ inline uint64_t readlane64(uint64_t v, uint32_t lane)
+{
+    return ((uint64_t)readlane32((uint32_t)(v >> 32), lane) << 32) | readlane32((uint32_t)v, lane);
 }
 
 __device__ inline uint32_t lane_prefix(uint64_t mask, uint32_t lane)
@@ -131,11 +156,6 @@ __device__ inline uint32_t lane_prefix(uint64_t mask, uint32_t lane)
     return (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
 }
 
-__device__ inline uint64_t shfl64(uint64_t v, int lane)
-{
-    const int lo = __shfl((int)(uint32_t)v, lane), hi = __shfl((int)(uint32_t)(v >> 32), lane);
-    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-}
 
 __device__ inline uint64_t u4lo(uint4 v) { return ((uint64_t)v.y << 32) | v.x; }
 __device__ inline uint64_t u4hi(uint4 v) { return ((uint64_t)v.w << 32) | v.z; }
@@ -177,7 +197,7 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
             const uint64_t m = __ballot((a[u] | b[u]) != 0ull);
             if (m) {
                 const int fl = __builtin_ffsll((long long)m) - 1;
-                const uint64_t x = shfl64(a[u], fl), y = shfl64(b[u], fl);
+                const uint64_t x = readlane64(a[u], (uint32_t)fl), y = readlane64(b[u], (uint32_t)fl);
                 const uint64_t idx = wb + 128 * u + 2 * (uint64_t)fl;
                 words += (x ? idx : idx + 1) + 1 - w0;
                 return x ? (uint32_t)(idx * 64 + __builtin_ctzll(x))
@@ -189,9 +209,6 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
     return NONE32;
 }
 
-// Grid-wide barrier: arrivals on a monotonic counter; the last arrival bumps
-// a separate release word that the others poll.  Returns false when the
-// wait timed out or another workgroup gave up (then the kernel ends).
 // Grid-wide exchange at the end of window `gen`, which is also the grid
 // barrier: every workgroup publishes its results in its own two 64-bit
 // slots, each tagged with gen+1 (16 bits): (tag, error flag, earliest
@@ -762,9 +779,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             while (cmask) {
                 const int j = __builtin_ffsll((long long)cmask) - 1;
                 cmask &= cmask - 1;
-                const uint32_t sj = (uint32_t)__shfl((int)ds.src, j);
+                const uint32_t sj = readlane32(ds.src, (uint32_t)j);
                 // continue after the probed words (from the cursor when none were probed)
-                const uint32_t from = max((uint32_t)(shfl64(pos, j) * 64), ws.cur[j]);
+                const uint32_t from = max((uint32_t)(readlane64(pos, (uint32_t)j) * 64), ws.cur[j]);
                 uint64_t w = 0;
                 const uint32_t pj = wave_first_candidate(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
                 acc.words += w;
@@ -823,7 +840,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint64_t key = act ? (((uint64_t)ds.tim << 32) | ws.link[lane]) : NONE64;
                 while (contested) {
                     const int j = __builtin_ffsll((long long)contested) - 1;
-                    const uint32_t v = (uint32_t)__shfl((int)pk, j);
+                    const uint32_t v = readlane32(pk, (uint32_t)j);
                     const uint64_t g = __ballot(act && pk == v);
                     const bool in_g = (g >> lane) & 1ull;
                     const uint64_t kmin = wave_min64(in_g ? key : NONE64);
