@@ -72,6 +72,8 @@ struct alignas(16) WaveShared {
     uint32_t seg_j[MAXIN], seg_p[MAXIN], seg_pos[MAXIN];  // probe groups: link, result, continuation word
     // clash detection: lane that last wrote a hashed pick, and slots written twice
     uint8_t clash_lane[CLASH_SLOTS], clash_hit[CLASH_SLOTS];
+    // round (low 16 bits) in which a chunk of each hash slot was last delivered
+    uint16_t dlv_round[CLASH_SLOTS];
 };
 
 
@@ -312,6 +314,7 @@ struct Dest {
     uint32_t src, tim;          // this lane's in-link (lane < n)
     uint32_t busy, infl, idle;  // its state
     uint32_t ready;             // the cursor points at a candidate found ahead of time
+    uint32_t ready_c;           // that candidate while it is valid (NONE32 when not kept)
     uint32_t fold;              // chunk delivered into d in the previous window, still to fold
     uint32_t n_arr_prev;        // length of the previous window's arrival list (kept in LDS)
     unsigned long long log;     // next send-log slot of d
@@ -334,6 +337,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
     ds.infl = NONE32;
     ds.idle = 0;
     ds.ready = 0;
+    ds.ready_c = NONE32;
     ds.fold = NONE32;
     ds.n_arr_prev = 0;
     if (lane < ds.n) {
@@ -468,6 +472,7 @@ __device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, 
         if (pk < probed) {
             ws.cur[lane] = pk;
             ds.ready = 1;
+            ds.ready_c = pk;
         } else {
             ws.cur[lane] = probed;
         }
@@ -645,8 +650,16 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint32_t cur = ws.cur[lane];
                 w0 = cur >> 6;
                 keep0 = ~0ull << (cur & 63);
-                scanning = w0 < Wp;
-                pos = w0 & ~1ull;
+                if (cur == ds.ready_c) {
+                    // the look-ahead's candidate, still at the cursor and not
+                    // delivered since: held by the source (holds only grow),
+                    // still needed, and nothing lies below the cursor
+                    p = cur;
+                    scanned = 1;
+                } else {
+                    scanning = w0 < Wp;
+                    pos = w0 & ~1ull;
+                }
             }
             const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
             if (__popcll(__ballot(scanning)) > FEW_SCANS && scanning) {
@@ -777,15 +790,15 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             acc.words += wave_sum(scanned);
             uint64_t cmask = __ballot(scanning);
             while (cmask) {
+                // continue after the probed words (from the cursor when none were probed)
                 const int j = __builtin_ffsll((long long)cmask) - 1;
                 cmask &= cmask - 1;
                 const uint32_t sj = readlane32(ds.src, (uint32_t)j);
-                // continue after the probed words (from the cursor when none were probed)
                 const uint32_t from = max((uint32_t)(readlane64(pos, (uint32_t)j) * 64), ws.cur[j]);
                 uint64_t w = 0;
                 const uint32_t pj = wave_first_candidate(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
-                acc.words += w;
                 if ((int)lane == j) p = pj;
+                acc.words += w;
             }
             // explicit candidates: arrivals not yet in the source's row
             if (mine) ws.pick[lane] = (md == M_FULL) ? p : NONE32;
@@ -865,6 +878,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     ds.busy = e32;
                     ds.idle = 0;
                     ds.ready = 0;
+                    ds.ready_c = NONE32;
                     ce = e32;
                     const uint32_t q = n_send + lane_prefix(wins, lane);
                     ws.snd_link[q] = ws.link[lane];
@@ -887,6 +901,14 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             acc.cstar = max(acc.cstar, wave_max(ce));
             if (__ballot(overflow)) acc.err = 1;
             wave_sync();
+            // a candidate found ahead of time is gone once its chunk is
+            // delivered: winners stamp their chunk's hash slot with the round,
+            // and a stamped slot drops the candidate (a hash collision only
+            // drops one that is still valid, which costs a scan)
+            if (win) ws.dlv_round[hs] = (uint16_t)acc.rounds;
+            wave_sync();
+            if (ds.ready_c != NONE32 && ws.dlv_round[(ds.ready_c * 2654435761u) >> 22] == (uint16_t)acc.rounds)
+                ds.ready_c = NONE32;
             // the delivered chunks are no longer needed: clear their flags
             for (uint64_t wm = (n_arr | n_unf) ? wins : 0ull; wm; wm &= wm - 1) {
                 const uint32_t c = ws.pick[__builtin_ffsll((long long)wm) - 1];
@@ -953,7 +975,10 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const bool resident = sz.D <= nwaves;
     WaveShared &ws = sh.w[wave];
     Dest ds{};
-    for (uint32_t i = lane; i < CLASH_SLOTS; i += 64) ws.clash_hit[i] = 0;
+    for (uint32_t i = lane; i < CLASH_SLOTS; i += 64) {
+        ws.clash_hit[i] = 0;
+        ws.dlv_round[i] = 0xFFFFu;
+    }
     const uint32_t passes = (sz.D + nwaves - 1) / nwaves;
     const uint32_t mine_d = resident ? ly.wave_dest[gwave] : NONE32;
     if (mine_d != NONE32) load_dest(ly, ws, mine_d, ds);
