@@ -68,7 +68,6 @@ struct alignas(16) WaveShared {
     uint32_t arr_end[PAIRS], arr_c[PAIRS];
     uint32_t unf_c[PAIRS];
     uint8_t arr_j[PAIRS], unf_j[PAIRS], arr_need[PAIRS], unf_need[PAIRS];
-    uint32_t snd_link[MAXIN], snd_rank[MAXIN], snd_t[MAXIN];
     uint32_t seg_j[MAXIN], seg_p[MAXIN], seg_pos[MAXIN];  // probe groups: link, result, continuation word
     // clash detection: lane that last wrote a hashed pick, and slots written twice
     uint8_t clash_lane[CLASH_SLOTS], clash_hit[CLASH_SLOTS];
@@ -240,21 +239,28 @@ struct BlockShared {
     Exchange ex;
 };
 
-__device__ bool window_exchange(Control *ctl, uint64_t *xslot, BlockShared &sh, uint32_t gen, uint32_t tmin,
-                                unsigned long long sent, uint32_t err, Exchange &ex)
+// First half: publish this workgroup's slots once every wave's writes and
+// atomics of the window have completed.
+__device__ void window_publish(uint64_t *xslot, uint32_t gen, uint32_t tmin, unsigned long long sent, uint32_t err)
+{
+    const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFFu) << 48;
+    uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * 2;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(&slot[2 * blockIdx.x], tag | ((uint64_t)(err ? 1u : 0u) << 47) | tmin, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&slot[2 * blockIdx.x + 1], tag | sent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// Second half: wait for every workgroup's slots and reduce them.
+__device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint32_t gen, Exchange &ex)
 {
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
     const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFFu) << 48;
     uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * 2;
-    // every wave's global writes and atomics of this window have completed
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    __syncthreads();
     if (threadIdx.x < 64) {
-        if (lane == 0) {
-            __hip_atomic_store(&slot[2 * blockIdx.x], tag | ((uint64_t)(err ? 1u : 0u) << 47) | tmin,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&slot[2 * blockIdx.x + 1], tag | sent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
         uint32_t spins = 0, ok = 1;
         uint32_t tn = NONE32, e = 0;
         unsigned long long s = 0;
@@ -515,6 +521,14 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             __hip_atomic_fetch_or(&hd[r >> 6], 1ull << (r & 63), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ds.fold = NONE32;
     }
+
+    // this window's snapshot entry, as far as known now: a transfer that
+    // outlasts the window stays in flight; any other link ends the window
+    // free unless it commits in it, and then the commit writes the entry
+    if (mine)
+        __hip_atomic_store(&snap0[sl],
+                           ds.infl != NONE32 && (uint64_t)ds.busy >= t1 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
     // arrivals at the sources of d's in-links that d needs: this window's
     // (snapshot k-1, ends in [t0, t1)) and last window's (snapshot k-2,
@@ -880,10 +894,11 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     ds.ready = 0;
                     ds.ready_c = NONE32;
                     ce = e32;
-                    const uint32_t q = n_send + lane_prefix(wins, lane);
-                    ws.snd_link[q] = ws.link[lane];
-                    ws.snd_rank[q] = pk;
-                    ws.snd_t[q] = t;
+                    __hip_atomic_store(&snap0[sl], ((uint64_t)pk << 32) | e32, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    const unsigned long long q = ds.log + n_send + lane_prefix(wins, lane);
+                    ly.skey[0][q] = ((uint64_t)t << 32) | ws.link[lane];
+                    ly.sval[0][q] = pk;
                     if (md == M_FULL) {
                         ws.cur[lane] = pk + 1;
                         md = M_IDLE;
@@ -940,21 +955,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     look_ahead_issue(ly, Wp, ws, ds, nd, mine, n_arr, n_unf, la);
     ds.n_arr_prev = n_arr;
     if (!resident) look_ahead_finish(Wp, ws, ds, mine, la);
-
-    // this window's snapshot and sends
-    if (mine)
-        __hip_atomic_store(&snap0[sl], ds.infl != NONE32 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64,
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
-    if (n_send) {
-        if (lane < n_send) {
-            const unsigned long long pos = ds.log + lane;
-            ly.skey[0][pos] = ((uint64_t)ws.snd_t[lane] << 32) | ws.snd_link[lane];
-            ly.sval[0][pos] = ws.snd_rank[lane];
-        }
-        ds.log += n_send;
-        acc.sent += n_send;
-    }
+    ds.log += n_send;
+    acc.sent += n_send;
     wave_sync();
 }
 
@@ -1018,7 +1021,8 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
             bsent += sh.red_sent[w];
         }
         Exchange ex;
-        if (!window_exchange(ctl, ly.xslot, sh, (uint32_t)k, bmin, bsent, berr, ex)) break;
+        window_publish(ly.xslot, (uint32_t)k, bmin, bsent, berr);
+        if (!window_wait(ctl, ly.xslot, sh, (uint32_t)k, ex)) break;
         remaining -= ex.sent;
         if (ex.err || remaining == 0) break;
         if (ex.tn == NONE32) {
