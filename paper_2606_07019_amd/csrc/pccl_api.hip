@@ -150,7 +150,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.lflags = cv.take<uint32_t>(L);
     ly.snap = cv.take<uint64_t>(3 * L);
     ly.dest_log = cv.take<unsigned long long>(D);
-    ly.xslot = cv.take<uint64_t>(4ull * MAX_MATCH_GRID);
+    ly.xslot = cv.take<uint64_t>(2ull * MAX_MATCH_GRID * XSLOT_WORDS);
     ly.wave_dest = cv.take<uint32_t>(D + (uint64_t)MATCH_WAVES * MAX_MATCH_GRID);
     ly.out = cv.take<pccl_send>((c->op == PCCL_OP_ALLREDUCE ? 2 : 1) * max_sends);
     total = (cv.off + 255) & ~size_t(255);

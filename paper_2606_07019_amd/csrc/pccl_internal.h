@@ -21,6 +21,7 @@ constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of the
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
 constexpr uint32_t MAX_MATCH_GRID = 1024; // workgroups of the matching kernel (window exchange slots)
 constexpr uint32_t MATCH_TARGET_GRID = 128; // workgroups the matching kernel aims for (measured on MI355X)
+constexpr uint32_t XSLOT_WORDS = 16;        // one 128-byte line per window exchange slot
 
 // Status codes mirrored from the public header.
 enum : uint32_t {
@@ -100,7 +101,7 @@ struct Layout {
     uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
     uint64_t *snap;           // [3 * L] by slot
     unsigned long long *dest_log;  // [D] next send-log slot of each destination
-    uint64_t *xslot;          // [2 * MAX_MATCH_GRID * 2] window exchange slots of the matching kernel
+    uint64_t *xslot;          // [2 * MAX_MATCH_GRID * XSLOT_WORDS] window exchange slots of the matching kernel
     uint32_t *wave_dest;      // [D + MATCH_WAVES * MAX_MATCH_GRID] destination of (pass, wave), NONE32 if none
     // output
     void *out;                // pccl_send [2 * max_sends]

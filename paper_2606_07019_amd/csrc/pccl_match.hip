@@ -211,14 +211,15 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
 }
 
 // Grid-wide exchange at the end of window `gen`, which is also the grid
-// barrier: every workgroup publishes its results in its own two 64-bit
-// slots, each tagged with gen+1 (16 bits): (tag, error flag, earliest
-// transfer end) and (tag, transfers committed).  Wave 0 of every workgroup
-// then polls all slots, one per lane, until each carries the tag, and
-// reduces them itself.  Slots alternate with the window parity: a workgroup
-// can run at most one window ahead of the slowest poller, so it never
-// overwrites a slot that is still being read.  No atomic read-modify-write
-// and no second round trip to release the waiters.
+// barrier: every workgroup publishes its results in one 64-bit slot of its
+// own cache line (so the pollers' loads spread over the memory channels):
+// gen+1 (12 bits) | error flag | transfers committed (19 bits) | earliest
+// transfer end (32 bits).  Wave 0 of every workgroup then polls all slots,
+// one per lane, until each carries the tag, and reduces them itself.  Slots
+// alternate with the window parity: a workgroup can run at most one window
+// ahead of the slowest poller, so it never overwrites a slot that is still
+// being read.  No atomic read-modify-write and no second round trip to
+// release the waiters.
 // Memory ordering: the writes of a window that other workgroups read (the
 // snapshot entries and the holds folds) are agent-scope atomics, coherent
 // without an L2 write-back; every wave waits for their completion before the
@@ -241,25 +242,27 @@ struct BlockShared {
 
 // First half: publish this workgroup's slots once every wave's writes and
 // atomics of the window have completed.
+constexpr uint64_t XTAG_MASK = 0xFFFull << 52;
+static_assert((uint64_t)MAX_DEVICES_SP * MAX_IN_LINKS < (1u << 19), "a window's transfers fit in 19 bits");
+
 __device__ void window_publish(uint64_t *xslot, uint32_t gen, uint32_t tmin, unsigned long long sent, uint32_t err)
 {
-    const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFFu) << 48;
-    uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * 2;
+    const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFu) << 52;
+    uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __hip_atomic_store(&slot[2 * blockIdx.x], tag | ((uint64_t)(err ? 1u : 0u) << 47) | tmin, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&slot[2 * blockIdx.x + 1], tag | sent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&slot[(uint64_t)blockIdx.x * XSLOT_WORDS],
+                           tag | ((uint64_t)(err ? 1u : 0u) << 51) | ((uint64_t)(sent & 0x7FFFFu) << 32) | tmin,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Second half: wait for every workgroup's slots and reduce them.
 __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint32_t gen, Exchange &ex)
 {
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
-    const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFFu) << 48;
-    uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * 2;
+    const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFu) << 52;
+    uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
     if (threadIdx.x < 64) {
         uint32_t spins = 0, ok = 1;
         uint32_t tn = NONE32, e = 0;
@@ -270,12 +273,12 @@ __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint
             e = 0;
             s = 0;
             for (uint32_t b = lane; b < nb; b += 64) {
-                const uint64_t a = __hip_atomic_load(&slot[2 * b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                const uint64_t c = __hip_atomic_load(&slot[2 * b + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if ((a & (0xFFFFull << 48)) != tag || (c & (0xFFFFull << 48)) != tag) all = false;
+                const uint64_t a = __hip_atomic_load(&slot[(uint64_t)b * XSLOT_WORDS], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                if ((a & XTAG_MASK) != tag) all = false;
                 tn = min(tn, (uint32_t)a);
-                e |= (uint32_t)(a >> 47) & 1u;
-                s += c & ((1ull << 47) - 1ull);
+                e |= (uint32_t)(a >> 51) & 1u;
+                s += (a >> 32) & 0x7FFFFull;
             }
             if (__ballot(!all) == 0) break;
             if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {

@@ -302,7 +302,7 @@ __global__ void k_init_match(Layout ly, Sizes sz)
         ly.snap[sz.L + i] = NONE64;
         ly.snap[2ull * sz.L + i] = NONE64;
     }
-    if (i < 4ull * MAX_MATCH_GRID) ly.xslot[i] = 0;
+    if (i < 2ull * MAX_MATCH_GRID) ly.xslot[i * XSLOT_WORDS] = 0;
     if (i == 0) {
         Control *ctl = ly.ctl;
         ctl->needs_remaining = ctl->needs_total;
