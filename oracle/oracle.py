@@ -45,7 +45,7 @@ def _load():
         P = ctypes.c_void_p
         U32, U64, I = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int
         lib.pccl_oracle_run.argtypes = [U32, U32, U32, P, P, P, P, U32, U64, P, P, P, U32, P,
-                                        I, U64, I, ctypes.POINTER(P)]
+                                        I, U64, I, P, P, ctypes.POINTER(P)]
         lib.pccl_oracle_run.restype = I
         lib.pccl_oracle_status.argtypes = [P]
         lib.pccl_oracle_status.restype = I
@@ -87,7 +87,10 @@ def _ptr(a):
 
 
 def run(n_npus, n_switches, src, dst, alpha, bw, n_chunks, chunk_bytes, pre, post,
-        group_masks, chunk_group=None, op=0, tie_seed=0, mode=MODE_SKIP_IDLE) -> OracleResult:
+        group_masks, chunk_group=None, op=0, tie_seed=0, mode=MODE_SKIP_IDLE,
+        sw_buffer=None, sw_unicast=None) -> OracleResult:
+    """sw_buffer / sw_unicast: the switch model (per switch: buffer capacity in
+    chunks, 0 = unlimited; 1 = no multicast), None for none."""
     lib = _load()
     src = np.ascontiguousarray(src, dtype=np.uint32)
     dst = np.ascontiguousarray(dst, dtype=np.uint32)
@@ -99,10 +102,16 @@ def run(n_npus, n_switches, src, dst, alpha, bw, n_chunks, chunk_bytes, pre, pos
     n_groups = gm.shape[0] if gm.ndim == 2 else 1
     cg = None if chunk_group is None else np.ascontiguousarray(chunk_group, dtype=np.uint16)
     L = int(src.shape[0])
+    swb = None if sw_buffer is None else np.ascontiguousarray(sw_buffer, dtype=np.uint32)
+    swu = None if sw_unicast is None else np.ascontiguousarray(sw_unicast, dtype=np.uint8)
+    for a in (swb, swu):
+        if a is not None and a.shape != (n_switches,):
+            raise ValueError("switch model arrays need one entry per switch")
     h = ctypes.c_void_p()
     st = lib.pccl_oracle_run(n_npus, n_switches, L, _ptr(src), _ptr(dst), _ptr(alpha), _ptr(bw),
                              n_chunks, chunk_bytes, _ptr(pre), _ptr(post), _ptr(gm), n_groups,
-                             _ptr(cg), op, tie_seed & ((1 << 64) - 1), mode, ctypes.byref(h))
+                             _ptr(cg), op, tie_seed & ((1 << 64) - 1), mode, _ptr(swb), _ptr(swu),
+                             ctypes.byref(h))
     try:
         msg = lib.pccl_oracle_message(h).decode()
         T = np.zeros(L, dtype=np.uint32)
@@ -130,7 +139,7 @@ def run_workload(wl, mode=MODE_SKIP_IDLE) -> OracleResult:
     t, c = wl.topo, wl.coll
     return run(t.n_npus, t.n_switches, t.src, t.dst, t.alpha_ns, t.bw_GBps, c.n_chunks,
                c.chunk_bytes, c.pre, c.post, c.group_masks, c.chunk_group, c.op, wl.tie_seed,
-               mode)
+               mode, t.sw_buffer, t.sw_unicast)
 
 
 def splitmix64(seed: int, c: int) -> int:

@@ -29,7 +29,11 @@
  *     of Alg. 1);
  *   - reductions by time-reversing the dual non-reduction schedule, and
  *     All-Reduce as the reversed schedule followed by the forward one
- *     (Sec. 4.5).
+ *     (Sec. 4.5);
+ *   - optionally, explicit switch nodes (Sec. 4.7 "Modeling Switches"): a
+ *     switch with a finite buffer accepts a new chunk only while fewer chunks
+ *     than its capacity are buffered there, and a switch without multicast
+ *     forwards one copy of a chunk at a time.
  * The readings taken where the paper is silent (tie-breaks, rounding, the
  * clash rule, relay needs) are listed in the repository's design notes; each
  * is restated at the step it governs below.
@@ -148,15 +152,34 @@ static void dijkstra(uint32_t D, uint32_t s, const uint32_t *out_off, const uint
  * mode bit 0: skip the rescan of a free link whose candidate set was found
  * empty and whose source has received nothing since (result-identical: the
  * destination's needs only shrink, so the candidate set of such a link stays
- * empty).  Without it every free link rescans at every event, as the event
- * loop is stated.
+ * empty; the one other way a candidate reappears is a unicast switch source
+ * finishing a copy, which wakes that switch's out-links too).  Without it
+ * every free link rescans at every event, as the event loop is stated.
+ */
+/*
+ * Switch model (Sec. 4.7), both arrays indexed by switch (device N + i), NULL
+ * for none:
+ *   sw_buffer[i]  0 = unlimited; else the most chunks switch i buffers at
+ *                 once.  A chunk counts as buffered at switch w from the start
+ *                 of its transfer into w until no out-neighbour of w still
+ *                 needs it; a transfer into w may start only while fewer than
+ *                 sw_buffer chunks are buffered there (visiting w would
+ *                 otherwise exceed its buffer).  Several transfers into w that
+ *                 win their clashes in the same round take the free places in
+ *                 (link time, link id) order; the others stay in the round loop.
+ *   sw_unicast[i] 1 = no multicast: switch i never has two copies of one chunk
+ *                 in flight on its out-links (it visits its next neighbours
+ *                 one by one).  A free out-link of i skips chunks i is
+ *                 sending; out-links of i that pick the same chunk in one round
+ *                 clash, after the destination clash, with the same rule
+ *                 (fastest link, then lowest id).
  */
 int pccl_oracle_run(uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
                     const uint32_t *lsrc, const uint32_t *ldst, const uint32_t *alpha,
                     const uint32_t *bw, uint32_t C, uint64_t m, const uint64_t *pre,
                     const uint64_t *post, const uint64_t *group_masks, uint32_t n_groups,
                     const uint16_t *chunk_group, int op, uint64_t tie_seed, int mode,
-                    void **handle)
+                    const uint32_t *sw_buffer, const uint8_t *sw_unicast, void **handle)
 {
     or_result *r = calloc(1, sizeof *r);
     *handle = r;
@@ -329,6 +352,10 @@ int pccl_oracle_run(uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
     uint32_t *inflight = malloc(sizeof(uint32_t) * (L ? L : 1));
     uint32_t *pick = malloc(sizeof(uint32_t) * (L ? L : 1));
     char *active = calloc(L ? L : 1, 1), *win = calloc(L ? L : 1, 1);
+    char *win2 = calloc(L ? L : 1, 1), *win3 = calloc(L ? L : 1, 1);
+    uint32_t *occ = calloc(D, sizeof(uint32_t));  /* chunks buffered at each limited switch */
+#define SW_BUF(v) ((sw_buffer && (v) >= N) ? sw_buffer[(v) - N] : 0u)
+#define SW_UNI(v) ((sw_unicast && (v) >= N) ? sw_unicast[(v) - N] != 0 : 0)
     char *idle = calloc(L ? L : 1, 1);      /* mode bit 0 only */
     char *dst_picked = calloc(D, 1);
     for (uint32_t l = 0; l < L; l++) inflight[l] = NONE;
@@ -344,8 +371,12 @@ int pccl_oracle_run(uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
             if (inflight[l] != NONE && busy_until[l] == t) {
                 bit_set(holds + (uint64_t)ldst[l] * W, inflight[l]);
                 inflight[l] = NONE;
-                if (mode & 1)
+                if (mode & 1) {
                     for (uint32_t k = out_off[ldst[l]]; k < out_off[ldst[l] + 1]; k++) idle[out_link[k]] = 0;
+                    /* a unicast switch that finished a copy may send that chunk again */
+                    if (SW_UNI(lsrc[l]))
+                        for (uint32_t k = out_off[lsrc[l]]; k < out_off[lsrc[l] + 1]; k++) idle[out_link[k]] = 0;
+                }
             }
         }
         /* rounds: every free link picks; clashes on (destination, chunk) are
@@ -356,15 +387,42 @@ int pccl_oracle_run(uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
             n_active += active[l];
         }
         while (n_active > 0) {
+            /* buffered chunks of each limited switch w: present at w or in
+             * flight into it, and still needed by an out-neighbour of w */
+            for (uint32_t w = N; w < D; w++) {
+                if (!SW_BUF(w)) continue;
+                occ[w] = 0;
+                for (uint32_t q = 0; q < C; q++) {
+                    int present = bit_get(holds + (uint64_t)w * W, q);
+                    for (uint32_t k = in_off[w]; k < in_off[w + 1] && !present; k++)
+                        present = inflight[in_link[k]] == q;
+                    if (!present) continue;
+                    int wanted = 0;
+                    for (uint32_t k = out_off[w]; k < out_off[w + 1] && !wanted; k++)
+                        wanted = bit_get(needs + (uint64_t)ldst[out_link[k]] * W, q);
+                    occ[w] += (uint32_t)wanted;
+                }
+            }
             int any = 0;
             for (uint32_t l = 0; l < L; l++) {
                 if (!active[l]) continue;
-                const uint64_t *h = holds + (uint64_t)lsrc[l] * W, *nd = needs + (uint64_t)ldst[l] * W;
+                const uint32_t s = lsrc[l], d = ldst[l];
+                const uint64_t *h = holds + (uint64_t)s * W, *nd = needs + (uint64_t)d * W;
                 pick[l] = NONE;
-                for (uint64_t k = 0; k < W; k++) {
+                /* a full switch buffer admits nothing: the link stays in the
+                 * round loop (a later round may free a place) */
+                if (SW_BUF(d) && occ[d] >= SW_BUF(d)) continue;
+                for (uint64_t k = 0; k < W && pick[l] == NONE; k++) {
                     r->scan_words++;
                     uint64_t x = h[k] & nd[k];
-                    if (x) { pick[l] = (uint32_t)(k * 64 + (uint64_t)__builtin_ctzll(x)); break; }
+                    for (; x; x &= x - 1) {
+                        const uint32_t c = (uint32_t)(k * 64 + (uint64_t)__builtin_ctzll(x));
+                        int sending = 0;  /* a unicast switch already sends c */
+                        if (SW_UNI(s))
+                            for (uint32_t o = out_off[s]; o < out_off[s + 1] && !sending; o++)
+                                sending = inflight[out_link[o]] == c;
+                        if (!sending) { pick[l] = c; break; }
+                    }
                 }
                 if (pick[l] == NONE) {
                     active[l] = 0;
@@ -375,8 +433,9 @@ int pccl_oracle_run(uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
                 }
             }
             if (!any) break;
+            /* clash on (destination, chunk) */
             for (uint32_t l = 0; l < L; l++) {
-                if (!active[l]) continue;
+                if (!active[l] || pick[l] == NONE) continue;
                 win[l] = 1;
                 uint32_t d = ldst[l];
                 for (uint32_t k = in_off[d]; k < in_off[d + 1]; k++) {
@@ -386,10 +445,36 @@ int pccl_oracle_run(uint32_t n_npus, uint32_t n_switches, uint32_t n_links,
                 }
                 if (!dst_picked[d]) { dst_picked[d] = 1; r->rounds++; }
             }
+            /* clash on (unicast switch, chunk) among the destination winners */
             for (uint32_t l = 0; l < L; l++) {
-                if (!active[l]) continue;
+                if (!active[l] || pick[l] == NONE) continue;
+                win2[l] = win[l];
+                const uint32_t s = lsrc[l];
+                if (!win[l] || !SW_UNI(s)) continue;
+                for (uint32_t k = out_off[s]; k < out_off[s + 1]; k++) {
+                    uint32_t o = out_link[k];
+                    if (o == l || !active[o] || pick[o] == NONE || !win[o] || pick[o] != pick[l]) continue;
+                    if (T[o] < T[l] || (T[o] == T[l] && o < l)) win2[l] = 0;
+                }
+            }
+            /* free places of a limited switch buffer, in (link time, link id) order */
+            for (uint32_t l = 0; l < L; l++) {
+                if (!active[l] || pick[l] == NONE) continue;
+                win3[l] = win2[l];
+                const uint32_t d = ldst[l];
+                if (!win2[l] || !SW_BUF(d)) continue;
+                uint32_t ahead = 0;
+                for (uint32_t k = in_off[d]; k < in_off[d + 1]; k++) {
+                    uint32_t o = in_link[k];
+                    if (o == l || !active[o] || pick[o] == NONE || !win2[o]) continue;
+                    if (T[o] < T[l] || (T[o] == T[l] && o < l)) ahead++;
+                }
+                if (ahead >= SW_BUF(d) - occ[d]) win3[l] = 0;
+            }
+            for (uint32_t l = 0; l < L; l++) {
+                if (!active[l] || pick[l] == NONE) continue;
                 dst_picked[ldst[l]] = 0;
-                if (!win[l]) { r->clashes++; continue; }
+                if (!win3[l]) { r->clashes++; continue; }
                 uint64_t end = (uint64_t)t + T[l];
                 if (end > 0xFFFFFFFFull) { status = fail(r, OR_ERANGE, "time does not fit in 32 bits"); goto done; }
                 bit_clr(needs + (uint64_t)ldst[l] * W, pick[l]);
@@ -483,6 +568,9 @@ done:
     free(pick);
     free(active);
     free(win);
+    free(win2);
+    free(win3);
+    free(occ);
     free(idle);
     free(dst_picked);
     free(key);

@@ -93,6 +93,10 @@ class Topology:
     dst: np.ndarray      # uint32 [L]
     alpha_ns: np.ndarray  # uint32 [L]
     bw_GBps: np.ndarray   # uint32 [L]  (1 GB/s == 1 byte per ns)
+    # switch model (Sec. 4.7), one entry per switch, None for none:
+    # buffer capacity in chunks (0 = unlimited) and no-multicast flag
+    sw_buffer: Optional[np.ndarray] = None   # uint32 [n_switches]
+    sw_unicast: Optional[np.ndarray] = None  # uint8 [n_switches]
 
     @property
     def n_devices(self) -> int:
@@ -474,6 +478,58 @@ def sweep_grid4x4x4(k: int) -> Workload:
 
 
 SWEEP_TOPOLOGIES = {"mesh8x8": sweep_mesh8x8, "grid4x4x4": sweep_grid4x4x4}
+
+
+# --------------------------------------------------------------------------
+# Explicit switches (Sec. 4.7): finite buffers and switches without multicast
+# --------------------------------------------------------------------------
+
+def with_switch_model(topo: Topology, buffer=None, unicast=None) -> Topology:
+    """Copy of `topo` with a switch model: per switch, a buffer capacity in
+    chunks (0 = unlimited) and a no-multicast flag; scalars apply to all."""
+    S = topo.n_switches
+    b = None if buffer is None else np.broadcast_to(np.asarray(buffer, dtype=np.uint32), (S,)).copy()
+    u = None if unicast is None else np.broadcast_to(np.asarray(unicast, dtype=np.uint8), (S,)).copy()
+    return dataclasses.replace(topo, sw_buffer=b, sw_unicast=u)
+
+
+def star(n: int, alpha: int = 500, bw: int = 50) -> Topology:
+    """n NPUs around one switch (device n): link 2i is NPU i -> switch,
+    link 2i + 1 is switch -> NPU i."""
+    pairs = []
+    for i in range(n):
+        pairs += [(i, n), (n, i)]
+    return make_topology(n, 1, pairs, alpha, bw)
+
+
+def star_all_gather(n: int, chunks_per_npu: int = 1, buffer: int = 0, unicast: bool = False,
+                    chunk_bytes: int = 1 << 20, alpha: int = 500, bw: int = 50) -> Workload:
+    """All-Gather through one switch (the star test case of the switch model)."""
+    topo = with_switch_model(star(n, alpha, bw), buffer, int(unicast))
+    coll = all_gather(n, range(n), chunks_per_npu, chunk_bytes)
+    return Workload(f"star{n}_allgather_b{buffer}_u{int(unicast)}", topo, coll, 0)
+
+
+def hol_blocking(buffer: int) -> Workload:
+    """Head-of-line blocking through a small switch buffer.  NPUs 0-3 and
+    switch 4; links 0: 0->4, 1: 1->4, 2: 4->2, 3: 4->3, all 1,000 ns except
+    4->2 (4,000 ns).  Chunks 0 and 1 go from NPU 0 to NPU 2 (the slow way),
+    chunks 2 and 3 from NPU 1 to NPU 3; chunk size 900 B at 1 GB/s."""
+    pairs = [(0, 4), (1, 4), (4, 2), (4, 3)]
+    alpha = [100, 100, 3100, 100]
+    topo = with_switch_model(make_topology(4, 1, pairs, alpha, 1), buffer, 0)
+    coll = collective_from_lists(4, 4, 900, [0, 0, 1, 1], [[2], [2], [3], [3]], [range(4)])
+    return Workload(f"hol_blocking_b{buffer}", topo, coll, 0)
+
+
+def switch2level_model(n_nodes: int = 8, per_node: int = 4, buffer: int = 4, unicast: bool = True,
+                       chunk_bytes: int = 128 << 10) -> Workload:
+    """All-to-All on a small rail-switched cluster whose rail switches have
+    finite buffers and/or no multicast."""
+    topo = with_switch_model(switch2level(n_nodes, per_node), buffer, int(unicast))
+    n = n_nodes * per_node
+    coll = a2a_bitmaps(n, chunk_bytes)
+    return Workload(f"switch2level_{n}_a2a_b{buffer}_u{int(unicast)}", topo, coll, 0)
 SWEEP_K = (1, 2, 4, 8, 16, 32, 64)
 
 
@@ -536,3 +592,15 @@ def random_small(seed: int, n_npus=None, n_switches=None, max_chunks=40) -> Work
     coll = collective_from_lists(n, C, 1 + rng.rand(4096), src_of, dests_of, groups,
                                  chunk_group=cg if len(groups) > 1 else None)
     return Workload(f"random_small_{seed}", topo, coll, rng.next())
+
+
+def random_switched(seed: int, max_chunks: int = 40) -> Workload:
+    """random_small with one to three switches and a random switch model
+    (buffer 0 = unlimited or 1-4 chunks, multicast or not)."""
+    rng = SplitMix64(seed ^ 0x5EED5A17C4)
+    wl = random_small(seed, n_switches=1 + rng.rand(3), max_chunks=max_chunks)
+    S = wl.topo.n_switches
+    buf = [0 if rng.rand(3) == 0 else 1 + rng.rand(4) for _ in range(S)]
+    uni = [rng.rand(2) for _ in range(S)]
+    topo = with_switch_model(wl.topo, buf, uni)
+    return Workload(f"random_switched_{seed}", topo, wl.coll, wl.tie_seed)

@@ -80,3 +80,46 @@ def check_reversed_schedule(topo, coll, sends: np.ndarray, copy_time: int):
         back.append((rl, c, copy_time - int(t) - int(T[l]), 0))
     back = np.array(back, dtype=np.int64).reshape(-1, 4)
     check_copy_schedule(topo, coll, back, copy_time)
+
+
+def check_switch_model(topo, coll, sends: np.ndarray):
+    """Switch-model invariants of a copy schedule (Sec. 4.7), from the
+    definitions alone:
+      6. a switch without multicast never has two copies of one chunk in
+         flight: its transfers of a chunk have disjoint intervals;
+      7. a switch with a buffer of B chunks never holds more than B buffered
+         chunks at the end of an instant: chunk c is buffered at switch w
+         from the start of its transfer into w until the last start of a
+         transfer of c into an out-neighbour of w (every received chunk was
+         needed until its transfer started)."""
+    T = link_times(topo, coll.chunk_bytes)
+    src, dst = topo.src.astype(np.int64), topo.dst.astype(np.int64)
+    N, S = topo.n_npus, topo.n_switches
+    buf = topo.sw_buffer if topo.sw_buffer is not None else np.zeros(S, np.uint32)
+    uni = topo.sw_unicast if topo.sw_unicast is not None else np.zeros(S, np.uint8)
+    recv = {}  # (device, chunk) -> start of the transfer that delivered it
+    for l, c, t, _ in sends.astype(np.int64):
+        recv[(int(dst[l]), int(c))] = int(t)
+    for i in range(S):
+        w = N + i
+        if uni[i]:
+            spans = {}
+            for l, c, t, _ in sends.astype(np.int64):
+                if src[l] == w:
+                    spans.setdefault(int(c), []).append((int(t), int(t + T[l])))
+            for c, iv in spans.items():
+                iv.sort()
+                for (a0, a1), (b0, b1) in zip(iv, iv[1:]):
+                    assert a1 <= b0, f"unicast switch {w} sends chunk {c} twice at once ({a0}, {b0})"
+        if buf[i]:
+            outs = sorted({int(dst[l]) for l in range(len(src)) if src[l] == w})
+            spans = []
+            for (v, c), t_in in recv.items():
+                if v != w:
+                    continue
+                last = max((recv[(u, c)] for u in outs if (u, c) in recv), default=-1)
+                if last > t_in:
+                    spans.append((t_in, last))
+            for tau in sorted({a for a, _ in spans}):
+                occ = sum(1 for a, b in spans if a <= tau < b)
+                assert occ <= int(buf[i]), f"switch {w} buffers {occ} chunks at {tau} (capacity {int(buf[i])})"
