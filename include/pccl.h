@@ -10,9 +10,9 @@
  * schedule runs on one AMD Instinct GPU (gfx950); the host side only checks
  * and stages the small topology arrays and launches kernels.
  *
- * Call order: pccl_create -> pccl_load_topology -> pccl_set_collective ->
- * pccl_workspace_bytes -> pccl_set_workspace -> pccl_synthesize (any number
- * of times) -> pccl_get_schedule / pccl_get_stats / pccl_get_setup ->
+ * Call order: pccl_create -> pccl_load_topology -> [pccl_set_switch_model]
+ * -> pccl_set_collective -> pccl_workspace_bytes -> pccl_set_workspace ->
+ * pccl_synthesize (any number of times) -> pccl_get_schedule / pccl_get_stats / pccl_get_setup ->
  * pccl_destroy.  A call made out of order returns PCCL_ESTATE.  A context is
  * not thread-safe; use one per thread.
  *
@@ -129,6 +129,40 @@ pccl_status pccl_set_collective(pccl_ctx *ctx, uint32_t n_chunks, uint64_t chunk
                                 const uint64_t *pre_bits, const uint64_t *post_bits,
                                 const uint64_t *group_masks, uint32_t n_groups,
                                 const uint16_t *chunk_group, pccl_op op);
+
+/*
+ * Explicit switch nodes (paper Sec. 4.7, "Modeling Switches"): buffer limits
+ * and switches without multicast.  Optional; call after pccl_load_topology
+ * (which clears the model) and before pccl_workspace_bytes /
+ * pccl_set_workspace (the model changes the workspace; a workspace set
+ * earlier must be set again: PCCL_ESTATE until then).
+ *   n_switches: must equal the topology's switch count.
+ *   buffer_chunks: HOST pointer to n_switches uint32 (copied), or NULL for
+ *     all unlimited.  Entry i belongs to device n_npus + i: 0 = unlimited,
+ *     else the most chunks the switch buffers at once.  A chunk is buffered
+ *     at switch w from the start of its transfer into w until no
+ *     out-neighbour of w still needs it; a transfer into w starts only while
+ *     fewer chunks than the capacity are buffered there.  Transfers into w
+ *     that win their clashes at the same instant take the free places in
+ *     (link time, link id) order; the others wait.
+ *   unicast: HOST pointer to n_switches uint8 (copied), or NULL for all
+ *     multicast.  1 = the switch keeps at most one copy of a chunk in flight
+ *     on its out-links (it forwards a chunk to its next neighbours one by
+ *     one); out-links of such a switch that pick the same chunk at the same
+ *     instant clash, after the destination clash, fastest link first, then
+ *     the lowest link id.
+ * A model with no limit leaves the plain matcher in use.  With limits the
+ * matcher runs one workgroup per switch group: a unicast switch's
+ * out-neighbours, and a limited switch together with its out-neighbours,
+ * form one group.  PCCL_EUNSUPPORTED (from pccl_workspace_bytes /
+ * pccl_set_workspace) when a group has more than 1024 in-links, 1024
+ * distinct sources of those links, 4096 in-links of those sources, 64 limited
+ * or unicast switches, or more than 1024 buffer places (capacities at or
+ * above the chunk count count as unlimited).  Buffers can deadlock: then
+ * pccl_synthesize returns PCCL_EDEADLOCK.  PCCL_EINVAL on a count mismatch.
+ */
+pccl_status pccl_set_switch_model(pccl_ctx *ctx, uint32_t n_switches, const uint32_t *buffer_chunks,
+                                  const uint8_t *unicast);
 
 /*
  * Device workspace needed by pccl_synthesize for at most `max_sends`

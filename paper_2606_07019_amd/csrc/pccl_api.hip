@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <exception>
+#include <numeric>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -35,6 +36,17 @@ struct pccl_ctx {
     int op = 0;
     std::vector<uint32_t> T, slot_time;
     uint32_t tmin = 0;
+    // switch model (Sec. 4.7)
+    std::vector<uint32_t> sw_buf;  // per switch: buffer capacity, 0 = unlimited
+    std::vector<uint8_t> sw_uni;   // per switch: 1 = no multicast
+    bool sw_model = false;         // some switch has a limit
+    bool sw_built = false;         // tables below match the topology, model and chunk count
+    bool sw_active = false;        // the switch-model matching kernel runs
+    std::vector<uint32_t> swt;     // switch-model tables, uploaded as one region
+    std::vector<uint32_t> sw_links;  // links of each switch group
+    uint64_t swo[18] = {};         // offsets of the tables inside swt (order of SwTab)
+    uint32_t sw_groups = 0, sw_pool = 0, sw_nbt = 0;
+    int sw_grid = 0;
     // workspace
     char *ws = nullptr;
     size_t ws_bytes = 0;
@@ -153,7 +165,223 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.xslot = cv.take<uint64_t>(2ull * MAX_MATCH_GRID * XSLOT_WORDS);
     ly.wave_dest = cv.take<uint32_t>(D + (uint64_t)MATCH_WAVES * MAX_MATCH_GRID);
     ly.out = cv.take<pccl_send>((c->op == PCCL_OP_ALLREDUCE ? 2 : 1) * max_sends);
+    ly.sw = SwTab{};
+    if (c->sw_active) {
+        uint32_t *t = cv.take<uint32_t>(c->swt.size());
+        const uint32_t **p[18] = {&ly.sw.grp,    &ly.sw.blk,     &ly.sw.blk_list, &ly.sw.lk_slot, &ly.sw.lk_dl,
+                                  &ly.sw.lk_srcj, &ly.sw.lk_uni,  &ly.sw.lk_dbuf,  &ly.sw.lk_sbuf, &ly.sw.d_off,
+                                  &ly.sw.s_poff, &ly.sw.p_slot,  &ly.sw.u_off,    &ly.sw.u_list,  &ly.sw.b_cap,
+                                  &ly.sw.b_poff, &ly.sw.b_ooff,  &ly.sw.b_out};
+        for (int i = 0; i < 18; i++) *p[i] = t ? t + c->swo[i] : nullptr;
+        ly.sw.pool_c = cv.take<uint32_t>(c->sw_pool);
+        ly.sw.pool_n = cv.take<uint32_t>(c->sw_pool);
+        ly.sw.occ = cv.take<uint32_t>(c->sw_nbt);
+    }
     total = (cv.off + 255) & ~size_t(255);
+}
+
+// Switch groups (Sec. 4.7 switch model): the out-neighbours of a unicast
+// switch, and a limited switch with its out-neighbours, must share one
+// workgroup, since their links clash on the same copy or the same buffer.
+// Union-find closes those sets; each group lists its destinations' in-links
+// (destination-major), the distinct sources of those links with the source's
+// own in-links (where arrivals come from), its unicast switches with their
+// out-links, and its limited switches with their buffer places and
+// out-neighbours.  Capacities at or above the chunk count never bind and
+// count as unlimited.
+pccl_status build_switch_tables(pccl_ctx *c)
+{
+    c->sw_built = true;
+    c->sw_active = false;
+    c->swt.clear();
+    c->sw_links.clear();
+    if (!c->sw_model) return PCCL_OK;
+    const uint32_t N = c->N, S = c->S, D = c->D, L = c->L;
+    std::vector<uint32_t> cap(S);
+    std::vector<uint8_t> uni(S);
+    bool any = false;
+    for (uint32_t i = 0; i < S; i++) {
+        cap[i] = (c->sw_buf[i] && c->sw_buf[i] < c->C) ? c->sw_buf[i] : 0u;
+        uni[i] = c->sw_uni[i] ? 1 : 0;
+        any = any || cap[i] || uni[i];
+    }
+    if (!any) return PCCL_OK;
+    std::vector<uint32_t> out_off(D + 1, 0), out_l(L), slot_of(L);
+    for (uint32_t l = 0; l < L; l++) out_off[c->src[l] + 1]++;
+    for (uint32_t v = 0; v < D; v++) out_off[v + 1] += out_off[v];
+    {
+        std::vector<uint32_t> fill(out_off.begin(), out_off.end() - 1);
+        for (uint32_t l = 0; l < L; l++) out_l[fill[c->src[l]]++] = l;
+    }
+    for (uint32_t sl = 0; sl < L; sl++) slot_of[c->slot_link[sl]] = sl;
+    std::vector<uint32_t> par(D);
+    std::iota(par.begin(), par.end(), 0u);
+    auto find = [&](uint32_t v) {
+        while (par[v] != v) v = par[v] = par[par[v]];
+        return v;
+    };
+    auto unite = [&](uint32_t a, uint32_t b) {
+        a = find(a);
+        b = find(b);
+        if (a != b) par[std::max(a, b)] = std::min(a, b);
+    };
+    for (uint32_t i = 0; i < S; i++) {
+        const uint32_t v = N + i;
+        for (uint32_t k = out_off[v]; k < out_off[v + 1]; k++) {
+            if (uni[i]) unite(c->dst[out_l[out_off[v]]], c->dst[out_l[k]]);
+            if (cap[i]) unite(v, c->dst[out_l[k]]);
+        }
+    }
+    std::vector<uint32_t> gid_of_root(D, NONE32);
+    std::vector<std::vector<uint32_t>> members, limited;
+    for (uint32_t v = 0; v < D; v++) {
+        if (c->in_off[v + 1] == c->in_off[v]) continue;
+        const uint32_t r = find(v);
+        if (gid_of_root[r] == NONE32) {
+            gid_of_root[r] = (uint32_t)members.size();
+            members.emplace_back();
+        }
+        members[gid_of_root[r]].push_back(v);
+    }
+    limited.resize(members.size());
+    for (uint32_t i = 0; i < S; i++)
+        if (cap[i] && gid_of_root[find(N + i)] != NONE32) limited[gid_of_root[find(N + i)]].push_back(N + i);
+    const uint32_t G = (uint32_t)members.size();
+    std::vector<uint32_t> grp(16ull * G), lk_slot, lk_dl, lk_srcj, lk_uni, lk_dbuf, lk_sbuf, d_off, s_poff, p_slot,
+        u_off, u_list, b_cap, b_poff, b_ooff, b_out;
+    std::vector<uint32_t> loc(L, NONE32), sidx(D, NONE32), bidx(D, NONE32), uidx(D, NONE32);
+    uint32_t pool = 0;
+    for (uint32_t g = 0; g < G; g++) {
+        const auto &mem = members[g];
+        const uint32_t lbase = (uint32_t)lk_slot.size(), dbase = (uint32_t)d_off.size();
+        const uint32_t sbase = (uint32_t)s_poff.size(), pbase = (uint32_t)p_slot.size();
+        const uint32_t ubase = (uint32_t)u_off.size(), ulbase = (uint32_t)u_list.size();
+        const uint32_t bbase = (uint32_t)b_cap.size(), bobase = (uint32_t)b_out.size();
+        uint32_t nl = 0;
+        for (uint32_t dl = 0; dl < mem.size(); dl++) {
+            d_off.push_back(nl);
+            for (uint32_t sl = c->in_off[mem[dl]]; sl < c->in_off[mem[dl] + 1]; sl++) {
+                loc[sl] = nl++;
+                lk_slot.push_back(sl);
+                lk_dl.push_back(dl);
+            }
+        }
+        d_off.push_back(nl);
+        std::vector<uint32_t> srcs;
+        for (uint32_t i = 0; i < nl; i++) {
+            const uint32_t sv = c->slot_src[lk_slot[lbase + i]];
+            if (sidx[sv] == NONE32) {
+                sidx[sv] = (uint32_t)srcs.size();
+                srcs.push_back(sv);
+            }
+            lk_srcj.push_back(sidx[sv]);
+        }
+        uint32_t np = 0;
+        for (uint32_t sv : srcs) {
+            s_poff.push_back(np);
+            for (uint32_t sl = c->in_off[sv]; sl < c->in_off[sv + 1]; sl++, np++) p_slot.push_back(sl);
+        }
+        s_poff.push_back(np);
+        uint32_t nu = 0, nul = 0;
+        for (uint32_t sv : srcs) {
+            if (sv < N || !uni[sv - N]) continue;
+            uidx[sv] = nu++;
+            u_off.push_back(nul);
+            for (uint32_t k = out_off[sv]; k < out_off[sv + 1]; k++, nul++) {
+                const uint32_t li = loc[slot_of[out_l[k]]];
+                if (li == NONE32) return fail(c, PCCL_EINTERNAL, "unicast switch %u: out-link outside its group", sv);
+                u_list.push_back(li);
+            }
+        }
+        u_off.push_back(nul);
+        uint32_t nb = 0, pl = 0, no = 0;
+        for (uint32_t w : limited[g]) {
+            bidx[w] = nb++;
+            b_cap.push_back(cap[w - N]);
+            b_poff.push_back(pl);
+            b_ooff.push_back(no);
+            pl += cap[w - N];
+            for (uint32_t k = out_off[w]; k < out_off[w + 1]; k++, no++) b_out.push_back(c->dst[out_l[k]]);
+        }
+        b_cap.push_back(0);
+        b_poff.push_back(pl);
+        b_ooff.push_back(no);
+        for (uint32_t i = 0; i < nl; i++) {
+            const uint32_t sl = lk_slot[lbase + i], sv = c->slot_src[sl], dv = c->dst[c->slot_link[sl]];
+            lk_uni.push_back(uidx[sv]);
+            lk_dbuf.push_back(bidx[dv]);
+            lk_sbuf.push_back(bidx[sv]);
+        }
+        const uint32_t nd = (uint32_t)mem.size();
+        for (uint32_t i = 0; i < nl; i++) loc[lk_slot[lbase + i]] = NONE32;
+        for (uint32_t sv : srcs) {
+            sidx[sv] = NONE32;
+            uidx[sv] = NONE32;
+        }
+        for (uint32_t w : limited[g]) bidx[w] = NONE32;
+        if (nl > SW_MAX_LINKS || nd > SW_MAX_LINKS)
+            return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u has %u in-links (limit %u)", mem[0], nl,
+                        SW_MAX_LINKS);
+        if (srcs.size() > SW_MAX_SRC)
+            return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u has %zu sources (limit %u)", mem[0],
+                        srcs.size(), SW_MAX_SRC);
+        if (np > SW_MAX_PAIRS)
+            return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u: its sources have %u in-links (limit %u)",
+                        mem[0], np, SW_MAX_PAIRS);
+        if (nu > SW_MAX_SW || nb > SW_MAX_SW)
+            return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u has %u unicast and %u limited switches "
+                        "(limit %u each)", mem[0], nu, nb, SW_MAX_SW);
+        if (pl > SW_MAX_POOL)
+            return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u has %u buffer places (limit %u)", mem[0], pl,
+                        SW_MAX_POOL);
+        const uint32_t h[16] = {nl, lbase, nd, dbase, (uint32_t)srcs.size(), sbase, np, pbase,
+                                nu, ubase, ulbase, nb, bbase, bobase, pool, pl};
+        std::copy(h, h + 16, grp.begin() + 16ull * g);
+        pool += pl;
+        c->sw_links.push_back(nl);
+    }
+    std::vector<const std::vector<uint32_t> *> parts = {&grp,    nullptr, nullptr, &lk_slot, &lk_dl,  &lk_srcj,
+                                                        &lk_uni, &lk_dbuf, &lk_sbuf, &d_off,  &s_poff, &p_slot,
+                                                        &u_off,  &u_list,  &b_cap,   &b_poff, &b_ooff, &b_out};
+    uint64_t off = 0;
+    for (int i = 0; i < 18; i++) {
+        c->swo[i] = off;
+        off += i == 1 ? MAX_MATCH_GRID + 1ull : i == 2 ? (uint64_t)G : parts[i]->size();
+        off = (off + 63) & ~63ull;
+    }
+    c->swt.assign(off, 0u);
+    for (int i = 0; i < 18; i++)
+        if (parts[i]) std::copy(parts[i]->begin(), parts[i]->end(), c->swt.begin() + c->swo[i]);
+    c->sw_groups = G;
+    c->sw_pool = pool;
+    c->sw_nbt = (uint32_t)b_cap.size();
+    c->sw_active = true;
+    return PCCL_OK;
+}
+
+// Switch groups to workgroups: heaviest first, dealt round-robin.
+pccl_status deal_switch_groups(pccl_ctx *c)
+{
+    const uint32_t G = c->sw_groups, nb = (uint32_t)c->sw_grid;
+    std::vector<uint32_t> byweight(G);
+    std::iota(byweight.begin(), byweight.end(), 0u);
+    std::stable_sort(byweight.begin(), byweight.end(),
+                     [&](uint32_t a, uint32_t b) { return c->sw_links[a] > c->sw_links[b]; });
+    uint32_t *blk = c->swt.data() + c->swo[1], *list = c->swt.data() + c->swo[2];
+    uint32_t k = 0;
+    for (uint32_t b = 0; b < nb; b++) {
+        blk[b] = k;
+        uint64_t links = 0;
+        for (uint32_t i = b; i < G; i += nb) {
+            list[k++] = byweight[i];
+            links += c->sw_links[byweight[i]];
+        }
+        if (links >= (1u << 19))
+            return fail(c, PCCL_EUNSUPPORTED, "switch-model workgroup %u would own %llu links", b,
+                        (unsigned long long)links);
+    }
+    blk[nb] = k;
+    return PCCL_OK;
 }
 
 // Destinations of the matching kernel's waves: heaviest first (most arrival
@@ -298,6 +526,9 @@ pccl_status pccl_load_topology(pccl_ctx *c, uint32_t n_npus, uint32_t n_switches
     c->slot_cum.swap(slot_cum);
     c->dest_pairs.swap(dest_pairs);
     c->rev.swap(rev);
+    c->sw_buf.assign(n_switches, 0u);
+    c->sw_uni.assign(n_switches, 0u);
+    c->sw_model = c->sw_built = c->sw_active = false;
     c->have_topo = true;
     c->have_coll = c->have_ws = c->uploaded = c->have_result = false;
     return PCCL_OK;
@@ -355,6 +586,29 @@ pccl_status pccl_set_collective(pccl_ctx *c, uint32_t n_chunks, uint64_t chunk_b
     c->slot_time.swap(slot_time);
     c->tmin = c->L ? tmin : 1;
     c->have_coll = true;
+    c->sw_built = false;
+    c->have_ws = c->uploaded = c->have_result = false;
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_set_switch_model(pccl_ctx *c, uint32_t n_switches, const uint32_t *buffer_chunks,
+                                  const uint8_t *unicast)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    if (!c->have_topo) return fail(c, PCCL_ESTATE, "load a topology first");
+    if (n_switches != c->S)
+        return fail(c, PCCL_EINVAL, "switch model for %u switches, topology has %u", n_switches, c->S);
+    bool any = false;
+    for (uint32_t i = 0; i < c->S; i++) {
+        c->sw_buf[i] = buffer_chunks ? buffer_chunks[i] : 0u;
+        c->sw_uni[i] = unicast ? (unicast[i] != 0) : 0u;
+        any = any || c->sw_buf[i] || c->sw_uni[i];
+    }
+    c->sw_model = any;
+    c->sw_built = c->sw_active = false;
     c->have_ws = c->uploaded = c->have_result = false;
     return PCCL_OK;
     GUARD_END(c)
@@ -365,6 +619,10 @@ pccl_status pccl_workspace_bytes(pccl_ctx *c, uint64_t max_sends, size_t *out_by
     if (!c || !out_bytes) return PCCL_EINVAL;
     GUARD_BEGIN
     if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
+    if (!c->sw_built) {
+        const pccl_status st = build_switch_tables(c);
+        if (st != PCCL_OK) return st;
+    }
     Layout ly{};
     Sizes sz{};
     size_t total = 0;
@@ -382,6 +640,10 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
     if (!device_ptr) return fail(c, PCCL_EINVAL, "null workspace");
     if (reinterpret_cast<uintptr_t>(device_ptr) & 255u) return fail(c, PCCL_EINVAL, "workspace not 256-byte aligned");
+    if (!c->sw_built) {
+        const pccl_status st = build_switch_tables(c);
+        if (st != PCCL_OK) return st;
+    }
     const uint64_t ms = max_sends ? max_sends : safe_max_sends(c);
     Layout ly{};
     Sizes sz{};
@@ -405,6 +667,13 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
                             (int)((D1 + wpb - 1) / wpb));
     if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
     deal_destinations(c);
+    if (c->sw_active) {
+        c->sw_grid = std::min<int>(std::min<int>(match_sw_max_grid(c->device), (int)MAX_MATCH_GRID),
+                                   (int)c->sw_groups);
+        if (c->sw_grid <= 0) return fail(c, PCCL_EDEVICE, "switch-model matching kernel cannot be resident");
+        const pccl_status st = deal_switch_groups(c);
+        if (st != PCCL_OK) return st;
+    }
     c->have_ws = true;
     c->uploaded = c->have_result = false;
     return PCCL_OK;
@@ -432,6 +701,7 @@ static pccl_status upload(pccl_ctx *c)
     HIP_OR_FAIL(c, put(ly.dest_pairs, c->dest_pairs.data(), sizeof(uint32_t) * c->D));
     HIP_OR_FAIL(c, put(ly.wave_dest, c->wave_dest.data(), sizeof(uint32_t) * c->wave_dest.size()));
     HIP_OR_FAIL(c, put(ly.group_masks, c->gmask.data(), sizeof(uint64_t) * c->gmask.size()));
+    if (c->sw_active) HIP_OR_FAIL(c, put(const_cast<uint32_t *>(ly.sw.grp), c->swt.data(), sizeof(uint32_t) * c->swt.size()));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));
     c->uploaded = true;
     return PCCL_OK;
@@ -478,7 +748,10 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     HIP_OR_FAIL(c, hipEventRecord(c->ev[0], st));
     HIP_OR_FAIL(c, launch_setup(c->ly, c->sz, c->pre, c->post, c->chunk_group, c->seed, st));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[1], st));
-    HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb));
+    if (c->sw_active)
+        HIP_OR_FAIL(c, launch_match_sw(c->ly, c->sz, st, c->sw_grid));
+    else
+        HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
     HIP_OR_FAIL(c, hipMemcpyAsync(&c->ctl_host, c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));

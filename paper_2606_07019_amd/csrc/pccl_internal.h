@@ -23,6 +23,16 @@ constexpr uint32_t MAX_MATCH_GRID = 1024; // workgroups of the matching kernel (
 constexpr uint32_t MATCH_TARGET_GRID = 128; // workgroups the matching kernel aims for (measured on MI355X)
 constexpr uint32_t XSLOT_WORDS = 16;        // one 128-byte line per window exchange slot
 
+// Switch-model matching kernel envelope (one workgroup owns a switch group:
+// a switch with its out-neighbours; checked on the host).
+constexpr uint32_t SW_THREADS = 256;
+constexpr uint32_t SW_MAX_LINKS = 1024;  // in-links of the destinations of one group
+constexpr uint32_t SW_MAX_SRC = 1024;    // distinct sources of those links
+constexpr uint32_t SW_MAX_PAIRS = 4096;  // in-links of those sources (arrival slots)
+constexpr uint32_t SW_MAX_SW = 64;       // unicast or limited switches in one group
+constexpr uint32_t SW_MAX_POOL = 1024;   // buffer places of a group's limited switches
+constexpr uint8_t SW_NONE8 = 0xFF;
+
 // Status codes mirrored from the public header.
 enum : uint32_t {
     ST_OK = 0, ST_EINVAL = 1, ST_EUNREACHABLE = 2, ST_ERANGE = 3, ST_ENOMEM = 4,
@@ -70,6 +80,35 @@ __device__ inline uint64_t splitmix64_key(uint64_t seed, uint64_t c)
     return z ^ (z >> 31);
 }
 
+// Tables of the switch-model matching kernel, built on the host (one u32
+// region of the workspace).  Group g's header sits at grp[16 g]: link
+// count and base, destination count and base, source count and base, arrival
+// pair count and base, unicast switch count and base, unicast out-link list
+// base, limited switch count and base, out-neighbour list base, buffer pool
+// base and size.  Per-group arrays are indexed base + local index.
+struct SwTab {
+    const uint32_t *grp;      // [16 G]
+    const uint32_t *blk;      // [nb + 1] groups of workgroup b: blk_list[blk[b] .. blk[b+1])
+    const uint32_t *blk_list; // [G]
+    const uint32_t *lk_slot;  // destination-major slot of each group link
+    const uint32_t *lk_dl;    // its destination's index in the group
+    const uint32_t *lk_srcj;  // its source's index in the group's source list
+    const uint32_t *lk_uni;   // group index of its source if a unicast switch, else NONE32
+    const uint32_t *lk_dbuf;  // group index of its destination if a limited switch, else NONE32
+    const uint32_t *lk_sbuf;  // group index of its source if a limited switch, else NONE32
+    const uint32_t *d_off;    // [nD + 1] per group: links of destination dl
+    const uint32_t *s_poff;   // [nS + 1] per group: arrival pairs of source j
+    const uint32_t *p_slot;   // slot of each pair's link (an in-link of the source)
+    const uint32_t *u_off;    // [nU + 1] per group: out-links of unicast switch u
+    const uint32_t *u_list;   // group-local link indices
+    const uint32_t *b_cap;    // [nB + 1] per group: buffer capacity of limited switch b
+    const uint32_t *b_poff;   // [nB + 1] per group: its places in the group's pool
+    const uint32_t *b_ooff;   // [nB + 1] per group: its out-neighbours
+    const uint32_t *b_out;    // out-neighbour device ids
+    uint32_t *pool_c, *pool_n;  // buffer places: chunk, out-neighbours still needing it (0 = free)
+    uint32_t *occ;              // [nB + 1] per group: occupied places
+};
+
 // Pointers into the caller's workspace (all device memory).
 struct Layout {
     // topology, link order
@@ -103,6 +142,7 @@ struct Layout {
     unsigned long long *dest_log;  // [D] next send-log slot of each destination
     uint64_t *xslot;          // [2 * MAX_MATCH_GRID * XSLOT_WORDS] window exchange slots of the matching kernel
     uint32_t *wave_dest;      // [D + MATCH_WAVES * MAX_MATCH_GRID] destination of (pass, wave), NONE32 if none
+    SwTab sw;                 // switch-model tables (null pointers without a switch model)
     // output
     void *out;                // pccl_send [2 * max_sends]
     Control *ctl;
@@ -123,6 +163,8 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
                         const uint16_t *chunk_group, uint64_t seed, hipStream_t st);
 hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block);
 int match_max_grid(int device, int waves_per_block);
+hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
+int match_sw_max_grid(int device);
 hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st);
 // LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;
 // the sorted order ends up in buffer ly.ctl->sort_cur (read it on the device).

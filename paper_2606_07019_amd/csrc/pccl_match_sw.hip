@@ -1,0 +1,553 @@
+// Matching kernel for networks with explicit switch nodes (Sec. 4.7
+// "Modeling Switches"): a switch with a finite buffer takes a new chunk only
+// while fewer chunks than its capacity are buffered there, and a switch
+// without multicast keeps at most one copy of a chunk in flight on its
+// out-links.
+//
+// The clash groups of these rules reach across destinations: every out-link
+// of a unicast switch competes for the same copy, and a limited switch's
+// buffer empties as its out-neighbours receive their chunks.  So ownership
+// moves from one destination per wavefront to one *switch group* per
+// workgroup: a unicast switch's out-neighbours, and a limited switch with its
+// out-neighbours, belong to one group (closed under both rules on the host),
+// and every other device is a group of its own.  A group's links, link state,
+// per-round picks and buffer places live in LDS for the window; its
+// destinations' event times are merged and each event runs the round loop of
+// the event-stepped matching (pick, clash on (destination, chunk), clash on
+// (unicast switch, chunk), free buffer places, commit) with workgroup barriers
+// between the stages.
+//
+// Groups interact only through chunk arrivals, which take at least the
+// smallest link time, so the windows [t0, t0 + Tmin) of the plain matcher
+// carry over: each window folds the previous window's arrivals into the
+// holds rows and publishes the transfers in flight at t0 (first grid
+// barrier), then every group matches its events inside the window against
+// holds-at-t0 plus the arrival list read from those entries (second grid
+// barrier, which also finds the next event time).
+#include "pccl_internal.h"
+
+namespace pccl {
+namespace {
+
+constexpr uint32_t ST = SW_THREADS;
+constexpr uint32_t SWAVES = ST / 64;
+constexpr uint32_t SW_SPIN_LIMIT = 1u << 24;
+constexpr uint64_t STAG_MASK = 0xFFFull << 52;
+
+struct SwShared {
+    // per group link: state, static description and per-round scratch
+    uint32_t busy[SW_MAX_LINKS], infl[SW_MAX_LINKS], cur[SW_MAX_LINKS], pick[SW_MAX_LINKS];
+    uint32_t lsrc[SW_MAX_LINKS], ldst[SW_MAX_LINKS], ltim[SW_MAX_LINKS], llink[SW_MAX_LINKS];
+    uint32_t lslot[SW_MAX_LINKS];
+    uint16_t ldl[SW_MAX_LINKS], lsrcj[SW_MAX_LINKS];
+    uint8_t luni[SW_MAX_LINKS], ldbuf[SW_MAX_LINKS], lsbuf[SW_MAX_LINKS];
+    uint8_t win1[SW_MAX_LINKS], win2[SW_MAX_LINKS], win3[SW_MAX_LINKS];
+    uint16_t doff[SW_MAX_LINKS + 1];  // links of destination dl: [doff[dl], doff[dl + 1])
+    uint16_t poff[SW_MAX_SRC + 1];    // arrival pairs of source j
+    uint32_t arr_t[SW_MAX_PAIRS];     // arrival time inside the window, NONE32 if none
+    uint32_t arr_c[SW_MAX_PAIRS];     // arriving chunk
+    uint16_t uoff[SW_MAX_SW + 1], ulist[SW_MAX_LINKS];
+    uint32_t bcap[SW_MAX_SW];
+    uint16_t bpoff[SW_MAX_SW + 1], booff[SW_MAX_SW + 1];
+    uint32_t bout[SW_MAX_LINKS];
+    uint32_t pc[SW_MAX_POOL], pn[SW_MAX_POOL], occ[SW_MAX_SW];
+    uint32_t red[SWAVES];
+    uint32_t x_tmin, x_err, x_ok;
+    unsigned long long x_sent;
+};
+
+struct SwGroup {
+    uint32_t nL, lbase, nD, dbase, nS, sbase, nP, pbase, nU, ubase, ulbase, nB, bbase, bobase, pool_base, pool_n;
+};
+
+__device__ inline SwGroup load_group(const SwTab &sw, uint32_t g)
+{
+    const uint32_t *h = sw.grp + 16ull * g;
+    SwGroup x;
+    x.nL = h[0];
+    x.lbase = h[1];
+    x.nD = h[2];
+    x.dbase = h[3];
+    x.nS = h[4];
+    x.sbase = h[5];
+    x.nP = h[6];
+    x.pbase = h[7];
+    x.nU = h[8];
+    x.ubase = h[9];
+    x.ulbase = h[10];
+    x.nB = h[11];
+    x.bbase = h[12];
+    x.bobase = h[13];
+    x.pool_base = h[14];
+    x.pool_n = h[15];
+    return x;
+}
+
+__device__ inline uint8_t small_index(uint32_t v) { return v == NONE32 ? SW_NONE8 : (uint8_t)v; }
+
+__device__ inline bool need_bit(const uint64_t *row, uint32_t c)
+{
+    const uint64_t w = __hip_atomic_load(&row[c >> 6], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (w >> (c & 63u)) & 1ull;
+}
+
+__device__ inline uint64_t link_key(const SwShared &sh, uint32_t i)
+{
+    return ((uint64_t)sh.ltim[i] << 32) | sh.llink[i];
+}
+
+__device__ uint32_t block_min(SwShared &sh, uint32_t v)
+{
+    for (int off = 32; off; off >>= 1) v = min(v, (uint32_t)__shfl_xor(v, off));
+    if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint32_t m = NONE32;
+    for (uint32_t w = 0; w < SWAVES; w++) m = min(m, sh.red[w]);
+    __syncthreads();
+    return m;
+}
+
+// Grid barrier with a reduction: every workgroup publishes (tag, error,
+// transfers committed, earliest transfer end in flight) in its own 128-byte
+// slot; wave 0 polls all slots.  Two slot sets alternate, so a workgroup
+// that is already one barrier ahead does not overwrite a slot still read.
+__device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tmin, uint32_t sent, uint32_t err,
+                        SwShared &sh)
+{
+    const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
+    const uint64_t tag = (uint64_t)(gen & 0xFFFu) << 52;
+    uint64_t *slot = xslot + (uint64_t)(gen & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores and atomics are done
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&slot[(uint64_t)blockIdx.x * XSLOT_WORDS],
+                           tag | ((uint64_t)(err ? 1u : 0u) << 51) | ((uint64_t)(sent & 0x7FFFFu) << 32) | tmin,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x < 64) {
+        uint32_t spins = 0, ok = 1, tn = NONE32, e = 0;
+        unsigned long long s = 0;
+        while (true) {
+            bool all = true;
+            tn = NONE32;
+            e = 0;
+            s = 0;
+            for (uint32_t b = lane; b < nb; b += 64) {
+                const uint64_t a = __hip_atomic_load(&slot[(uint64_t)b * XSLOT_WORDS], __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                if ((a & STAG_MASK) != tag) all = false;
+                tn = min(tn, (uint32_t)a);
+                e |= (uint32_t)(a >> 51) & 1u;
+                s += (a >> 32) & 0x7FFFFull;
+            }
+            if (__ballot(!all) == 0) break;
+            if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                ok = 0;
+                break;
+            }
+            if (++spins > SW_SPIN_LIMIT) {
+                if (lane == 0) atomicExch(&ctl->abort, 1u);
+                ok = 0;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        // acquire: drop cached lines that other workgroups wrote
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        for (int off = 32; off; off >>= 1) {
+            tn = min(tn, (uint32_t)__shfl_xor(tn, off));
+            e |= (uint32_t)__shfl_xor(e, off);
+            s += (unsigned long long)__shfl_xor(s, off);
+        }
+        if (lane == 0) {
+            sh.x_tmin = tn;
+            sh.x_err = e;
+            sh.x_sent = s;
+            sh.x_ok = ok;
+        }
+    }
+    __syncthreads();
+    return sh.x_ok != 0;
+}
+
+// First half of a window, for one group: fold the arrivals of the previous
+// window into the destinations' holds rows, then publish the transfers in
+// flight at t0 (the entries other groups read their arrival lists from).
+__device__ void fold_and_publish(const Layout &ly, const Sizes &sz, const SwGroup &gp, uint32_t t0)
+{
+    for (uint32_t i = threadIdx.x; i < gp.nL; i += ST) {
+        const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
+        const uint32_t d = ly.ldst[ly.slot_link[sl]];
+        const uint64_t e = ly.snap[sl];
+        if (e != NONE64 && (uint32_t)e < t0) {
+            const uint32_t c = (uint32_t)(e >> 32);
+            __hip_atomic_fetch_or(&ly.holds[(uint64_t)d * sz.Wp + (c >> 6)], 1ull << (c & 63u), __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const uint32_t in = ly.infl[sl], b = ly.busy[sl];
+        const uint64_t ne = (in != NONE32 && b >= t0) ? (((uint64_t)in << 32) | b) : NONE64;
+        __hip_atomic_store(&ly.snap[sl], ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__device__ void load_group_state(const Layout &ly, const SwGroup &gp, SwShared &sh)
+{
+    const SwTab &sw = ly.sw;
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t i = tid; i < gp.nL; i += ST) {
+        const uint32_t x = gp.lbase + i, sl = sw.lk_slot[x], l = ly.slot_link[sl];
+        sh.lslot[i] = sl;
+        sh.llink[i] = l;
+        sh.lsrc[i] = ly.lsrc[l];
+        sh.ldst[i] = ly.ldst[l];
+        sh.ltim[i] = ly.slot_time[sl];
+        sh.ldl[i] = (uint16_t)sw.lk_dl[x];
+        sh.lsrcj[i] = (uint16_t)sw.lk_srcj[x];
+        sh.luni[i] = small_index(sw.lk_uni[x]);
+        sh.ldbuf[i] = small_index(sw.lk_dbuf[x]);
+        sh.lsbuf[i] = small_index(sw.lk_sbuf[x]);
+        sh.busy[i] = ly.busy[sl];
+        sh.infl[i] = ly.infl[sl];
+        sh.cur[i] = ly.cur[sl];
+    }
+    for (uint32_t x = tid; x <= gp.nD; x += ST) sh.doff[x] = (uint16_t)sw.d_off[gp.dbase + x];
+    for (uint32_t x = tid; x <= gp.nS; x += ST) sh.poff[x] = (uint16_t)sw.s_poff[gp.sbase + x];
+    for (uint32_t x = tid; x <= gp.nU; x += ST) sh.uoff[x] = (uint16_t)sw.u_off[gp.ubase + x];
+    for (uint32_t x = tid; x <= gp.nB; x += ST) {
+        sh.bpoff[x] = (uint16_t)sw.b_poff[gp.bbase + x];
+        sh.booff[x] = (uint16_t)sw.b_ooff[gp.bbase + x];
+        if (x < gp.nB) {
+            sh.bcap[x] = sw.b_cap[gp.bbase + x];
+            sh.occ[x] = sw.occ[gp.bbase + x];
+        }
+    }
+    for (uint32_t x = tid; x < gp.pool_n; x += ST) {
+        sh.pc[x] = sw.pool_c[gp.pool_base + x];
+        sh.pn[x] = sw.pool_n[gp.pool_base + x];
+    }
+    __syncthreads();
+    // list lengths are known once the offsets are in LDS
+    const uint32_t nul = gp.nU ? sh.uoff[gp.nU] : 0u;
+    for (uint32_t x = tid; x < nul; x += ST) sh.ulist[x] = (uint16_t)sw.u_list[gp.ulbase + x];
+    const uint32_t nbo = gp.nB ? sh.booff[gp.nB] : 0u;
+    for (uint32_t x = tid; x < nbo; x += ST) sh.bout[x] = sw.b_out[gp.bobase + x];
+}
+
+// A unicast switch keeps one copy of a chunk in flight: is chunk c in flight
+// on one of switch u's out-links at time t?
+__device__ inline bool sending(const SwShared &sh, uint32_t u, uint32_t c, uint32_t t)
+{
+    for (uint32_t q = sh.uoff[u]; q < sh.uoff[u + 1]; q++) {
+        const uint32_t j = sh.ulist[q];
+        if (sh.busy[j] > t && sh.infl[j] == c) return true;
+    }
+    return false;
+}
+
+// The pick of free link i at event t (the BFS step: the first chunk in
+// priority order that the source holds and the destination still needs),
+// skipping chunks its unicast source switch is already sending.  Candidates
+// are the source's holds row as of the window start, scanned from the link's
+// cursor (no such chunk lies below it), and the chunks arriving at the source
+// inside the window up to t.
+__device__ uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, uint32_t i, uint32_t t,
+                              unsigned long long &words)
+{
+    const uint64_t *hs = ly.holds + (uint64_t)sh.lsrc[i] * sz.Wp;
+    const uint64_t *nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
+    const uint32_t u = sh.luni[i] == SW_NONE8 ? NONE32 : sh.luni[i];
+    const uint32_t cu = sh.cur[i];
+    uint32_t best = NONE32, first = NONE32;
+    for (uint64_t w = cu >> 6; w < sz.W && best == NONE32; w++) {
+        words++;
+        uint64_t x = hs[w] & __hip_atomic_load(&nd[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (w == (cu >> 6)) x &= NONE64 << (cu & 63u);
+        for (; x; x &= x - 1) {
+            const uint32_t c = (uint32_t)(w * 64 + (uint64_t)__builtin_ctzll(x));
+            if (first == NONE32) first = c;
+            if (u == NONE32 || !sending(sh, u, c, t)) {
+                best = c;
+                break;
+            }
+        }
+    }
+    sh.cur[i] = first == NONE32 ? (uint32_t)(sz.W * 64) : first;
+    const uint32_t j = sh.lsrcj[i];
+    for (uint32_t p = sh.poff[j]; p < sh.poff[j + 1]; p++) {
+        const uint32_t a = sh.arr_t[p], c = sh.arr_c[p];
+        if (a == NONE32 || a > t || c >= best) continue;
+        if (need_bit(nd, c) && (u == NONE32 || !sending(sh, u, c, t))) best = c;
+    }
+    return best;
+}
+
+struct SwAcc {
+    uint32_t tmin, cstar, err, sent;
+    unsigned long long rounds, clashes, words;
+};
+
+// Second half of a window, for one group: the group's events inside
+// [t0, t1), in time order, each with its round loop.
+__device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp, SwShared &sh, uint32_t t0,
+                            uint64_t t1, bool first_window, SwAcc &acc)
+{
+    const uint32_t tid = threadIdx.x;
+    load_group_state(ly, gp, sh);
+    // arrivals at the group's sources inside the window, from the entries
+    // published at t0 (the source's in-links, pair p of source j)
+    for (uint32_t p = tid; p < gp.nP; p += ST) {
+        const uint64_t e = ly.snap[ly.sw.p_slot[gp.pbase + p]];
+        const uint32_t b = (uint32_t)e;
+        const bool in = e != NONE64 && b >= t0 && (uint64_t)b < t1;
+        sh.arr_t[p] = in ? b : NONE32;
+        sh.arr_c[p] = (uint32_t)(e >> 32);
+    }
+    __syncthreads();
+    int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
+    for (;;) {
+        // next event of the group: a transfer into it ends, or a chunk
+        // arrives at one of its sources (time 0 opens the first window)
+        uint32_t m = (first_window && t_prev < 0) ? 0u : NONE32;
+        for (uint32_t i = tid; i < gp.nL; i += ST) {
+            const uint32_t b = sh.busy[i];
+            if (sh.infl[i] != NONE32 && (int64_t)b > t_prev && (uint64_t)b < t1) m = min(m, b);
+        }
+        for (uint32_t p = tid; p < gp.nP; p += ST) {
+            const uint32_t a = sh.arr_t[p];
+            if (a != NONE32 && (int64_t)a > t_prev) m = min(m, a);
+        }
+        const uint32_t t = block_min(sh, m);
+        if (t == NONE32) break;
+        for (;;) {
+            // picks of the free links; a full buffer admits nothing
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                uint32_t pk = NONE32;
+                if (sh.busy[i] <= t) {
+                    const uint32_t b = sh.ldbuf[i];
+                    if (b == SW_NONE8 || sh.occ[b] < sh.bcap[b]) pk = pick_link(ly, sz, sh, i, t, acc.words);
+                }
+                sh.pick[i] = pk;
+            }
+            __syncthreads();
+            // clash on (destination, chunk): fastest link, then lowest id
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                const uint32_t pk = sh.pick[i];
+                uint8_t w = pk != NONE32;
+                if (w) {
+                    const uint64_t key = link_key(sh, i);
+                    const uint32_t dl = sh.ldl[i];
+                    bool first = true;  // rounds are counted per destination that picked
+                    for (uint32_t j = sh.doff[dl]; j < sh.doff[dl + 1]; j++) {
+                        if (j < i && sh.pick[j] != NONE32) first = false;
+                        if (j != i && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
+                    }
+                    if (first) acc.rounds++;
+                }
+                sh.win1[i] = w;
+            }
+            __syncthreads();
+            // clash on (unicast switch, chunk) among the destination winners
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                uint8_t w = sh.win1[i];
+                const uint32_t u = sh.luni[i];
+                if (w && u != SW_NONE8) {
+                    const uint32_t pk = sh.pick[i];
+                    const uint64_t key = link_key(sh, i);
+                    for (uint32_t q = sh.uoff[u]; q < sh.uoff[u + 1]; q++) {
+                        const uint32_t j = sh.ulist[q];
+                        if (j != i && sh.win1[j] && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
+                    }
+                }
+                sh.win2[i] = w;
+            }
+            __syncthreads();
+            // free places of a limited switch, in (link time, link id) order
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                uint8_t w = sh.win2[i];
+                const uint32_t b = sh.ldbuf[i];
+                if (w && b != SW_NONE8) {
+                    const uint64_t key = link_key(sh, i);
+                    const uint32_t dl = sh.ldl[i];
+                    uint32_t ahead = 0;
+                    for (uint32_t j = sh.doff[dl]; j < sh.doff[dl + 1]; j++)
+                        if (j != i && sh.win2[j] && link_key(sh, j) < key) ahead++;
+                    if (ahead >= sh.bcap[b] - sh.occ[b]) w = 0;
+                }
+                sh.win3[i] = w;
+            }
+            __syncthreads();
+            // commit: the destination no longer needs the chunk, so neither
+            // do the limited switches feeding it on its behalf
+            uint32_t mine = 0;
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                const uint32_t pk = sh.pick[i];
+                if (pk == NONE32) continue;
+                if (!sh.win3[i]) {
+                    acc.clashes++;
+                    continue;
+                }
+                const uint32_t d = sh.ldst[i];
+                __hip_atomic_fetch_and(&ly.needs[(uint64_t)d * sz.Wp + (pk >> 6)], ~(1ull << (pk & 63u)),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t dl = sh.ldl[i];
+                for (uint32_t j = sh.doff[dl]; j < sh.doff[dl + 1]; j++) {
+                    const uint32_t b = sh.lsbuf[j];
+                    if (b == SW_NONE8) continue;
+                    for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
+                        if (sh.pc[s] == pk && sh.pn[s] != 0u) {
+                            if (atomicSub(&sh.pn[s], 1u) == 1u) atomicSub(&sh.occ[b], 1u);
+                            break;
+                        }
+                }
+                const uint64_t end = (uint64_t)t + sh.ltim[i];
+                if (end > 0xFFFFFFFFull) {
+                    record_error(ly.ctl, ST_ERANGE, pk, d, 2);
+                    acc.err = 1;
+                }
+                const uint32_t e32 = end > 0xFFFFFFFFull ? NONE32 - 1u : (uint32_t)end;
+                sh.busy[i] = e32;
+                sh.infl[i] = pk;
+                acc.cstar = max(acc.cstar, e32);
+                const unsigned long long q = atomicAdd(&ly.dest_log[d], 1ull);
+                ly.skey[0][q] = ((uint64_t)t << 32) | sh.llink[i];
+                ly.sval[0][q] = pk;
+                mine++;
+            }
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // the needs updates are done before the next stage reads them
+            __syncthreads();
+            // a limited switch that took a chunk buffers it while an
+            // out-neighbour still needs it
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                const uint32_t b = sh.ldbuf[i];
+                if (!sh.win3[i] || b == SW_NONE8) continue;
+                const uint32_t pk = sh.pick[i];
+                uint32_t cnt = 0;
+                for (uint32_t q = sh.booff[b]; q < sh.booff[b + 1]; q++)
+                    cnt += need_bit(ly.needs + (uint64_t)sh.bout[q] * sz.Wp, pk) ? 1u : 0u;
+                if (!cnt) continue;
+                for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
+                    if (atomicCAS(&sh.pn[s], 0u, cnt) == 0u) {
+                        sh.pc[s] = pk;
+                        atomicAdd(&sh.occ[b], 1u);
+                        break;
+                    }
+            }
+            acc.sent += mine;
+            const int any = __syncthreads_or(mine != 0);
+            if (!any) break;
+        }
+        t_prev = t;
+    }
+    // chunks that arrived at a source inside the window join its holds row
+    // at the next window start: no link cursor may stay above them
+    uint32_t tm = NONE32;
+    for (uint32_t i = tid; i < gp.nL; i += ST) {
+        const uint32_t j = sh.lsrcj[i];
+        uint32_t c = sh.cur[i];
+        for (uint32_t p = sh.poff[j]; p < sh.poff[j + 1]; p++)
+            if (sh.arr_t[p] != NONE32) c = min(c, sh.arr_c[p]);
+        const uint32_t sl = sh.lslot[i];
+        ly.cur[sl] = c;
+        ly.busy[sl] = sh.busy[i];
+        ly.infl[sl] = sh.infl[i];
+        if (sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1) tm = min(tm, sh.busy[i]);
+    }
+    acc.tmin = min(acc.tmin, tm);
+    for (uint32_t x = tid; x < gp.pool_n; x += ST) {
+        ly.sw.pool_c[gp.pool_base + x] = sh.pc[x];
+        ly.sw.pool_n[gp.pool_base + x] = sh.pn[x];
+    }
+    for (uint32_t x = tid; x < gp.nB; x += ST) ly.sw.occ[gp.bbase + x] = sh.occ[x];
+    __syncthreads();
+}
+
+__global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
+{
+    __shared__ SwShared sh;
+    Control *ctl = ly.ctl;
+    if (__hip_atomic_load(&ctl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+    const uint32_t tid = threadIdx.x;
+    if (ctl->needs_total == 0) {
+        if (blockIdx.x == 0 && tid == 0) ctl->windows = 0;
+        return;
+    }
+    const SwTab &sw = ly.sw;
+    const uint32_t q0 = sw.blk[blockIdx.x], q1 = sw.blk[blockIdx.x + 1];
+    // empty buffers
+    for (uint32_t q = q0; q < q1; q++) {
+        const SwGroup gp = load_group(sw, sw.blk_list[q]);
+        for (uint32_t x = tid; x < gp.pool_n; x += ST) sw.pool_n[gp.pool_base + x] = 0u;
+        for (uint32_t x = tid; x < gp.nB; x += ST) sw.occ[gp.bbase + x] = 0u;
+    }
+    const unsigned long long max_windows = ctl->needs_total + 2ull;
+    unsigned long long remaining = ctl->needs_total;
+    SwAcc acc = {NONE32, 0u, 0u, 0u, 0ull, 0ull, 0ull};
+    uint32_t t0 = 0, gen = 0;
+    unsigned long long k = 0;
+    for (;; k++) {
+        const uint64_t t1 = (uint64_t)t0 + sz.tmin;
+        for (uint32_t q = q0; q < q1; q++) fold_and_publish(ly, sz, load_group(sw, sw.blk_list[q]), t0);
+        if (!sw_sync(ctl, ly.xslot, ++gen, NONE32, 0u, 0u, sh)) break;
+        acc.tmin = NONE32;
+        acc.sent = 0;
+        for (uint32_t q = q0; q < q1; q++)
+            match_group(ly, sz, load_group(sw, sw.blk_list[q]), sh, t0, t1, k == 0, acc);
+        const uint32_t btmin = block_min(sh, acc.tmin);
+        uint32_t bsent = acc.sent;
+        for (int off = 32; off; off >>= 1) bsent += (uint32_t)__shfl_xor(bsent, off);
+        if ((tid & 63) == 0) sh.red[tid >> 6] = bsent;
+        __syncthreads();
+        bsent = 0;
+        for (uint32_t w = 0; w < SWAVES; w++) bsent += sh.red[w];
+        const int berr = __syncthreads_or(acc.err != 0);
+        if (!sw_sync(ctl, ly.xslot, ++gen, btmin, bsent, (uint32_t)berr, sh)) break;
+        remaining -= sh.x_sent;
+        if (sh.x_err || remaining == 0) break;
+        if (sh.x_tmin == NONE32) {
+            record_error(ctl, ST_EDEADLOCK, (uint32_t)remaining, 0, 0);
+            break;
+        }
+        if (k + 1 >= max_windows) {
+            record_error(ctl, ST_EINTERNAL, 1, 0, 0);
+            break;
+        }
+        t0 = sh.x_tmin;
+    }
+    if (blockIdx.x == 0 && tid == 0) {
+        ctl->needs_remaining = remaining;
+        ctl->windows = k + 1;
+        ctl->n_log = ctl->needs_total - remaining;
+    }
+    for (int off = 32; off; off >>= 1) {
+        acc.cstar = max(acc.cstar, (uint32_t)__shfl_xor(acc.cstar, off));
+        acc.rounds += (unsigned long long)__shfl_xor(acc.rounds, off);
+        acc.clashes += (unsigned long long)__shfl_xor(acc.clashes, off);
+        acc.words += (unsigned long long)__shfl_xor(acc.words, off);
+    }
+    if ((tid & 63) == 0) {
+        atomicMax(&ctl->cstar, acc.cstar);
+        if (acc.clashes) atomicAdd(&ctl->clashes, acc.clashes);
+        if (acc.words) atomicAdd(&ctl->scan_words, acc.words);
+        if (acc.rounds) atomicAdd(&ctl->rounds, acc.rounds);
+    }
+}
+
+}  // namespace
+
+int match_sw_max_grid(int device)
+{
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_match_sw, ST, 0) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return 0;
+    return per_cu * cus;
+}
+
+hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid)
+{
+    if (grid < 1 || grid > (int)MAX_MATCH_GRID) return hipErrorInvalidValue;
+    Layout l = ly;
+    Sizes s = sz;
+    void *args[] = {&l, &s};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_match_sw), dim3(grid), dim3(ST), args, 0, st);
+}
+
+}  // namespace pccl

@@ -56,6 +56,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "pccl_destroy": ([P], None),
         "pccl_load_topology": ([P, U32, U32, U32, P, P, P, P], I),
         "pccl_set_collective": ([P, U32, U64, P, P, P, U32, P, I], I),
+        "pccl_set_switch_model": ([P, U32, P, P], I),
         "pccl_workspace_bytes": ([P, U64, ctypes.POINTER(ctypes.c_size_t)], I),
         "pccl_set_workspace": ([P, P, ctypes.c_size_t, U64, P], I),
         "pccl_synthesize": ([P, ctypes.POINTER(U64), ctypes.POINTER(U32)], I),
@@ -121,6 +122,16 @@ def pccl_set_collective(h, n_chunks, chunk_bytes, pre_bits_dev_ptr, post_bits_de
         chunk_group_dev_ptr, op))
 
 
+def pccl_set_switch_model(h, n_switches, buffer_chunks=None, unicast=None) -> None:
+    """buffer_chunks / unicast: host arrays with one entry per switch, or None."""
+    b = None if buffer_chunks is None else np.ascontiguousarray(buffer_chunks, dtype=np.uint32)
+    u = None if unicast is None else np.ascontiguousarray(unicast, dtype=np.uint8)
+    for a in (b, u):
+        if a is not None and a.shape != (n_switches,):
+            raise ValueError("switch model arrays need one entry per switch")
+    _check(h, load_library().pccl_set_switch_model(h, n_switches, _np_ptr(b), _np_ptr(u)))
+
+
 def pccl_workspace_bytes(h, max_sends: int = 0) -> int:
     out = ctypes.c_size_t()
     _check(h, load_library().pccl_workspace_bytes(h, max_sends, ctypes.byref(out)))
@@ -181,6 +192,9 @@ class Synthesizer:
         self.h = pccl_create(device, tie_seed)
         pccl_load_topology(self.h, topo.n_npus, topo.n_switches, topo.src, topo.dst,
                            topo.alpha_ns, topo.bw_GBps)
+        sw_buffer, sw_unicast = getattr(topo, "sw_buffer", None), getattr(topo, "sw_unicast", None)
+        if sw_buffer is not None or sw_unicast is not None:
+            pccl_set_switch_model(self.h, topo.n_switches, sw_buffer, sw_unicast)
         self.pre = torch.from_numpy(coll.pre.view(np.int64).copy()).to(self.dev)
         self.post = torch.from_numpy(coll.post.view(np.int64).copy()).to(self.dev)
         self.cg = None

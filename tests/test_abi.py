@@ -31,6 +31,7 @@ def lib():
 def test_header_declares_the_documented_calls():
     names = declared()
     for n in ["pccl_create", "pccl_destroy", "pccl_load_topology", "pccl_set_collective",
+              "pccl_set_switch_model",
               "pccl_workspace_bytes", "pccl_set_workspace", "pccl_synthesize",
               "pccl_get_schedule", "pccl_get_stats", "pccl_get_setup", "pccl_get_profile",
               "pccl_last_error"]:

@@ -1,0 +1,94 @@
+"""GPU parity of the switch model (Sec. 4.7): the switch-group matching
+kernel against the CPU oracle, element by element, on the hand-worked
+cases, the broadcast closed forms, a buffer deadlock, seeded random
+switched topologies and rail-switched clusters.  Runs through the C ABI."""
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2606_07019_amd import workloads as W
+from tests.test_switch_model import HAND_WORKLOADS, _broadcast, _crossing
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_gpu(wl):
+    from paper_2606_07019_amd.pccl import Synthesizer, PcclError
+    s = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed)
+    try:
+        try:
+            s.synthesize()
+        except PcclError as e:
+            return e.name, None, None, None
+        return "PCCL_OK", s.schedule(), s.collective_time, s.stats()
+    finally:
+        s.close()
+
+
+def _compare(wl, label):
+    print(f"[switch parity] {label}: {wl.name}", flush=True)
+    ref = O.run_workload(wl)
+    status, sched, ct, st = _run_gpu(wl)
+    if ref.status != 0:
+        assert status == "PCCL_" + ref.status_name, (status, ref.message)
+        return
+    assert status == "PCCL_OK"
+    assert ct == ref.collective_time
+    np.testing.assert_array_equal(sched, ref.sends)
+    assert st["events"] == ref.stats["events"]
+    assert st["rounds"] == ref.stats["rounds"]
+    assert st["clashes"] == ref.stats["clashes"]
+
+
+@pytest.mark.parametrize("name", sorted(HAND_WORKLOADS))
+def test_hand_worked_parity(name):
+    _compare(HAND_WORKLOADS[name](), name)
+
+
+@pytest.mark.parametrize("n,k", [(3, 2), (4, 3), (9, 5)])
+@pytest.mark.parametrize("buffer,unicast", [(0, True), (1, True), (1, False)])
+def test_broadcast_parity(n, k, buffer, unicast):
+    _compare(_broadcast(n, k, buffer, unicast), "broadcast")
+
+
+@pytest.mark.parametrize("buffer", [1, 2])
+def test_crossing_parity(buffer):
+    # buffer 1 deadlocks: both sides must report PCCL_EDEADLOCK
+    _compare(_crossing(buffer), "crossing")
+
+
+@pytest.mark.parametrize("seed", list(range(40)))
+def test_random_switched_parity(seed):
+    _compare(W.random_switched(seed), f"switched seed {seed}")
+
+
+@pytest.mark.parametrize("seed", [3, 11, 19])
+@pytest.mark.parametrize("op", [1, 2])
+def test_random_switched_reduction_parity(seed, op):
+    wl = W.random_switched(seed)
+    wl.coll.op = op
+    _compare(wl, f"switched seed {seed} op {op}")
+
+
+@pytest.mark.parametrize("buffer,unicast", [(1, True), (2, False), (4, True), (0, True), (3, False)])
+def test_rail_cluster_parity(buffer, unicast):
+    _compare(W.switch2level_model(4, 4, buffer, unicast), "rail cluster")
+
+
+def test_larger_rail_cluster_parity():
+    # 16 nodes x 8 NPUs, 8 unicast rail switches with 4 buffer places: 8
+    # switch groups (a rail switch and its 16 NPUs), one per workgroup
+    _compare(W.switch2level_model(16, 8, 4, True, chunk_bytes=64 << 10), "rail cluster 128")
+
+
+def test_model_without_limits_uses_the_plain_matcher():
+    # zero capacities, capacities at or above the chunk count, no unicast:
+    # the schedule is the plain one
+    wl = W.random_small(5, n_switches=2)
+    ref = O.run_workload(wl)
+    for buf in (0, wl.coll.n_chunks, wl.coll.n_chunks + 7):
+        t = W.with_switch_model(wl.topo, buf, 0)
+        status, sched, ct, _ = _run_gpu(W.Workload(wl.name, t, wl.coll, wl.tie_seed))
+        assert status == "PCCL_OK" and ct == ref.collective_time
+        np.testing.assert_array_equal(sched, ref.sends)
