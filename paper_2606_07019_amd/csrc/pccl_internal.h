@@ -25,10 +25,10 @@ constexpr uint32_t XSLOT_WORDS = 16;        // one 128-byte line per window exch
 
 // Switch-model matching kernel envelope (one workgroup owns a switch group:
 // a switch with its out-neighbours; checked on the host).
-constexpr uint32_t SW_THREADS = 256;
+constexpr uint32_t SW_THREADS = 1024;
 constexpr uint32_t SW_MAX_LINKS = 1024;  // in-links of the destinations of one group
 constexpr uint32_t SW_MAX_SRC = 1024;    // distinct sources of those links
-constexpr uint32_t SW_MAX_PAIRS = 4096;  // in-links of those sources (arrival slots)
+constexpr uint32_t SW_MAX_PAIRS = 8192;  // in-links of those sources (arrival slots)
 constexpr uint32_t SW_MAX_SW = 64;       // unicast or limited switches in one group
 constexpr uint32_t SW_MAX_POOL = 1024;   // buffer places of a group's limited switches
 constexpr uint8_t SW_NONE8 = 0xFF;

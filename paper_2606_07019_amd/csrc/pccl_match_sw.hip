@@ -32,6 +32,9 @@ namespace {
 constexpr uint32_t ST = SW_THREADS;
 constexpr uint32_t SWAVES = ST / 64;
 constexpr uint32_t SW_SPIN_LIMIT = 1u << 24;
+constexpr uint32_t SCAN_STEP = 4;  // row words one link's scan loads at once
+constexpr uint32_t PEND = 4;       // needed chunks below a link's cursor it keeps as explicit candidates
+static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
 
 struct SwShared {
@@ -46,6 +49,9 @@ struct SwShared {
     uint16_t poff[SW_MAX_SRC + 1];    // arrival pairs of source j
     uint32_t arr_t[SW_MAX_PAIRS];     // arrival time inside the window, NONE32 if none
     uint32_t arr_c[SW_MAX_PAIRS];     // arriving chunk
+    uint64_t amask[SW_MAX_LINKS];     // arrivals (bit q: pair q of the source) the link's destination needs
+    uint32_t pend[SW_MAX_LINKS][PEND];  // needed arrivals outside [cur, hi), NONE32 = empty
+    uint32_t hi[SW_MAX_LINKS];          // a link's row candidates lie in [cur, hi) (or in pend)
     uint16_t uoff[SW_MAX_SW + 1], ulist[SW_MAX_LINKS];
     uint32_t bcap[SW_MAX_SW];
     uint16_t bpoff[SW_MAX_SW + 1], booff[SW_MAX_SW + 1];
@@ -84,6 +90,13 @@ __device__ inline SwGroup load_group(const SwTab &sw, uint32_t g)
 }
 
 __device__ inline uint8_t small_index(uint32_t v) { return v == NONE32 ? SW_NONE8 : (uint8_t)v; }
+
+// Pending candidates of slot sl when they leave LDS: PEND words in the
+// second and third snapshot planes, which this kernel does not use otherwise.
+__device__ inline uint64_t pend_index(const Sizes &sz, uint32_t sl)
+{
+    return (uint64_t)sz.L + (uint64_t)sl * (PEND / 2);
+}
 
 __device__ inline bool need_bit(const uint64_t *row, uint32_t c)
 {
@@ -172,24 +185,25 @@ __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tm
 // First half of a window, for one group: fold the arrivals of the previous
 // window into the destinations' holds rows, then publish the transfers in
 // flight at t0 (the entries other groups read their arrival lists from).
-__device__ void fold_and_publish(const Layout &ly, const Sizes &sz, const SwGroup &gp, uint32_t t0)
+__device__ void fold_and_publish(const Layout &ly, const Sizes &sz, const SwGroup &gp, uint32_t t0,
+                                 const SwShared &sh, bool in_lds)
 {
     for (uint32_t i = threadIdx.x; i < gp.nL; i += ST) {
-        const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
-        const uint32_t d = ly.ldst[ly.slot_link[sl]];
+        const uint32_t sl = in_lds ? sh.lslot[i] : ly.sw.lk_slot[gp.lbase + i];
+        const uint32_t d = in_lds ? sh.ldst[i] : ly.ldst[ly.slot_link[sl]];
         const uint64_t e = ly.snap[sl];
         if (e != NONE64 && (uint32_t)e < t0) {
             const uint32_t c = (uint32_t)(e >> 32);
             __hip_atomic_fetch_or(&ly.holds[(uint64_t)d * sz.Wp + (c >> 6)], 1ull << (c & 63u), __ATOMIC_RELAXED,
                                   __HIP_MEMORY_SCOPE_AGENT);
         }
-        const uint32_t in = ly.infl[sl], b = ly.busy[sl];
+        const uint32_t in = in_lds ? sh.infl[i] : ly.infl[sl], b = in_lds ? sh.busy[i] : ly.busy[sl];
         const uint64_t ne = (in != NONE32 && b >= t0) ? (((uint64_t)in << 32) | b) : NONE64;
         __hip_atomic_store(&ly.snap[sl], ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
-__device__ void load_group_state(const Layout &ly, const SwGroup &gp, SwShared &sh)
+__device__ void load_group_state(const Layout &ly, const Sizes &sz, const SwGroup &gp, SwShared &sh)
 {
     const SwTab &sw = ly.sw;
     const uint32_t tid = threadIdx.x;
@@ -208,6 +222,10 @@ __device__ void load_group_state(const Layout &ly, const SwGroup &gp, SwShared &
         sh.busy[i] = ly.busy[sl];
         sh.infl[i] = ly.infl[sl];
         sh.cur[i] = ly.cur[sl];
+        sh.hi[i] = (uint32_t)(sz.W * 64) - ly.lflags[sl];  // stored as the distance to the row end
+        const uint32_t *pg = reinterpret_cast<const uint32_t *>(ly.snap + pend_index(sz, sl));
+#pragma unroll
+        for (uint32_t e = 0; e < PEND; e++) sh.pend[i][e] = pg[e];
     }
     for (uint32_t x = tid; x <= gp.nD; x += ST) sh.doff[x] = (uint16_t)sw.d_off[gp.dbase + x];
     for (uint32_t x = tid; x <= gp.nS; x += ST) sh.poff[x] = (uint16_t)sw.s_poff[gp.sbase + x];
@@ -246,38 +264,93 @@ __device__ inline bool sending(const SwShared &sh, uint32_t u, uint32_t c, uint3
 // The pick of free link i at event t (the BFS step: the first chunk in
 // priority order that the source holds and the destination still needs),
 // skipping chunks its unicast source switch is already sending.  Candidates
-// are the source's holds row as of the window start, scanned from the link's
-// cursor (no such chunk lies below it), and the chunks arriving at the source
-// inside the window up to t.
+// come from three places: the source's holds row as of the window start,
+// scanned from the link's cursor (no such chunk lies below it); earlier
+// arrivals kept below the cursor; and chunks arriving at the source inside
+// the window up to t.  The needs words are read through the caches: only
+// this workgroup clears bits of its destinations' rows and nothing sets them
+// while matching, so a cached word can only show a chunk as still needed.
+// The lowest candidate is confirmed with one coherent load; a stale one is
+// dropped where it came from and the pick repeats.
 __device__ uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, uint32_t i, uint32_t t,
                               unsigned long long &words)
 {
     const uint64_t *hs = ly.holds + (uint64_t)sh.lsrc[i] * sz.Wp;
     const uint64_t *nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
     const uint32_t u = sh.luni[i] == SW_NONE8 ? NONE32 : sh.luni[i];
-    const uint32_t cu = sh.cur[i];
-    uint32_t best = NONE32, first = NONE32;
-    for (uint64_t w = cu >> 6; w < sz.W && best == NONE32; w++) {
-        words++;
-        uint64_t x = hs[w] & __hip_atomic_load(&nd[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (w == (cu >> 6)) x &= NONE64 << (cu & 63u);
-        for (; x; x &= x - 1) {
-            const uint32_t c = (uint32_t)(w * 64 + (uint64_t)__builtin_ctzll(x));
-            if (first == NONE32) first = c;
-            if (u == NONE32 || !sending(sh, u, c, t)) {
-                best = c;
-                break;
+    const uint32_t base = sh.poff[sh.lsrcj[i]];
+    const uint32_t hi = sh.hi[i];
+    const uint64_t wend = min<uint64_t>(sz.W, ((uint64_t)hi + 63) >> 6);
+    uint32_t skip = 0;  // row hits below this were found delivered in this call
+    for (;;) {
+        // row: the first cached hit at or above the cursor (the new cursor)
+        // and the first one from `skip` on that the source switch is not
+        // sending (the row candidate)
+        const uint32_t cu = sh.cur[i];
+        uint32_t row = NONE32, first = NONE32;
+        bool done = false;
+        for (uint64_t w0 = cu >> 6; w0 < wend && !done; w0 += SCAN_STEP) {
+            uint64_t x[SCAN_STEP];
+#pragma unroll
+            for (uint32_t k = 0; k < SCAN_STEP; k++) {
+                const uint64_t w = w0 + k;
+                x[k] = w < wend ? hs[w] & nd[w] : 0ull;
+            }
+            x[0] &= NONE64 << (w0 == (cu >> 6) ? (cu & 63u) : 0u);
+            words += min<uint64_t>(SCAN_STEP, wend - w0);
+#pragma unroll
+            for (uint32_t k = 0; k < SCAN_STEP; k++) {
+                for (uint64_t y = done ? 0ull : x[k]; y; y &= y - 1) {
+                    const uint32_t c = (uint32_t)((w0 + k) * 64 + (uint64_t)__builtin_ctzll(y));
+                    if (c >= hi) {
+                        done = true;
+                        break;
+                    }
+                    if (first == NONE32) first = c;
+                    if (c >= skip && (u == NONE32 || !sending(sh, u, c, t))) {
+                        row = c;
+                        done = true;
+                        break;
+                    }
+                }
             }
         }
+        sh.cur[i] = first == NONE32 ? max(cu, hi) : first;
+        uint32_t best = row, from = 0, slot = 0;
+        // earlier arrivals kept below the cursor
+#pragma unroll
+        for (uint32_t e = 0; e < PEND; e++) {
+            const uint32_t c = sh.pend[i][e];
+            if (c == NONE32 || c >= best) continue;
+            if (!((nd[c >> 6] >> (c & 63u)) & 1ull)) {
+                sh.pend[i][e] = NONE32;
+                continue;
+            }
+            if (u != NONE32 && sending(sh, u, c, t)) continue;
+            best = c;
+            from = 1;
+            slot = e;
+        }
+        // arrivals up to t that the destination may still need
+        for (uint64_t y = sh.amask[i]; y; y &= y - 1) {
+            const uint32_t q = (uint32_t)__builtin_ctzll(y), p = base + q, c = sh.arr_c[p];
+            if (sh.arr_t[p] > t || c >= best) continue;
+            if (u != NONE32 && sending(sh, u, c, t)) continue;
+            best = c;
+            from = 2;
+            slot = q;
+        }
+        if (best == NONE32 || need_bit(nd, best)) return best;
+        // delivered since its word was cached: drop it and pick again
+        if (from == 0) {
+            if (best == first) sh.cur[i] = best + 1;
+            skip = best + 1;
+        } else if (from == 1) {
+            sh.pend[i][slot] = NONE32;
+        } else {
+            sh.amask[i] &= ~(1ull << slot);
+        }
     }
-    sh.cur[i] = first == NONE32 ? (uint32_t)(sz.W * 64) : first;
-    const uint32_t j = sh.lsrcj[i];
-    for (uint32_t p = sh.poff[j]; p < sh.poff[j + 1]; p++) {
-        const uint32_t a = sh.arr_t[p], c = sh.arr_c[p];
-        if (a == NONE32 || a > t || c >= best) continue;
-        if (need_bit(nd, c) && (u == NONE32 || !sending(sh, u, c, t))) best = c;
-    }
-    return best;
 }
 
 struct SwAcc {
@@ -288,10 +361,11 @@ struct SwAcc {
 // Second half of a window, for one group: the group's events inside
 // [t0, t1), in time order, each with its round loop.
 __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp, SwShared &sh, uint32_t t0,
-                            uint64_t t1, bool first_window, SwAcc &acc)
+                            uint64_t t1, bool first_window, bool resident, SwAcc &acc)
 {
     const uint32_t tid = threadIdx.x;
-    load_group_state(ly, gp, sh);
+    // a workgroup with one group keeps its tables and state in LDS
+    if (!resident || first_window) load_group_state(ly, sz, gp, sh);
     // arrivals at the group's sources inside the window, from the entries
     // published at t0 (the source's in-links, pair p of source j)
     for (uint32_t p = tid; p < gp.nP; p += ST) {
@@ -300,6 +374,33 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         const bool in = e != NONE64 && b >= t0 && (uint64_t)b < t1;
         sh.arr_t[p] = in ? b : NONE32;
         sh.arr_c[p] = (uint32_t)(e >> 32);
+    }
+    for (uint32_t i = tid; i < gp.nL; i += ST) sh.amask[i] = 0ull;
+    __syncthreads();
+    // which arrivals each link's destination may still need: (link, pair)
+    // items spread over the workgroup, need words loaded four at a time
+    // through the caches (a superset: picks confirm each candidate)
+    const uint32_t nx = gp.nL * 64u;
+    for (uint32_t x0 = tid; x0 < nx; x0 += 4u * ST) {
+        bool v[4];
+        uint32_t c[4];
+        const uint64_t *row[4];
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++) {
+            const uint32_t x = x0 + k * ST, i = x >> 6, j = i < gp.nL ? sh.lsrcj[i] : 0u;
+            const uint32_t p = i < gp.nL ? sh.poff[j] + (x & 63u) : 0u;
+            v[k] = x < nx && p < sh.poff[j + 1] && sh.arr_t[p] != NONE32;
+            c[k] = v[k] ? sh.arr_c[p] : 0u;
+            row[k] = ly.needs + (uint64_t)(v[k] ? sh.ldst[i] : 0u) * sz.Wp;
+        }
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++) v[k] = v[k] && ((row[k][c[k] >> 6] >> (c[k] & 63u)) & 1ull);
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++)
+            if (v[k]) {
+                const uint32_t x = x0 + k * ST;
+                atomicOr((unsigned long long *)&sh.amask[x >> 6], 1ull << (x & 63u));
+            }
     }
     __syncthreads();
     int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
@@ -421,8 +522,14 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 if (!sh.win3[i] || b == SW_NONE8) continue;
                 const uint32_t pk = sh.pick[i];
                 uint32_t cnt = 0;
-                for (uint32_t q = sh.booff[b]; q < sh.booff[b + 1]; q++)
-                    cnt += need_bit(ly.needs + (uint64_t)sh.bout[q] * sz.Wp, pk) ? 1u : 0u;
+                for (uint32_t q0 = sh.booff[b]; q0 < sh.booff[b + 1]; q0 += 4) {
+                    bool nb[4];
+#pragma unroll
+                    for (uint32_t k = 0; k < 4; k++)
+                        nb[k] = q0 + k < sh.booff[b + 1] && need_bit(ly.needs + (uint64_t)sh.bout[q0 + k] * sz.Wp, pk);
+#pragma unroll
+                    for (uint32_t k = 0; k < 4; k++) cnt += nb[k] ? 1u : 0u;
+                }
                 if (!cnt) continue;
                 for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
                     if (atomicCAS(&sh.pn[s], 0u, cnt) == 0u) {
@@ -438,25 +545,52 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         t_prev = t;
     }
     // chunks that arrived at a source inside the window join its holds row
-    // at the next window start: no link cursor may stay above them
+    // at the next window start, possibly outside the region [cur, hi) a
+    // link still scans: the link keeps the ones its destination still needs
+    // as pending candidates, and only when those are full widens the region
+    // to cover them (the others can never be candidates again)
     uint32_t tm = NONE32;
     for (uint32_t i = tid; i < gp.nL; i += ST) {
-        const uint32_t j = sh.lsrcj[i];
-        uint32_t c = sh.cur[i];
-        for (uint32_t p = sh.poff[j]; p < sh.poff[j + 1]; p++)
-            if (sh.arr_t[p] != NONE32) c = min(c, sh.arr_c[p]);
-        const uint32_t sl = sh.lslot[i];
-        ly.cur[sl] = c;
-        ly.busy[sl] = sh.busy[i];
-        ly.infl[sl] = sh.infl[i];
+        const uint64_t *nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
+        const uint32_t base = sh.poff[sh.lsrcj[i]];
+        uint32_t c = sh.cur[i], h = sh.hi[i];
+        for (uint64_t y = sh.amask[i]; y; y &= y - 1) {
+            const uint32_t ac = sh.arr_c[base + (uint32_t)__builtin_ctzll(y)];
+            if ((c <= ac && ac < h) || !need_bit(nd, ac)) continue;
+            uint32_t e = 0;
+            while (e < PEND && sh.pend[i][e] != NONE32 && sh.pend[i][e] != ac) e++;
+            if (e < PEND) {
+                sh.pend[i][e] = ac;
+            } else if (c >= h) {
+                c = ac;
+                h = ac + 1;
+            } else {
+                c = min(c, ac);
+                h = max(h, ac + 1);
+            }
+        }
+        sh.cur[i] = c;
+        sh.hi[i] = h;
         if (sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1) tm = min(tm, sh.busy[i]);
+        if (!resident) {
+            const uint32_t sl = sh.lslot[i];
+            ly.cur[sl] = c;
+            ly.lflags[sl] = (uint32_t)(sz.W * 64) - h;
+            ly.busy[sl] = sh.busy[i];
+            ly.infl[sl] = sh.infl[i];
+            uint32_t *pg = reinterpret_cast<uint32_t *>(ly.snap + pend_index(sz, sl));
+#pragma unroll
+            for (uint32_t e = 0; e < PEND; e++) pg[e] = sh.pend[i][e];
+        }
     }
     acc.tmin = min(acc.tmin, tm);
-    for (uint32_t x = tid; x < gp.pool_n; x += ST) {
-        ly.sw.pool_c[gp.pool_base + x] = sh.pc[x];
-        ly.sw.pool_n[gp.pool_base + x] = sh.pn[x];
+    if (!resident) {
+        for (uint32_t x = tid; x < gp.pool_n; x += ST) {
+            ly.sw.pool_c[gp.pool_base + x] = sh.pc[x];
+            ly.sw.pool_n[gp.pool_base + x] = sh.pn[x];
+        }
+        for (uint32_t x = tid; x < gp.nB; x += ST) ly.sw.occ[gp.bbase + x] = sh.occ[x];
     }
-    for (uint32_t x = tid; x < gp.nB; x += ST) ly.sw.occ[gp.bbase + x] = sh.occ[x];
     __syncthreads();
 }
 
@@ -472,6 +606,7 @@ __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
     }
     const SwTab &sw = ly.sw;
     const uint32_t q0 = sw.blk[blockIdx.x], q1 = sw.blk[blockIdx.x + 1];
+    const bool resident = q1 - q0 == 1;
     // empty buffers
     for (uint32_t q = q0; q < q1; q++) {
         const SwGroup gp = load_group(sw, sw.blk_list[q]);
@@ -485,12 +620,13 @@ __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
     unsigned long long k = 0;
     for (;; k++) {
         const uint64_t t1 = (uint64_t)t0 + sz.tmin;
-        for (uint32_t q = q0; q < q1; q++) fold_and_publish(ly, sz, load_group(sw, sw.blk_list[q]), t0);
+        for (uint32_t q = q0; q < q1; q++)
+            fold_and_publish(ly, sz, load_group(sw, sw.blk_list[q]), t0, sh, resident && k > 0);
         if (!sw_sync(ctl, ly.xslot, ++gen, NONE32, 0u, 0u, sh)) break;
         acc.tmin = NONE32;
         acc.sent = 0;
         for (uint32_t q = q0; q < q1; q++)
-            match_group(ly, sz, load_group(sw, sw.blk_list[q]), sh, t0, t1, k == 0, acc);
+            match_group(ly, sz, load_group(sw, sw.blk_list[q]), sh, t0, t1, k == 0, resident, acc);
         const uint32_t btmin = block_min(sh, acc.tmin);
         uint32_t bsent = acc.sent;
         for (int off = 32; off; off >>= 1) bsent += (uint32_t)__shfl_xor(bsent, off);

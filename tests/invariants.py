@@ -113,13 +113,15 @@ def check_switch_model(topo, coll, sends: np.ndarray):
                     assert a1 <= b0, f"unicast switch {w} sends chunk {c} twice at once ({a0}, {b0})"
         if buf[i]:
             outs = sorted({int(dst[l]) for l in range(len(src)) if src[l] == w})
-            spans = []
+            delta = {}
             for (v, c), t_in in recv.items():
                 if v != w:
                     continue
                 last = max((recv[(u, c)] for u in outs if (u, c) in recv), default=-1)
-                if last > t_in:
-                    spans.append((t_in, last))
-            for tau in sorted({a for a, _ in spans}):
-                occ = sum(1 for a, b in spans if a <= tau < b)
+                if last > t_in:  # buffered over [t_in, last)
+                    delta[t_in] = delta.get(t_in, 0) + 1
+                    delta[last] = delta.get(last, 0) - 1
+            occ = 0
+            for tau in sorted(delta):  # occupancy at the end of each instant
+                occ += delta[tau]
                 assert occ <= int(buf[i]), f"switch {w} buffers {occ} chunks at {tau} (capacity {int(buf[i])})"
