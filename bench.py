@@ -9,6 +9,7 @@ pre/postcondition bitmaps already resident in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config k] [--no-cpu-baseline]
     python bench.py --sweep   # chunk-count sweep: 64-NPU All-to-All, 1..64 chunks per pair
+    python bench.py --switch-model   # the same 512-NPU All-to-All with finite switch buffers / no multicast
 """
 
 from __future__ import annotations
@@ -122,6 +123,55 @@ def sweep(args, W, Synthesizer, torch):
     }), flush=True)
 
 
+SWITCH_POINTS = ((64, 8, 0, True), (64, 8, 64, True), (64, 8, 16, False), (16, 8, 4, True))
+
+
+def switch_model(args, W, Synthesizer, torch):
+    """Rail-cluster All-to-All with explicit switch nodes (Sec. 4.7): the
+    switch-group matching kernel on the 512-NPU topology (unicast rail
+    switches, with and without a buffer limit) and on 16 nodes x 8 NPUs,
+    where the oracle is also timed."""
+    steps = max(1, min(args.steps, 3))
+    points = []
+    for nn, pn, buf, uni in SWITCH_POINTS:
+        wl = W.switch2level_model(nn, pn, buf, uni)
+        syn = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed, device=0)
+        syn.synthesize()
+        torch.cuda.synchronize()
+        match_ms = []
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            syn.synthesize()
+            match_ms.append(syn.profile()["match_ms"])
+        torch.cuda.synchronize()
+        step_s = (time.perf_counter() - t0) / steps
+        st, pr = syn.stats(), syn.profile()
+        kms = sum(match_ms) / len(match_ms)
+        alg = BYTES_PER_SCANNED_WORD * pr["scan_words"] + BYTES_PER_MATCH * syn.n_sends
+        pt = {"workload": wl.name, "npus": nn * pn, "buffer_chunks": buf, "unicast": bool(uni),
+              "sends": syn.n_sends, "collective_time_ns": syn.collective_time, "windows": st["windows"],
+              "synthesis_ms": step_s * 1e3, "match_ms": kms, "matches_per_s": syn.n_sends / step_s,
+              "roofline": {"bound": "hbm", "kernel": "k_match_sw", "achieved": round(alg / (kms * 1e-3) / 1e9, 3),
+                           "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                           "frac": round(alg / (kms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 6),
+                           "alg_bytes_per_launch": alg, "scan_words": pr["scan_words"]}}
+        syn.close()
+        if nn * pn <= 128 and not args.no_cpu_baseline:
+            log(f"[switch] timing the CPU oracle on {wl.name} ...")
+            pt["cpu_baseline"] = cpu_baseline(wl)
+        log(f"[switch] {wl.name}: {pt['synthesis_ms']:.1f} ms, {pt['sends']} sends, collective {syn.collective_time} ns")
+        points.append(pt)
+    head = points[1]
+    print(json.dumps({
+        "metric": "synthesis wall time + link-chunk matches/s, 512-NPU All-to-All with a switch model (Sec. 4.7)",
+        "value": head["matches_per_s"], "unit": "matches/s", "n_gpus": 1, "steps": steps, "warmup": 1,
+        "ms_per_step": head["synthesis_ms"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": head["workload"], "points": len(points)},
+        "points": points,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -129,6 +179,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--switch-model", action="store_true",
+                    help="512-NPU All-to-All with finite switch buffers / no multicast (Sec. 4.7)")
     ap.add_argument("--sweep", action="store_true",
                     help="time the chunk-count sweep (8x8 mesh and 4x4x4 grid All-to-All, k = 1..64)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -158,6 +210,9 @@ def main():
         raise RuntimeError("no GPU visible")
     if args.sweep:
         sweep(args, W, Synthesizer, torch)
+        return
+    if args.switch_model:
+        switch_model(args, W, Synthesizer, torch)
         return
     wl = W.CONFIGS[args.config]()
     log(f"[bench] workload {wl.name}: {wl.topo.n_devices} devices, {wl.topo.n_links} links, "
