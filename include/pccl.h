@@ -201,6 +201,24 @@ pccl_status pccl_synthesize(pccl_ctx *ctx, uint64_t *n_sends, uint32_t *collecti
 pccl_status pccl_get_schedule(pccl_ctx *ctx, pccl_send *out, uint64_t capacity);
 
 /*
+ * The schedule in the paper's path form (Sec. 4.3, BFS pathfinding: a path
+ * is an ordered list of (t, n) -- the chunk is sent from where it is to
+ * device n at time t -- and a condition's result maps each destination to
+ * its path).  Writes the path of `chunk` (caller's chunk id) from its
+ * source to `device`: entry i is sent at t_start[i] (ns) to next_device[i];
+ * the last entry is `device` itself, relays (switches, devices outside the
+ * group) appear as intermediate entries.  *length receives the number of
+ * hops; entries beyond `capacity` are not written (call again with a larger
+ * buffer).  For reduction ops the path is the one of the dual copy schedule
+ * (before reversal).  Output arrays are HOST memory.
+ * PCCL_ESTATE without a schedule, PCCL_EINVAL for a chunk or device out of
+ * range, a null output with capacity > 0, or a device that receives no
+ * copy of the chunk (its source included).
+ */
+pccl_status pccl_get_path(pccl_ctx *ctx, uint32_t chunk, uint32_t device, uint32_t *t_start,
+                          uint32_t *next_device, uint32_t capacity, uint32_t *length);
+
+/*
  * Statistics of the last synthesize call:
  *   events  -- distinct event times visited by the event loop (time 0 plus
  *              every transfer end up to the last transfer start),

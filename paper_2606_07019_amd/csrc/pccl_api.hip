@@ -64,6 +64,8 @@ struct pccl_ctx {
             if (e) (void)hipEventDestroy(e);
     }
     // results
+    std::unordered_map<uint64_t, uint64_t> receipt;  // (chunk << 32 | device) -> (link << 32 | t_start), copy schedule
+    bool have_receipts = false;
     uint64_t n_sends = 0, n_copy = 0;
     uint32_t coll_time = 0;
     Control ctl_host{};
@@ -772,6 +774,7 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     c->n_sends = c->op == PCCL_OP_ALLREDUCE ? 2 * n : n;
     c->coll_time = c->op == PCCL_OP_ALLREDUCE ? 2 * h.cstar : h.cstar;
     c->have_result = true;
+    c->have_receipts = false;
     if (n_sends) *n_sends = c->n_sends;
     if (collective_time_ns) *collective_time_ns = c->coll_time;
     return PCCL_OK;
@@ -789,6 +792,61 @@ pccl_status pccl_get_schedule(pccl_ctx *c, pccl_send *out, uint64_t capacity)
         if (!out) return fail(c, PCCL_EINVAL, "null output");
         HIP_OR_FAIL(c, hipMemcpyAsync(out, c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDefault, c->stream));
         HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+    }
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_get_path(pccl_ctx *c, uint32_t chunk, uint32_t device, uint32_t *t_start, uint32_t *next_device,
+                          uint32_t capacity, uint32_t *length)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (chunk >= c->C) return fail(c, PCCL_EINVAL, "chunk %u out of range (%u chunks)", chunk, c->C);
+    if (device >= c->D) return fail(c, PCCL_EINVAL, "device %u out of range (%u devices)", device, c->D);
+    if (capacity && (!t_start || !next_device)) return fail(c, PCCL_EINVAL, "null output");
+    if (!c->have_receipts) {
+        // which transfer delivered each (chunk, device), from the copy schedule
+        std::vector<pccl_send> s(c->n_sends);
+        if (c->n_sends) {
+            HIP_OR_FAIL(c, hipMemcpyAsync(s.data(), c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDeviceToHost,
+                                          c->stream));
+            HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+        }
+        const uint32_t cs = c->ctl_host.cstar;
+        c->receipt.clear();
+        c->receipt.reserve(c->n_copy * 2 + 1);
+        for (const pccl_send &x : s) {
+            uint32_t t = x.t_start_ns, l = x.link;
+            if (c->op == PCCL_OP_REDUCE_REVERSED) {
+                l = c->rev[x.link];
+                t = cs - x.t_start_ns - c->T[l];
+            } else if (c->op == PCCL_OP_ALLREDUCE) {
+                if (x.flags & PCCL_SEND_REDUCE) continue;
+                t -= cs;
+            }
+            c->receipt[((uint64_t)x.chunk << 32) | c->dst[l]] = ((uint64_t)l << 32) | t;
+        }
+        c->have_receipts = true;
+    }
+    // walk back from the device to the chunk's source
+    std::vector<std::pair<uint32_t, uint32_t>> hops;
+    uint32_t v = device;
+    for (;;) {
+        auto it = c->receipt.find(((uint64_t)chunk << 32) | v);
+        if (it == c->receipt.end()) break;
+        if (hops.size() >= c->D) return fail(c, PCCL_EINTERNAL, "delivery chain of chunk %u does not end", chunk);
+        const uint32_t l = (uint32_t)(it->second >> 32);
+        hops.emplace_back((uint32_t)it->second, v);
+        v = c->src[l];
+    }
+    if (hops.empty()) return fail(c, PCCL_EINVAL, "device %u receives no copy of chunk %u", device, chunk);
+    std::reverse(hops.begin(), hops.end());
+    if (length) *length = (uint32_t)hops.size();
+    for (uint32_t i = 0; i < hops.size() && i < capacity; i++) {
+        t_start[i] = hops[i].first;
+        next_device[i] = hops[i].second;
     }
     return PCCL_OK;
     GUARD_END(c)

@@ -61,6 +61,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "pccl_set_workspace": ([P, P, ctypes.c_size_t, U64, P], I),
         "pccl_synthesize": ([P, ctypes.POINTER(U64), ctypes.POINTER(U32)], I),
         "pccl_get_schedule": ([P, P, U64], I),
+        "pccl_get_path": ([P, U32, U32, P, P, U32, ctypes.POINTER(U32)], I),
         "pccl_get_stats": ([P, ctypes.POINTER(U64), ctypes.POINTER(U64), ctypes.POINTER(U64),
                             ctypes.POINTER(U64)], I),
         "pccl_get_setup": ([P, P, P, P, P], I),
@@ -153,6 +154,16 @@ def pccl_get_schedule(h, out_ptr: int, capacity: int) -> None:
     _check(h, load_library().pccl_get_schedule(h, out_ptr, capacity))
 
 
+def pccl_get_path(h, chunk: int, device: int) -> list:
+    """[(t_start_ns, next_device), ...] from the chunk's source to `device`."""
+    n = ctypes.c_uint32()
+    _check(h, load_library().pccl_get_path(h, chunk, device, None, None, 0, ctypes.byref(n)))
+    t = np.zeros(max(n.value, 1), np.uint32)
+    v = np.zeros(max(n.value, 1), np.uint32)
+    _check(h, load_library().pccl_get_path(h, chunk, device, _np_ptr(t), _np_ptr(v), n.value, ctypes.byref(n)))
+    return [(int(a), int(b)) for a, b in zip(t[:n.value], v[:n.value])]
+
+
 def pccl_get_stats(h) -> dict:
     v = [ctypes.c_uint64() for _ in range(4)]
     _check(h, load_library().pccl_get_stats(h, *[ctypes.byref(x) for x in v]))
@@ -232,6 +243,9 @@ class Synthesizer:
 
     def stats(self) -> dict:
         return pccl_get_stats(self.h)
+
+    def path(self, chunk: int, device: int) -> list:
+        return pccl_get_path(self.h, chunk, device)
 
     def profile(self) -> dict:
         return pccl_get_profile(self.h)
