@@ -594,11 +594,37 @@ def random_small(seed: int, n_npus=None, n_switches=None, max_chunks=40) -> Work
     return Workload(f"random_small_{seed}", topo, coll, rng.next())
 
 
-def random_switched(seed: int, max_chunks: int = 40) -> Workload:
-    """random_small with one to three switches and a random switch model
-    (buffer 0 = unlimited or 1-4 chunks, multicast or not)."""
+def mesh_switched(seed: int, w: int = 24, h: int = 24, n_switches: int = 3, fan: int = 8,
+                  n_chunks: int = 400, buffer: int = 2, unicast: bool = True) -> Workload:
+    """A w x h mesh of NPUs plus switches, each linked both ways to `fan`
+    random NPUs, with a switch model, and a random generic collective: many
+    single-device groups next to a few switch groups (more groups than the
+    matching kernel keeps resident, so workgroups own several)."""
+    rng = SplitMix64(seed ^ 0x3E5A5A17)
+    base = mesh2d(w, h)
+    n = w * h
+    pairs = list(zip(base.src.tolist(), base.dst.tolist()))
+    for k in range(n_switches):
+        for v in rng.shuffle(range(n))[:fan]:
+            pairs += [(n + k, v), (v, n + k)]
+    topo = with_switch_model(make_topology(n, n_switches, pairs, 500, 50), buffer, int(unicast))
+    src_of, dests_of = [], []
+    for c in range(n_chunks):
+        sv = rng.rand(n)
+        kd = 1 + rng.rand(8)
+        dests_of.append([v for v in rng.shuffle(range(n))[:kd + 1] if v != sv][:kd])
+        src_of.append(sv)
+    coll = collective_from_lists(n, n_chunks, 64 << 10, src_of, dests_of, [range(n)])
+    return Workload(f"mesh{w}x{h}_sw{n_switches}_seed{seed}", topo, coll, rng.next())
+
+
+def random_switched(seed: int, max_chunks: int = 40, n_npus=None, n_switches=None) -> Workload:
+    """random_small with one to three switches (or the given counts) and a
+    random switch model (buffer 0 = unlimited or 1-4 chunks, multicast or
+    not)."""
     rng = SplitMix64(seed ^ 0x5EED5A17C4)
-    wl = random_small(seed, n_switches=1 + rng.rand(3), max_chunks=max_chunks)
+    ns = n_switches if n_switches is not None else 1 + rng.rand(3)
+    wl = random_small(seed, n_npus=n_npus, n_switches=ns, max_chunks=max_chunks)
     S = wl.topo.n_switches
     buf = [0 if rng.rand(3) == 0 else 1 + rng.rand(4) for _ in range(S)]
     uni = [rng.rand(2) for _ in range(S)]

@@ -132,3 +132,18 @@ def test_full_size_buffered_rails_invariants():
     assert len(sched) == 745472
     check_copy_schedule(wl.topo, wl.coll, sched, ct)
     check_switch_model(wl.topo, wl.coll, sched)
+
+
+@pytest.mark.parametrize("seed", list(range(200, 216)))
+def test_medium_random_switched_parity(seed):
+    # 24-48 NPUs, 2-5 switches with random buffers / multicast, up to 300 chunks
+    wl = W.random_switched(seed, max_chunks=300, n_npus=24 + seed % 25, n_switches=2 + seed % 4)
+    _compare(wl, f"medium switched seed {seed}")
+
+
+@pytest.mark.parametrize("seed,buffer,unicast", [(0, 2, True), (1, 1, False), (2, 0, True), (3, 3, True)])
+def test_many_groups_parity(seed, buffer, unicast):
+    # a 24 x 24 mesh with 3 switches: ~550 switch groups, more than the
+    # workgroups the kernel can keep resident, so each workgroup owns
+    # several groups and their state leaves LDS between windows
+    _compare(W.mesh_switched(seed, buffer=buffer, unicast=unicast), "many groups")

@@ -149,3 +149,23 @@ def test_rail_cluster_invariants(buffer, unicast):
     assert r.status == 0, r.message
     check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
     check_switch_model(wl.topo, wl.coll, r.sends)
+
+
+@pytest.mark.parametrize("seed", range(200, 216))
+def test_medium_random_switched_invariants(seed):
+    wl = W.random_switched(seed, max_chunks=300, n_npus=24 + seed % 25, n_switches=2 + seed % 4)
+    r = O.run_workload(wl)
+    r0 = O.run_workload(wl, mode=O.MODE_PLAIN)
+    assert r.status == r0.status == 0, r.message
+    assert np.array_equal(r.sends, r0.sends)
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+    check_switch_model(wl.topo, wl.coll, r.sends)
+
+
+@pytest.mark.parametrize("seed,buffer,unicast", [(0, 2, True), (1, 1, False), (2, 0, True), (3, 3, True)])
+def test_mesh_switched_invariants(seed, buffer, unicast):
+    wl = W.mesh_switched(seed, buffer=buffer, unicast=unicast)
+    r = O.run_workload(wl)
+    assert r.status == 0, r.message
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+    check_switch_model(wl.topo, wl.coll, r.sends)
