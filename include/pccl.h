@@ -76,6 +76,22 @@ typedef struct {
 
 #define PCCL_SEND_REDUCE 1u
 
+/* One step of an exported program (pccl_export_program). */
+typedef struct {
+    uint32_t rank;       /* NPU that executes the step */
+    uint32_t tb;         /* thread block of that rank */
+    uint32_t op;         /* PCCL_STEP_SEND / PCCL_STEP_RECV / PCCL_STEP_RECV_REDUCE */
+    uint32_t peer;       /* the NPU at the other end of the transfer */
+    uint32_t chunk;      /* the caller's chunk id */
+    uint32_t t_start_ns; /* scheduled start of the transfer */
+    uint32_t dep_first;  /* this step waits for deps[dep_first .. dep_first + dep_count) (step indices) */
+    uint32_t dep_count;
+} pccl_step;
+
+#define PCCL_STEP_SEND 0u
+#define PCCL_STEP_RECV 1u
+#define PCCL_STEP_RECV_REDUCE 2u
+
 /*
  * Creates a context bound to HIP device `hip_device`.  `tie_seed` seeds the
  * tie-break among chunks of equal distance: chunks are ordered by distance
@@ -217,6 +233,29 @@ pccl_status pccl_get_schedule(pccl_ctx *ctx, pccl_send *out, uint64_t capacity);
  */
 pccl_status pccl_get_path(pccl_ctx *ctx, uint32_t chunk, uint32_t device, uint32_t *t_start,
                           uint32_t *next_device, uint32_t capacity, uint32_t *length);
+
+/*
+ * The schedule as a program for GPUs that execute it (the translation of
+ * synthesis results to MSCCL-style representations, Sec. 4.8): switches are
+ * folded away, so each transfer runs directly from NPU to NPU over the
+ * fabric (a chunk forwarded by a switch goes from the NPU that sent it into
+ * the switch to each NPU the switch sends it to; a partial sum sent into a
+ * switch goes to where the switch sends it on).  Rank r gets one thread
+ * block per peer it sends to and one per peer it receives from (send blocks
+ * by ascending peer first, then receive blocks); a block's steps are its
+ * transfers in (start time, chunk) order.  Each transfer is a SEND step on
+ * the sender and a RECV step (RECV_REDUCE for a reduction transfer) on the
+ * receiver.  A SEND of chunk c on rank r waits for every receive of c on r
+ * that ends before it starts (the chunk, or the partial sums of its
+ * reduction subtree, must be there).
+ * Steps are written ordered by (rank, tb, position in the block); `deps`
+ * holds step indices.  Output arrays are HOST memory.  *n_steps / *n_deps
+ * receive the sizes.  With steps and deps both NULL the call only sizes the
+ * buffers; with a buffer smaller than needed nothing is written
+ * (PCCL_EINVAL).  PCCL_ESTATE without a schedule.
+ */
+pccl_status pccl_export_program(pccl_ctx *ctx, pccl_step *steps, uint64_t step_capacity, uint32_t *deps,
+                                uint64_t dep_capacity, uint64_t *n_steps, uint64_t *n_deps);
 
 /*
  * Statistics of the last synthesize call:

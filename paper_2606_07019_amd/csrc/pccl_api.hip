@@ -852,6 +852,122 @@ pccl_status pccl_get_path(pccl_ctx *c, uint32_t chunk, uint32_t device, uint32_t
     GUARD_END(c)
 }
 
+pccl_status pccl_export_program(pccl_ctx *c, pccl_step *steps, uint64_t step_capacity, uint32_t *deps,
+                                uint64_t dep_capacity, uint64_t *n_steps, uint64_t *n_deps)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    std::vector<pccl_send> s(c->n_sends);
+    if (c->n_sends) {
+        HIP_OR_FAIL(c, hipMemcpyAsync(s.data(), c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDeviceToHost,
+                                      c->stream));
+        HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+    }
+    const uint32_t N = c->N;
+    auto key = [](uint32_t chunk, uint32_t dev, uint32_t phase) {
+        return ((uint64_t)phase << 63) | ((uint64_t)chunk << 32) | dev;
+    };
+    // a switch's copy came in over one transfer, and a partial sum leaves it
+    // over one transfer; the All-Reduce's two halves are told apart by the
+    // reduce flag
+    std::unordered_map<uint64_t, uint64_t> into_sw, from_sw;
+    for (uint64_t i = 0; i < s.size(); i++) {
+        const uint32_t l = s[i].link, red = s[i].flags & PCCL_SEND_REDUCE;
+        if (!red && c->dst[l] >= N) into_sw[key(s[i].chunk, c->dst[l], 0)] = i;
+        if (red && c->src[l] >= N) from_sw[key(s[i].chunk, c->src[l], 1)] = i;
+    }
+    // NPU-to-NPU transfers with the switches folded away
+    struct Xfer {
+        uint32_t from, to, chunk, t, end, red;
+    };
+    std::vector<Xfer> xs;
+    xs.reserve(s.size());
+    for (const pccl_send &x : s) {
+        const uint32_t l = x.link, red = x.flags & PCCL_SEND_REDUCE;
+        if (!red) {
+            if (c->dst[l] >= N) continue;  // carried on by the switch's out-transfers
+            uint32_t u = c->src[l];
+            for (uint32_t hop = 0; u >= N; hop++) {
+                auto it = into_sw.find(key(x.chunk, u, 0));
+                if (it == into_sw.end() || hop > c->D)
+                    return fail(c, PCCL_EINTERNAL, "switch %u forwards chunk %u it never received", u, x.chunk);
+                u = c->src[s[it->second].link];
+            }
+            xs.push_back({u, c->dst[l], x.chunk, x.t_start_ns, x.t_start_ns + c->T[l], 0u});
+        } else {
+            if (c->src[l] >= N) continue;  // folded into the transfers that fed the switch
+            uint32_t v = c->dst[l], end = x.t_start_ns + c->T[l];
+            for (uint32_t hop = 0; v >= N; hop++) {
+                auto it = from_sw.find(key(x.chunk, v, 1));
+                if (it == from_sw.end() || hop > c->D)
+                    return fail(c, PCCL_EINTERNAL, "switch %u reduces chunk %u but never sends it on", v, x.chunk);
+                const pccl_send &y = s[it->second];
+                v = c->dst[y.link];
+                end = y.t_start_ns + c->T[y.link];
+            }
+            xs.push_back({c->src[l], v, x.chunk, x.t_start_ns, end, 1u});
+        }
+    }
+    // thread blocks: per rank, send blocks by ascending peer, then receive blocks
+    std::vector<std::vector<uint32_t>> sendp(N), recvp(N);
+    for (const Xfer &x : xs) {
+        sendp[x.from].push_back(x.to);
+        recvp[x.to].push_back(x.from);
+    }
+    for (uint32_t r = 0; r < N; r++) {
+        for (auto *v : {&sendp[r], &recvp[r]}) {
+            std::sort(v->begin(), v->end());
+            v->erase(std::unique(v->begin(), v->end()), v->end());
+        }
+    }
+    auto tb_of = [&](uint32_t r, uint32_t peer, bool send) {
+        const auto &v = send ? sendp[r] : recvp[r];
+        const uint32_t k = (uint32_t)(std::lower_bound(v.begin(), v.end(), peer) - v.begin());
+        return send ? k : (uint32_t)sendp[r].size() + k;
+    };
+    struct Tmp {
+        uint32_t rank, tb, op, peer, chunk, t, end;
+    };
+    std::vector<Tmp> st;
+    st.reserve(2 * xs.size());
+    for (const Xfer &x : xs) {
+        st.push_back({x.from, tb_of(x.from, x.to, true), PCCL_STEP_SEND, x.to, x.chunk, x.t, x.end});
+        st.push_back({x.to, tb_of(x.to, x.from, false), x.red ? PCCL_STEP_RECV_REDUCE : PCCL_STEP_RECV, x.from,
+                      x.chunk, x.t, x.end});
+    }
+    std::sort(st.begin(), st.end(), [](const Tmp &a, const Tmp &b) {
+        if (a.rank != b.rank) return a.rank < b.rank;
+        if (a.tb != b.tb) return a.tb < b.tb;
+        if (a.t != b.t) return a.t < b.t;
+        return a.chunk < b.chunk;
+    });
+    // a send waits for the receives of its chunk on its rank that end before it starts
+    std::unordered_map<uint64_t, std::vector<std::pair<uint32_t, uint32_t>>> recvs;  // (chunk, rank) -> (end, step)
+    for (uint32_t i = 0; i < st.size(); i++)
+        if (st[i].op != PCCL_STEP_SEND) recvs[key(st[i].chunk, st[i].rank, 0)].push_back({st[i].end, i});
+    std::vector<uint32_t> dep_first(st.size(), 0), dep_count(st.size(), 0), dl;
+    for (uint32_t i = 0; i < st.size(); i++) {
+        dep_first[i] = (uint32_t)dl.size();
+        if (st[i].op != PCCL_STEP_SEND) continue;
+        auto it = recvs.find(key(st[i].chunk, st[i].rank, 0));
+        if (it == recvs.end()) continue;
+        for (const auto &e : it->second)
+            if (e.first <= st[i].t) dl.push_back(e.second);
+        dep_count[i] = (uint32_t)dl.size() - dep_first[i];
+    }
+    if (n_steps) *n_steps = st.size();
+    if (n_deps) *n_deps = dl.size();
+    if (!steps && !deps) return PCCL_OK;
+    if (!steps || !deps || step_capacity < st.size() || dep_capacity < dl.size())
+        return fail(c, PCCL_EINVAL, "program needs %zu steps and %zu dependencies", st.size(), dl.size());
+    for (uint32_t i = 0; i < st.size(); i++)
+        steps[i] = {st[i].rank, st[i].tb, st[i].op, st[i].peer, st[i].chunk, st[i].t, dep_first[i], dep_count[i]};
+    if (!dl.empty()) std::memcpy(deps, dl.data(), sizeof(uint32_t) * dl.size());
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
 pccl_status pccl_get_stats(pccl_ctx *c, uint64_t *events, uint64_t *rounds, uint64_t *clashes, uint64_t *windows)
 {
     if (!c) return PCCL_EINVAL;

@@ -62,6 +62,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "pccl_synthesize": ([P, ctypes.POINTER(U64), ctypes.POINTER(U32)], I),
         "pccl_get_schedule": ([P, P, U64], I),
         "pccl_get_path": ([P, U32, U32, P, P, U32, ctypes.POINTER(U32)], I),
+        "pccl_export_program": ([P, P, U64, P, U64, ctypes.POINTER(U64), ctypes.POINTER(U64)], I),
         "pccl_get_stats": ([P, ctypes.POINTER(U64), ctypes.POINTER(U64), ctypes.POINTER(U64),
                             ctypes.POINTER(U64)], I),
         "pccl_get_setup": ([P, P, P, P, P], I),
@@ -164,6 +165,19 @@ def pccl_get_path(h, chunk: int, device: int) -> list:
     return [(int(a), int(b)) for a, b in zip(t[:n.value], v[:n.value])]
 
 
+def pccl_export_program(h):
+    """(steps, deps): steps an (S, 8) uint32 array of rank, tb, op, peer,
+    chunk, t_start_ns, dep_first, dep_count; deps the step indices."""
+    ns, nd = ctypes.c_uint64(), ctypes.c_uint64()
+    lib = load_library()
+    _check(h, lib.pccl_export_program(h, None, 0, None, 0, ctypes.byref(ns), ctypes.byref(nd)))
+    steps = np.zeros((max(ns.value, 1), 8), np.uint32)
+    deps = np.zeros(max(nd.value, 1), np.uint32)
+    _check(h, lib.pccl_export_program(h, _np_ptr(steps), ns.value, _np_ptr(deps), nd.value,
+                                      ctypes.byref(ns), ctypes.byref(nd)))
+    return steps[:ns.value], deps[:nd.value]
+
+
 def pccl_get_stats(h) -> dict:
     v = [ctypes.c_uint64() for _ in range(4)]
     _check(h, load_library().pccl_get_stats(h, *[ctypes.byref(x) for x in v]))
@@ -246,6 +260,9 @@ class Synthesizer:
 
     def path(self, chunk: int, device: int) -> list:
         return pccl_get_path(self.h, chunk, device)
+
+    def program(self):
+        return pccl_export_program(self.h)
 
     def profile(self) -> dict:
         return pccl_get_profile(self.h)
