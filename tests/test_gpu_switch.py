@@ -147,3 +147,22 @@ def test_many_groups_parity(seed, buffer, unicast):
     # workgroups the kernel can keep resident, so each workgroup owns
     # several groups and their state leaves LDS between windows
     _compare(W.mesh_switched(seed, buffer=buffer, unicast=unicast), "many groups")
+
+
+@pytest.mark.parametrize("make", [lambda: W.switch2level_model(16, 8, 4, True, chunk_bytes=64 << 10),
+                                  lambda: W.mesh_switched(1, buffer=1, unicast=False)])
+def test_repeat_runs_identical(make):
+    # the schedule must not depend on workgroup timing (resident groups, and
+    # workgroups that own several groups)
+    from paper_2606_07019_amd.pccl import Synthesizer
+    wl = make()
+    print(f"[switch repeat] {wl.name}", flush=True)
+    s = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed)
+    try:
+        s.synthesize()
+        a = s.schedule()
+        for _ in range(3):
+            s.synthesize()
+            np.testing.assert_array_equal(s.schedule(), a)
+    finally:
+        s.close()
