@@ -14,7 +14,7 @@ constexpr uint64_t NONE64 = 0xFFFFFFFFFFFFFFFFull;
 constexpr uint32_t ROW_ALIGN_WORDS = 128;
 
 // Matching kernel envelope (checked on the host when a topology is loaded).
-constexpr uint32_t MATCH_THREADS = 512;   // at most 8 wavefronts per workgroup, one destination device each
+constexpr uint32_t MATCH_THREADS = 256;   // at most 4 wavefronts per workgroup (one per SIMD), one destination device each
 constexpr uint32_t MATCH_WAVES = MATCH_THREADS / 64;
 constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one device (one lane each)
 constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of their sources' in-degree

@@ -49,12 +49,13 @@ constexpr uint32_t K_NONE = 0, K_BUSY = 1, K_IDLE = 2;
 constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
 constexpr uint32_t SEG_STEPS = 3;    // lane-group probe steps before the whole wave helps
-constexpr uint32_t LA_WORDS = 8;     // words per row of one look-ahead step
+constexpr uint32_t LA_WORDS = 16;    // words per row of one look-ahead step
 constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose loads are in flight together
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
 constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
 constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
+constexpr uint32_t POLL_BATCH = 4;      // exchange slots one polling lane loads per batch (256 workgroups)
 
 static_assert(MAXIN == 64, "one lane per in-link");
 
@@ -158,8 +159,35 @@ __device__ inline uint32_t lane_prefix(uint64_t mask, uint32_t lane)
 }
 
 
-__device__ inline uint64_t u4lo(uint4 v) { return ((uint64_t)v.y << 32) | v.x; }
-__device__ inline uint64_t u4hi(uint4 v) { return ((uint64_t)v.w << 32) | v.z; }
+// 128-bit pieces of the two rows, handled as four 32-bit dwords (x holds the
+// lowest bits): wave64 VALU work is issued at one instruction per four
+// cycles, so the scans avoid 64-bit compares, selects and bit counts.
+__device__ inline uint4 and4(uint4 a, uint4 b) { return make_uint4(a.x & b.x, a.y & b.y, a.z & b.z, a.w & b.w); }
+
+// Keeps the bits of the 128-bit piece starting at bit `base` that lie at or
+// above bit `from`.
+__device__ inline uint4 keep_from(uint4 a, uint32_t base, uint32_t from)
+{
+    const uint32_t sh = from > base ? from - base : 0u;
+    const uint32_t q = sh >> 5, t = ~0u << (sh & 31u);
+    a.x &= q > 0u ? 0u : t;
+    a.y &= q > 1u ? 0u : (q == 1u ? t : ~0u);
+    a.z &= q > 2u ? 0u : (q == 2u ? t : ~0u);
+    a.w &= q > 3u ? 0u : (q == 3u ? t : ~0u);
+    return a;
+}
+
+// Offset of the lowest set bit of a 128-bit piece, NONE32 if it is zero.
+__device__ inline uint32_t first4(uint4 a)
+{
+    uint32_t r = a.w ? 96u + (uint32_t)__builtin_ctz(a.w) : NONE32;
+    r = a.z ? 64u + (uint32_t)__builtin_ctz(a.z) : r;
+    r = a.y ? 32u + (uint32_t)__builtin_ctz(a.y) : r;
+    r = a.x ? (uint32_t)__builtin_ctz(a.x) : r;
+    return r;
+}
+
+__device__ inline bool any4(uint4 a) { return (a.x | a.y | a.z | a.w) != 0u; }
 
 // Bitset intersect + select for one link, by a whole wave: the first set bit
 // at position >= cur of holds[src] & needs[dst], in priority order.  Each
@@ -171,38 +199,28 @@ __device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const u
                                          uint32_t cur, uint64_t Wp, uint64_t &words)
 {
     const uint32_t lane = threadIdx.x & 63;
-    const uint64_t w0 = cur >> 6;
-    if (w0 >= Wp) return NONE32;
-    const uint64_t keep0 = ~0ull << (cur & 63);
-    for (uint64_t wb = w0 & ~1ull; wb < Wp; wb += 128 * SWEEPS) {
-        uint64_t a[SWEEPS], b[SWEEPS];
+    const uint32_t w0 = cur >> 6, wp = (uint32_t)Wp;
+    if (w0 >= wp) return NONE32;
+    for (uint32_t wb = w0 & ~1u; wb < wp; wb += 128 * SWEEPS) {
+        uint4 a[SWEEPS];
 #pragma unroll
-        for (int u = 0; u < (int)SWEEPS; u++) {
-            const uint64_t idx = wb + 128 * u + 2 * lane;
-            uint64_t x = 0, y = 0;
-            if (idx < Wp) {
-                const uint4 hv = *reinterpret_cast<const uint4 *>(h + idx);
-                const uint4 nv = *reinterpret_cast<const uint4 *>(nd + idx);
-                x = u4lo(hv) & u4lo(nv);
-                y = u4hi(hv) & u4hi(nv);
-                if (idx < w0) x = 0;
-                else if (idx == w0) x &= keep0;
-                if (idx + 1 < w0) y = 0;
-                else if (idx + 1 == w0) y &= keep0;
-            }
-            a[u] = x;
-            b[u] = y;
+        for (uint32_t u = 0; u < SWEEPS; u++) {
+            const uint32_t idx = wb + 128 * u + 2 * lane;
+            a[u] = make_uint4(0, 0, 0, 0);
+            if (idx < wp)
+                a[u] = keep_from(and4(*reinterpret_cast<const uint4 *>(h + idx),
+                                      *reinterpret_cast<const uint4 *>(nd + idx)),
+                                 idx * 64, cur);
         }
 #pragma unroll
-        for (int u = 0; u < (int)SWEEPS; u++) {
-            const uint64_t m = __ballot((a[u] | b[u]) != 0ull);
+        for (uint32_t u = 0; u < SWEEPS; u++) {
+            const uint64_t m = __ballot(any4(a[u]));
             if (m) {
-                const int fl = __builtin_ffsll((long long)m) - 1;
-                const uint64_t x = readlane64(a[u], (uint32_t)fl), y = readlane64(b[u], (uint32_t)fl);
-                const uint64_t idx = wb + 128 * u + 2 * (uint64_t)fl;
-                words += (x ? idx : idx + 1) + 1 - w0;
-                return x ? (uint32_t)(idx * 64 + __builtin_ctzll(x))
-                         : (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
+                const uint32_t fl = (uint32_t)__builtin_ffsll((long long)m) - 1u;
+                const uint32_t r = readlane32(first4(a[u]), fl);
+                const uint32_t idx = wb + 128 * u + 2 * fl;
+                words += (uint64_t)(idx + (r >> 6) + 1 - w0);
+                return idx * 64 + r;
             }
         }
     }
@@ -272,16 +290,28 @@ __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint
             tn = NONE32;
             e = 0;
             s = 0;
-            for (uint32_t b = lane; b < nb; b += 64) {
-                const uint64_t a = __hip_atomic_load(&slot[(uint64_t)b * XSLOT_WORDS], __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-                if ((a & XTAG_MASK) != tag) all = false;
-                tn = min(tn, (uint32_t)a);
-                e |= (uint32_t)(a >> 51) & 1u;
-                s += (a >> 32) & 0x7FFFFull;
+            // every load of one spin is issued before any result is used, so
+            // a spin costs one memory round trip, not one per slot
+            const uint32_t ab = __hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (uint32_t b0 = 0; b0 < nb; b0 += 64 * POLL_BATCH) {
+                uint64_t a[POLL_BATCH];
+#pragma unroll
+                for (uint32_t u = 0; u < POLL_BATCH; u++) {
+                    const uint32_t b = b0 + 64 * u + lane;
+                    a[u] = b < nb ? __hip_atomic_load(&slot[(uint64_t)b * XSLOT_WORDS], __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                  : (tag | NONE32);
+                }
+#pragma unroll
+                for (uint32_t u = 0; u < POLL_BATCH; u++) {
+                    if ((a[u] & XTAG_MASK) != tag) all = false;
+                    tn = min(tn, (uint32_t)a[u]);
+                    e |= (uint32_t)(a[u] >> 51) & 1u;
+                    s += (a[u] >> 32) & 0x7FFFFull;
+                }
             }
             if (__ballot(!all) == 0) break;
-            if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+            if (ab) {
                 ok = 0;
                 break;
             }
@@ -443,21 +473,17 @@ __device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, 
     const bool pf = mine && la.cur != NONE32;
     if (!__ballot(pf)) return;
     uint32_t p = NONE32;
-    const uint64_t w0 = la.cur >> 6, pos = w0 & ~1ull;
+    const uint64_t pos = (la.cur >> 6) & ~1u;
     if (pf) {
-        const uint64_t keep0 = ~0ull << (la.cur & 63);
+        // the words were loaded from bit (cur & ~127): only the first piece
+        // holds bits below the cursor
+        const uint32_t base = la.cur & ~127u;
 #pragma unroll
-        for (uint32_t u = 0; u < LA_WORDS / 2; u++) {
-            const uint64_t idx = pos + 2 * u;
-            uint64_t x = u4lo(la.hv[u]) & u4lo(la.nv[u]), y = u4hi(la.hv[u]) & u4hi(la.nv[u]);
-            if (idx < w0) x = 0;
-            else if (idx == w0) x &= keep0;
-            if (idx + 1 < w0) y = 0;
-            else if (idx + 1 == w0) y &= keep0;
-            if (p == NONE32) {
-                if (x) p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
-                else if (y) p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
-            }
+        for (int u = (int)(LA_WORDS / 2) - 1; u >= 0; u--) {
+            uint4 a = and4(la.hv[u], la.nv[u]);
+            if (u == 0) a = keep_from(a, base, la.cur);
+            const uint32_t r = first4(a);
+            if (r != NONE32) p = base + 128u * (uint32_t)u + r;
         }
     }
     if (mine) ws.pick[lane] = pf ? p : NONE32;
@@ -662,11 +688,10 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             // whole wave, one link at a time.
             uint32_t p = NONE32, scanned = 0;
             bool scanning = false;
-            uint64_t pos = 0, w0 = 0, keep0 = 0;
+            uint64_t pos = 0, w0 = 0;
             if (mine && md == M_FULL) {
                 const uint32_t cur = ws.cur[lane];
                 w0 = cur >> 6;
-                keep0 = ~0ull << (cur & 63);
                 if (cur == ds.ready_c) {
                     // the look-ahead's candidate, still at the cursor and not
                     // delivered since: held by the source (holds only grow),
@@ -692,24 +717,17 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                         nv[u] = make_uint4(0, 0, 0, 0);
                     }
                 }
+                // pos = the even word below the cursor: only the first piece
+                // holds bits below it
+                const uint32_t cur = ws.cur[lane], base = (uint32_t)pos * 64u;
 #pragma unroll
-                for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
-                    const uint64_t idx = pos + 2 * u;
-                    uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
-                    if (idx < w0) x = 0;
-                    else if (idx == w0) x &= keep0;
-                    if (idx + 1 < w0) y = 0;
-                    else if (idx + 1 == w0) y &= keep0;
-                    if (p == NONE32) {
-                        if (x) {
-                            p = (uint32_t)(idx * 64 + __builtin_ctzll(x));
-                            scanned = (uint32_t)(idx + 1 - w0);
-                        } else if (y) {
-                            p = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
-                            scanned = (uint32_t)(idx + 2 - w0);
-                        }
-                    }
+                for (int u = (int)(PROBE_WORDS / 2) - 1; u >= 0; u--) {
+                    uint4 a = and4(hv[u], nv[u]);
+                    if (u == 0) a = keep_from(a, base, cur);
+                    const uint32_t r = first4(a);
+                    if (r != NONE32) p = base + 128u * (uint32_t)u + r;
                 }
+                if (p != NONE32) scanned = (p >> 6) + 1u - (uint32_t)w0;
                 if (p != NONE32) {
                     scanning = false;
                 } else {
@@ -735,13 +753,12 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint32_t g = lane >> (6u - lg), sub = lane & (G - 1u);
                 const bool act = g < ks;
                 uint32_t j = 0;
-                uint64_t gw0 = 0, gkeep0 = 0, gpos = 0, gstart = 0;
+                uint64_t gw0 = 0, gpos = 0, gstart = 0;
                 const uint64_t *hj = ly.holds;
                 if (act) {
                     j = ws.seg_j[g];
                     const uint32_t cj = ws.cur[j];
                     gw0 = cj >> 6;
-                    gkeep0 = ~0ull << (cj & 63);
                     gpos = gstart = ws.seg_pos[j];
                     hj = ly.holds + (uint64_t)ws.src[j] * Wp;
                 }
@@ -764,18 +781,11 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                                 nv[u] = make_uint4(0, 0, 0, 0);
                             }
                         }
+                        // group steps start past the per-lane probe, above the cursor
 #pragma unroll
-                        for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
-                            const uint64_t idx = base + 2 * u;
-                            uint64_t x = u4lo(hv[u]) & u4lo(nv[u]), y = u4hi(hv[u]) & u4hi(nv[u]);
-                            if (idx < gw0) x = 0;
-                            else if (idx == gw0) x &= gkeep0;
-                            if (idx + 1 < gw0) y = 0;
-                            else if (idx + 1 == gw0) y &= gkeep0;
-                            if (lp == NONE32) {
-                                if (x) lp = (uint32_t)(idx * 64 + __builtin_ctzll(x));
-                                else if (y) lp = (uint32_t)((idx + 1) * 64 + __builtin_ctzll(y));
-                            }
+                        for (int u = (int)(PROBE_WORDS / 2) - 1; u >= 0; u--) {
+                            const uint32_t r = first4(and4(hv[u], nv[u]));
+                            if (r != NONE32) lp = (uint32_t)base * 64u + 128u * (uint32_t)u + r;
                         }
                     }
                     for (uint32_t off = 1; off < G; off <<= 1) lp = min(lp, (uint32_t)__shfl_xor((int)lp, off));
