@@ -55,6 +55,7 @@ struct pccl_ctx {
     Layout ly{};
     Sizes sz{};
     int grid = 0, wpb = 0;  // matching kernel: workgroups, waves per workgroup
+    bool mirror = false;    // matching kernel keeps each destination's needs row in LDS
     // stage timing
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     float stage_ms[3] = {0.f, 0.f, 0.f};
@@ -663,9 +664,26 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     // units while many destinations do not make the window exchange poll
     // too many slots
     const uint32_t D1 = std::max<uint32_t>(c->D, 1);
-    const int wpb = (int)std::min<uint32_t>(MATCH_WAVES, std::max<uint32_t>(1, (D1 + MATCH_TARGET_GRID - 1) / MATCH_TARGET_GRID));
+    int wpb = (int)std::min<uint32_t>(MATCH_WAVES, std::max<uint32_t>(1, (D1 + MATCH_TARGET_GRID - 1) / MATCH_TARGET_GRID));
+    // needs rows in LDS: with as many of those waves as leave room for one
+    // row per wave and still give every destination a wave of its own
+    c->mirror = false;
+    int lds_cu = 0;
+    HIP_OR_FAIL(c, hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, c->device));
+    const size_t lds_static = match_static_lds(), row_bytes = (size_t)c->sz.Wp * sizeof(uint64_t);
+    for (int w = wpb; w >= 1 && lds_static > 0; w--) {
+        const size_t dyn = (size_t)w * row_bytes;
+        if (lds_static + dyn > (size_t)lds_cu) continue;
+        const int gmax = std::min<int>(match_max_grid(c->device, w, true, dyn), (int)MAX_MATCH_GRID);
+        if (gmax > 0 && (uint64_t)gmax * (uint64_t)w >= D1) {
+            wpb = w;
+            c->mirror = true;
+            break;
+        }
+    }
     c->wpb = wpb;
-    c->grid = std::min<int>(std::min<int>(match_max_grid(c->device, wpb), (int)MAX_MATCH_GRID),
+    const size_t dyn = c->mirror ? (size_t)wpb * row_bytes : 0;
+    c->grid = std::min<int>(std::min<int>(match_max_grid(c->device, wpb, c->mirror, dyn), (int)MAX_MATCH_GRID),
                             (int)((D1 + wpb - 1) / wpb));
     if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
     deal_destinations(c);
@@ -753,7 +771,7 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     if (c->sw_active)
         HIP_OR_FAIL(c, launch_match_sw(c->ly, c->sz, st, c->sw_grid));
     else
-        HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb));
+        HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb, c->mirror));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
     HIP_OR_FAIL(c, hipMemcpyAsync(&c->ctl_host, c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));

@@ -161,8 +161,11 @@ struct Sizes {
 // ---- launchers (each defined in the translation unit that holds its kernels)
 hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, const uint64_t *post,
                         const uint16_t *chunk_group, uint64_t seed, hipStream_t st);
-hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block);
-int match_max_grid(int device, int waves_per_block);
+// mirror: every wave keeps its destination's needs row in LDS (waves_per_block
+// rows of Wp words of dynamic shared memory); requires one destination per wave.
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror);
+int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds);
+size_t match_static_lds();  // static LDS bytes of the matching kernel
 hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
 int match_sw_max_grid(int device);
 hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st);

@@ -59,6 +59,12 @@ constexpr uint32_t POLL_BATCH = 4;      // exchange slots one polling lane loads
 
 static_assert(MAXIN == 64, "one lane per in-link");
 
+// Needs rows of the workgroup's destinations, one per wave, when they fit in
+// LDS (dynamic shared memory, sized at launch).  A destination's needs row
+// is read and written only by the wave that owns it, so the copy is exact;
+// the row in device memory is not updated while the kernel runs.
+extern __shared__ __attribute__((aligned(16))) uint64_t needs_lds[];
+
 // Per-wavefront scratch (one destination at a time).  When every wave owns
 // one destination for the whole run, the per-link part persists across
 // windows (no reload).
@@ -195,7 +201,7 @@ __device__ inline bool any4(uint4 a) { return (a.x | a.y | a.z | a.w) != 0u; }
 // per row per wave), a ballot finds the first lane with a non-zero AND, and
 // a count-trailing-zeros gives the chunk.  `words` counts the words per row the
 // scan needed (through the word holding the pick, or to the row end).
-__device__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
+__device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
                                          uint32_t cur, uint64_t Wp, uint64_t &words)
 {
     const uint32_t lane = threadIdx.x & 63;
@@ -440,9 +446,10 @@ struct LookAhead {
     uint32_t n_arr, n_unf;  // list lengths of the issuing window
 };
 
-__device__ inline void look_ahead_issue(const Layout &ly, uint64_t Wp, const WaveShared &ws, const Dest &ds,
-                                        const uint64_t *nd, bool mine, uint32_t n_arr, uint32_t n_unf,
-                                        LookAhead &la)
+template <bool MIRROR>
+__device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, const WaveShared &ws,
+                                                 const Dest &ds, const uint64_t *nd, bool mine, uint32_t n_arr,
+                                                 uint32_t n_unf, LookAhead &la)
 {
     const uint32_t lane = threadIdx.x & 63;
     la.cur = NONE32;
@@ -459,15 +466,17 @@ __device__ inline void look_ahead_issue(const Layout &ly, uint64_t Wp, const Wav
         const uint64_t idx = pos + 2 * u;
         if (idx < Wp) {
             la.hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
-            la.nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
+            if constexpr (!MIRROR) la.nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
         } else {
             la.hv[u] = make_uint4(0, 0, 0, 0);
-            la.nv[u] = make_uint4(0, 0, 0, 0);
+            if constexpr (!MIRROR) la.nv[u] = make_uint4(0, 0, 0, 0);
         }
     }
 }
 
-__device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, bool mine, LookAhead &la)
+template <bool MIRROR>
+__device__ __forceinline__ void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, const uint64_t *nd, bool mine,
+                                                  LookAhead &la)
 {
     const uint32_t lane = threadIdx.x & 63;
     const bool pf = mine && la.cur != NONE32;
@@ -478,6 +487,13 @@ __device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, 
         // the words were loaded from bit (cur & ~127): only the first piece
         // holds bits below the cursor
         const uint32_t base = la.cur & ~127u;
+        if constexpr (MIRROR) {
+            // the needs words come from the destination's row in LDS (no
+            // commit can have changed it since the holds words were loaded)
+#pragma unroll
+            for (uint32_t u = 0; u < LA_WORDS / 2; u++)
+                la.nv[u] = pos + 2 * u < Wp ? *reinterpret_cast<const uint4 *>(nd + pos + 2 * u) : make_uint4(0, 0, 0, 0);
+        }
 #pragma unroll
         for (int u = (int)(LA_WORDS / 2) - 1; u >= 0; u--) {
             uint4 a = and4(la.hv[u], la.nv[u]);
@@ -517,6 +533,7 @@ __device__ inline void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, 
 }
 
 // All events of window [t0, t1) for one destination, by one wavefront.
+template <bool MIRROR>
 __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws, Dest &ds, uint32_t k,
                                uint32_t t0, uint64_t t1, bool resident, Acc &acc, LookAhead &la)
 {
@@ -525,7 +542,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     if (n == 0) return;
     const uint64_t Wp = sz.Wp, L = sz.L;
     const uint32_t END = (uint32_t)(Wp * 64);
-    uint64_t *nd = ly.needs + (uint64_t)d * Wp;
+    uint64_t *nd;
+    if constexpr (MIRROR) nd = needs_lds + (uint64_t)(threadIdx.x >> 6) * Wp;
+    else nd = ly.needs + (uint64_t)d * Wp;
     uint64_t *hd = ly.holds + (uint64_t)d * Wp;
     const uint64_t *snap1 = ly.snap + (uint64_t)((k + 2) % 3) * L;  // in flight at the end of window k-1
     const uint64_t *snap2 = ly.snap + (uint64_t)((k + 1) % 3) * L;  // in flight at the end of window k-2 (unless carried)
@@ -533,7 +552,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     const bool mine = lane < n;
     const uint32_t sl = ds.base + lane;
     // the look-ahead issued at the end of the last window
-    if (resident) look_ahead_finish(Wp, ws, ds, mine, la);
+    if (resident) look_ahead_finish<MIRROR>(Wp, ws, ds, nd, mine, la);
 
     // fold the arrivals of window k-1 into d's holds row (a resident wave
     // remembers them; otherwise they are the snapshot entries that ended)
@@ -965,15 +984,18 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         t_prev = t;
     }
 
-    look_ahead_issue(ly, Wp, ws, ds, nd, mine, n_arr, n_unf, la);
+    look_ahead_issue<MIRROR>(ly, Wp, ws, ds, nd, mine, n_arr, n_unf, la);
     ds.n_arr_prev = n_arr;
-    if (!resident) look_ahead_finish(Wp, ws, ds, mine, la);
+    if (!resident) look_ahead_finish<MIRROR>(Wp, ws, ds, nd, mine, la);
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
     ds.log += n_send;
     acc.sent += n_send;
     wave_sync();
 }
 
+// MIRROR: every wave owns one destination for the whole run and keeps its
+// needs row in LDS (the host checks both).
+template <bool MIRROR>
 __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 {
     __shared__ BlockShared sh;
@@ -989,6 +1011,10 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const unsigned long long max_windows = ctl->needs_total + 2ull;
     // every wave owns at most one destination: its state stays on chip
     const bool resident = sz.D <= nwaves;
+    if (MIRROR && !resident) {
+        if (blockIdx.x == 0 && tid == 0) record_error(ctl, ST_EINTERNAL, 2, 0, 0);
+        return;
+    }
     WaveShared &ws = sh.w[wave];
     Dest ds{};
     for (uint32_t i = lane; i < CLASH_SLOTS; i += 64) {
@@ -998,6 +1024,15 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const uint32_t passes = (sz.D + nwaves - 1) / nwaves;
     const uint32_t mine_d = resident ? ly.wave_dest[gwave] : NONE32;
     if (mine_d != NONE32) load_dest(ly, ws, mine_d, ds);
+    if constexpr (MIRROR) {
+        if (mine_d != NONE32) {
+            uint64_t *row = needs_lds + (uint64_t)wave * sz.Wp;
+            const uint64_t *g = ly.needs + (uint64_t)mine_d * sz.Wp;
+            for (uint64_t i = 2 * lane; i < sz.Wp; i += 128)
+                *reinterpret_cast<uint4 *>(row + i) = *reinterpret_cast<const uint4 *>(g + i);
+        }
+        wave_sync();
+    }
     Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull};
     LookAhead la;
     la.cur = NONE32;
@@ -1010,13 +1045,13 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         acc.tmin = NONE32;
         const unsigned long long sent0 = acc.sent;
         if (resident) {
-            if (mine_d != NONE32) process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc, la);
-        } else {
+            if (mine_d != NONE32) process_window<MIRROR>(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc, la);
+        } else if constexpr (!MIRROR) {
             for (uint32_t r = 0; r < passes; r++) {
                 const uint32_t d = ly.wave_dest[(uint64_t)r * nwaves + gwave];
                 if (d == NONE32) continue;
                 load_dest(ly, ws, d, ds);
-                process_window(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc, la);
+                process_window<false>(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc, la);
                 store_dest(ly, ws, ds);
             }
         }
@@ -1063,23 +1098,45 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 
 }  // namespace
 
-int match_max_grid(int device, int waves_per_block)
+namespace {
+const void *match_kernel(bool mirror)
+{
+    return mirror ? reinterpret_cast<const void *>(k_match<true>) : reinterpret_cast<const void *>(k_match<false>);
+}
+}  // namespace
+
+size_t match_static_lds()
+{
+    hipFuncAttributes a{};
+    if (hipFuncGetAttributes(&a, match_kernel(true)) != hipSuccess) return 0;
+    return a.sharedSizeBytes;
+}
+
+int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds)
 {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_match, 64 * waves_per_block, 0) != hipSuccess)
+    const void *kern = match_kernel(mirror);
+    if (dyn_lds && hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds) != hipSuccess)
+        return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * waves_per_block, dyn_lds) != hipSuccess)
         return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return 0;
     return per_cu * cus;
 }
 
-hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block)
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror)
 {
     if (waves_per_block < 1 || waves_per_block > (int)NWAVES) return hipErrorInvalidValue;
+    const size_t dyn = mirror ? (size_t)waves_per_block * sz.Wp * sizeof(uint64_t) : 0;
+    const void *kern = match_kernel(mirror);
+    if (dyn) {
+        const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+        if (e != hipSuccess) return e;
+    }
     Layout l = ly;
     Sizes s = sz;
     void *args[] = {&l, &s};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_match), dim3(grid),
-                                      dim3(64 * waves_per_block), args, 0, st);
+    return hipLaunchCooperativeKernel(kern, dim3(grid), dim3(64 * waves_per_block), args, dyn, st);
 }
 
 }  // namespace pccl
