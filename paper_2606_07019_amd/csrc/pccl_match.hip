@@ -53,6 +53,7 @@ constexpr uint32_t LA_WORDS = 16;    // words per row of one look-ahead step
 constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose loads are in flight together
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
+constexpr uint32_t SWEEPS_LDS = 8;   // the same with the needs row in LDS (only holds words are loaded)
 constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
 constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
 constexpr uint32_t POLL_BATCH = 4;      // exchange slots one polling lane loads per batch (256 workgroups)
@@ -201,25 +202,48 @@ __device__ inline bool any4(uint4 a) { return (a.x | a.y | a.z | a.w) != 0u; }
 // per row per wave), a ballot finds the first lane with a non-zero AND, and
 // a count-trailing-zeros gives the chunk.  `words` counts the words per row the
 // scan needed (through the word holding the pick, or to the row end).
+//
+// With the needs row in LDS (MIRROR) only the holds words are loaded, and
+// twice as many sweeps are in flight per round trip.
+template <bool MIRROR>
 __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
-                                         uint32_t cur, uint64_t Wp, uint64_t &words)
+                                                         uint32_t cur, uint64_t Wp, uint64_t &words)
 {
+    constexpr uint32_t SW = MIRROR ? SWEEPS_LDS : SWEEPS;
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t w0 = cur >> 6, wp = (uint32_t)Wp;
     if (w0 >= wp) return NONE32;
-    for (uint32_t wb = w0 & ~1u; wb < wp; wb += 128 * SWEEPS) {
-        uint4 a[SWEEPS];
+    for (uint32_t wb = w0 & ~1u; wb < wp; wb += 128 * SW) {
+        uint4 a[SW];
+        if constexpr (MIRROR) {
+            // every load is issued before any is used (a load past the row
+            // end reads its last piece and is masked out)
+            uint4 hv[SW];
 #pragma unroll
-        for (uint32_t u = 0; u < SWEEPS; u++) {
-            const uint32_t idx = wb + 128 * u + 2 * lane;
-            a[u] = make_uint4(0, 0, 0, 0);
-            if (idx < wp)
-                a[u] = keep_from(and4(*reinterpret_cast<const uint4 *>(h + idx),
-                                      *reinterpret_cast<const uint4 *>(nd + idx)),
-                                 idx * 64, cur);
+            for (uint32_t u = 0; u < SW; u++) {
+                const uint32_t idx = wb + 128 * u + 2 * lane;
+                hv[u] = *reinterpret_cast<const uint4 *>(h + min(idx, wp - 2u));
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < SW; u++) {
+                const uint32_t idx = wb + 128 * u + 2 * lane;
+                a[u] = idx < wp ? and4(hv[u], *reinterpret_cast<const uint4 *>(nd + idx)) : make_uint4(0, 0, 0, 0);
+            }
+            // wb is the even word below the cursor: only the first sweep's
+            // piece in lane 0 holds bits below it
+            a[0] = keep_from(a[0], (wb + 2 * lane) * 64, cur);
+        } else {
+#pragma unroll
+            for (uint32_t u = 0; u < SW; u++) {
+                const uint32_t idx = wb + 128 * u + 2 * lane;
+                a[u] = make_uint4(0, 0, 0, 0);
+                if (idx < wp)
+                    a[u] = and4(*reinterpret_cast<const uint4 *>(h + idx), *reinterpret_cast<const uint4 *>(nd + idx));
+            }
+            a[0] = keep_from(a[0], (wb + 2 * lane) * 64, cur);
         }
 #pragma unroll
-        for (uint32_t u = 0; u < SWEEPS; u++) {
+        for (uint32_t u = 0; u < SW; u++) {
             const uint64_t m = __ballot(any4(a[u]));
             if (m) {
                 const uint32_t fl = (uint32_t)__builtin_ffsll((long long)m) - 1u;
@@ -842,7 +866,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint32_t sj = readlane32(ds.src, (uint32_t)j);
                 const uint32_t from = max((uint32_t)(readlane64(pos, (uint32_t)j) * 64), ws.cur[j]);
                 uint64_t w = 0;
-                const uint32_t pj = wave_first_candidate(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
+                const uint32_t pj = wave_first_candidate<MIRROR>(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
                 if ((int)lane == j) p = pj;
                 acc.words += w;
             }
