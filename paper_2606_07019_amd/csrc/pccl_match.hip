@@ -50,7 +50,6 @@ constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
 constexpr uint32_t SEG_STEPS = 3;    // lane-group probe steps before the whole wave helps
 constexpr uint32_t LA_WORDS = 16;    // words per row of one look-ahead step
-constexpr uint32_t PAIR_GROUP = 8;   // arrival-list entries per lane whose loads are in flight together
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
 constexpr uint32_t SWEEPS_LDS = 8;   // the same with the needs row in LDS (only holds words are loaded)
@@ -90,11 +89,6 @@ __device__ inline void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ inline bool need_bit(const uint64_t *nd, uint32_t c)
-{
-    return (nd[c >> 6] >> (c & 63)) & 1ull;
 }
 
 // Wave-wide reductions with DPP row operations (no LDS round trip): two quad
@@ -575,9 +569,6 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     uint64_t *snap0 = ly.snap + (uint64_t)(k % 3) * L;              // written for window k+1
     const bool mine = lane < n;
     const uint32_t sl = ds.base + lane;
-    // the look-ahead issued at the end of the last window
-    if (resident) look_ahead_finish<MIRROR>(Wp, ws, ds, nd, mine, la);
-
     // fold the arrivals of window k-1 into d's holds row (a resident wave
     // remembers them; otherwise they are the snapshot entries that ended)
     if (mine) {
@@ -602,6 +593,24 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                            ds.infl != NONE32 && (uint64_t)ds.busy >= t1 ? (((uint64_t)ds.infl << 32) | ds.busy) : NONE64,
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
+    // the snapshot entries of the arrival pairs (below) are loaded next, so
+    // that their round trip overlaps the look-ahead; the fold and the entry
+    // above go out first, so waiting for these loads waits for them too
+    const bool carry = resident && k >= 2;
+    uint64_t e1[PAIRS_PER_LANE], e2[PAIRS_PER_LANE];
+#pragma unroll
+    for (uint32_t u = 0; u < PAIRS_PER_LANE; u++) {
+        e1[u] = NONE64;
+        e2[u] = NONE64;
+        const uint32_t pr = ds.pair[u];
+        if (k >= 1 && pr != NONE32) {
+            e1[u] = snap1[pr >> 8];
+            if (k >= 2 && !carry) e2[u] = snap2[pr >> 8];
+        }
+    }
+    // the look-ahead issued at the end of the last window
+    if (resident) look_ahead_finish<MIRROR>(Wp, ws, ds, nd, mine, la);
+
     // arrivals at the sources of d's in-links that d needs: this window's
     // (snapshot k-1, ends in [t0, t1)) and last window's (snapshot k-2,
     // ends before t0; possibly not folded into the source's row yet).
@@ -610,7 +619,6 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     // flags of the chunks delivered since cleared, is exactly this window's
     // second list: it is carried over in LDS instead of reloaded.
     uint32_t n_arr = 0, n_unf = 0;
-    const bool carry = resident && k >= 2;
     if (carry) {
         for (uint32_t q0 = 0; q0 < ds.n_arr_prev; q0 += 64) {
             const uint32_t q = q0 + lane;
@@ -633,30 +641,27 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         wave_sync();
     }
     if (k >= 1) {
+        {
+            // the needs words of all entries are read before any is used (an
+            // empty entry reads chunk 0's word), so their latencies overlap
+            bool a_ok[PAIRS_PER_LANE], u_ok[PAIRS_PER_LANE];
+            uint64_t nw1[PAIRS_PER_LANE], nw2[PAIRS_PER_LANE];
 #pragma unroll
-        for (uint32_t g = 0; g < PAIRS_PER_LANE; g += PAIR_GROUP) {
-            if (64 * g >= ds.pairs) break;
-            uint64_t e1[PAIR_GROUP], e2[PAIR_GROUP];
-#pragma unroll
-            for (uint32_t u = 0; u < PAIR_GROUP; u++) {
-                e1[u] = NONE64;
-                e2[u] = NONE64;
-                const uint32_t pr = ds.pair[g + u];
-                if (pr != NONE32) {
-                    e1[u] = snap1[pr >> 8];
-                    if (k >= 2 && !carry) e2[u] = snap2[pr >> 8];
-                }
-            }
-            bool a_ok[PAIR_GROUP], u_ok[PAIR_GROUP];
-#pragma unroll
-            for (uint32_t u = 0; u < PAIR_GROUP; u++) {
-                a_ok[u] = e1[u] != NONE64 && (uint64_t)(uint32_t)e1[u] < t1 && need_bit(nd, (uint32_t)(e1[u] >> 32));
-                u_ok[u] = e2[u] != NONE64 && (uint32_t)e2[u] < t0 && need_bit(nd, (uint32_t)(e2[u] >> 32));
+            for (uint32_t u = 0; u < PAIRS_PER_LANE; u++) {
+                nw1[u] = nd[(e1[u] != NONE64 ? (uint32_t)(e1[u] >> 32) : 0u) >> 6];
+                if (!carry) nw2[u] = nd[(e2[u] != NONE64 ? (uint32_t)(e2[u] >> 32) : 0u) >> 6];
             }
 #pragma unroll
-            for (uint32_t u = 0; u < PAIR_GROUP; u++) {
+            for (uint32_t u = 0; u < PAIRS_PER_LANE; u++) {
+                const uint32_t c1 = (uint32_t)(e1[u] >> 32), c2 = (uint32_t)(e2[u] >> 32);
+                a_ok[u] = e1[u] != NONE64 && (uint64_t)(uint32_t)e1[u] < t1 && ((nw1[u] >> (c1 & 63)) & 1ull);
+                u_ok[u] = !carry && e2[u] != NONE64 && (uint32_t)e2[u] < t0 && ((nw2[u] >> (c2 & 63)) & 1ull);
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < PAIRS_PER_LANE; u++) {
+                if (64 * u >= ds.pairs) break;
                 const uint64_t ma = __ballot(a_ok[u]), mu = __ballot(u_ok[u]);
-                const uint8_t j = (uint8_t)(ds.pair[g + u] & 0xFFu);
+                const uint8_t j = (uint8_t)(ds.pair[u] & 0xFFu);
                 if (a_ok[u]) {
                     const uint32_t q = n_arr + lane_prefix(ma, lane);
                     ws.arr_end[q] = (uint32_t)e1[u];
