@@ -305,78 +305,7 @@ __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
     const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFu) << 52;
     uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
-    if (threadIdx.x < 64 && nb <= 64 * POLL_BATCH) {
-        // two batches of loads in flight: one batch is checked while the
-        // next is already on its way, so the last slot written is seen about
-        // half a round trip sooner than with one spin at a time
-        uint32_t spins = 0, ok = 1;
-        uint32_t tn = NONE32, e = 0;
-        unsigned long long s = 0;
-        uint64_t a[POLL_BATCH], b[POLL_BATCH];
-        uint32_t ab_a = 0, ab_b = 0;
-        // the loads are unconditional (lanes past the last workgroup reread
-        // its slot and are ignored): a load under a branch would make the
-        // compiler wait for it where the branches join
-        auto issue = [&](uint64_t (&v)[POLL_BATCH], uint32_t &ab) {
-            ab = __hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-            for (uint32_t u = 0; u < POLL_BATCH; u++)
-                v[u] = __hip_atomic_load(&slot[(uint64_t)min(64 * u + lane, nb - 1u) * XSLOT_WORDS], __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT);
-        };
-        // true when every slot carries the tag (tn, e, s then hold the reduction)
-        auto check = [&](const uint64_t (&v)[POLL_BATCH]) {
-            bool all = true;
-            tn = NONE32;
-            e = 0;
-            s = 0;
-#pragma unroll
-            for (uint32_t u = 0; u < POLL_BATCH; u++) {
-                if (64 * u + lane >= nb) continue;
-                if ((v[u] & XTAG_MASK) != tag) all = false;
-                tn = min(tn, (uint32_t)v[u]);
-                e |= (uint32_t)(v[u] >> 51) & 1u;
-                s += (v[u] >> 32) & 0x7FFFFull;
-            }
-            return __ballot(!all) == 0;
-        };
-        auto give_up = [&](uint32_t ab) {
-            if (ab) return true;
-            if (++spins > SPIN_LIMIT) {
-                if (lane == 0) atomicExch(&ctl->abort, 1u);
-                return true;
-            }
-            return false;
-        };
-        issue(a, ab_a);
-        while (true) {
-            issue(b, ab_b);
-            if (check(a)) break;
-            if (give_up(ab_a)) {
-                ok = 0;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-            issue(a, ab_a);
-            if (check(b)) break;
-            if (give_up(ab_b)) {
-                ok = 0;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-        // acquire: this compute unit's caches drop lines other workgroups wrote
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        tn = wave_min(tn);
-        e = __ballot(e != 0) ? 1u : 0u;
-        s = wave_sum64(s);
-        if (lane == 0) {
-            sh.ex.tn = tn;
-            sh.ex.err = e;
-            sh.ex.sent = s;
-            sh.ex.ok = ok;
-        }
-    } else if (threadIdx.x < 64) {
+    if (threadIdx.x < 64) {
         uint32_t spins = 0, ok = 1;
         uint32_t tn = NONE32, e = 0;
         unsigned long long s = 0;
@@ -386,19 +315,20 @@ __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint
             e = 0;
             s = 0;
             // every load of one spin is issued before any result is used, so
-            // a spin costs one memory round trip, not one per slot
+            // a spin costs one memory round trip, not one per slot.  The loads
+            // are unconditional (lanes past the last workgroup reread its slot
+            // and are ignored): a load under a branch would make the compiler
+            // wait for it where the branches join.
             const uint32_t ab = __hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             for (uint32_t b0 = 0; b0 < nb; b0 += 64 * POLL_BATCH) {
                 uint64_t a[POLL_BATCH];
 #pragma unroll
-                for (uint32_t u = 0; u < POLL_BATCH; u++) {
-                    const uint32_t b = b0 + 64 * u + lane;
-                    a[u] = b < nb ? __hip_atomic_load(&slot[(uint64_t)b * XSLOT_WORDS], __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT)
-                                  : (tag | NONE32);
-                }
+                for (uint32_t u = 0; u < POLL_BATCH; u++)
+                    a[u] = __hip_atomic_load(&slot[(uint64_t)min(b0 + 64 * u + lane, nb - 1u) * XSLOT_WORDS],
+                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
                 for (uint32_t u = 0; u < POLL_BATCH; u++) {
+                    if (b0 + 64 * u + lane >= nb) continue;
                     if ((a[u] & XTAG_MASK) != tag) all = false;
                     tn = min(tn, (uint32_t)a[u]);
                     e |= (uint32_t)(a[u] >> 51) & 1u;
@@ -1057,12 +987,23 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             if (ds.ready_c != NONE32 && ws.dlv_round[(ds.ready_c * 2654435761u) >> 22] == (uint16_t)acc.rounds)
                 ds.ready_c = NONE32;
             // the delivered chunks are no longer needed: clear their flags
-            for (uint64_t wm = (n_arr | n_unf) ? wins : 0ull; wm; wm &= wm - 1) {
-                const uint32_t c = ws.pick[__builtin_ffsll((long long)wm) - 1];
-                for (uint32_t q = lane; q < n_arr; q += 64)
-                    if (ws.arr_c[q] == c) ws.arr_need[q] = 0;
-                for (uint32_t q = lane; q < n_unf; q += 64)
-                    if (ws.unf_c[q] == c) ws.unf_need[q] = 0;
+            // (each entry is compared with the winners' picks, read from
+            // their lanes)
+            if ((n_arr | n_unf) && wins) {
+                for (uint32_t q = lane; q < n_arr; q += 64) {
+                    const uint32_t c = ws.arr_c[q];
+                    bool hit = false;
+                    for (uint64_t wm = wins; wm; wm &= wm - 1)
+                        hit |= readlane32(pk, (uint32_t)__builtin_ffsll((long long)wm) - 1u) == c;
+                    if (hit) ws.arr_need[q] = 0;
+                }
+                for (uint32_t q = lane; q < n_unf; q += 64) {
+                    const uint32_t c = ws.unf_c[q];
+                    bool hit = false;
+                    for (uint64_t wm = wins; wm; wm &= wm - 1)
+                        hit |= readlane32(pk, (uint32_t)__builtin_ffsll((long long)wm) - 1u) == c;
+                    if (hit) ws.unf_need[q] = 0;
+                }
             }
             wave_sync();
             // a link that won an arrival keeps the other arrivals as its cursor
