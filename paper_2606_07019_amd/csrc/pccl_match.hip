@@ -463,6 +463,7 @@ struct LookAhead {
     uint4 hv[LA_WORDS / 2], nv[LA_WORDS / 2];  // the two rows' words from the even word below the cursor
     uint32_t cur;           // cursor the words were loaded from, NONE32 if none
     uint32_t n_arr, n_unf;  // list lengths of the issuing window
+    unsigned long long words;  // word positions this lane's look-aheads passed (summed at the end)
 };
 
 template <bool MIRROR>
@@ -539,12 +540,15 @@ __device__ __forceinline__ void look_ahead_finish(uint64_t Wp, WaveShared &ws, D
         const uint64_t end_w = pos + LA_WORDS;
         const uint32_t probed = end_w >= Wp ? (uint32_t)(Wp * 64) : (uint32_t)(end_w * 64);
         const uint32_t pk = ws.pick[lane];
+        const uint64_t w0 = la.cur >> 6;
         if (pk < probed) {
             ws.cur[lane] = pk;
             ds.ready = 1;
             ds.ready_c = pk;
+            la.words += (pk >> 6) + 1 - w0;
         } else {
             ws.cur[lane] = probed;
+            la.words += min(end_w, Wp) - w0;
         }
     }
     la.cur = NONE32;
@@ -1081,6 +1085,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     LookAhead la;
     la.cur = NONE32;
     la.n_arr = la.n_unf = 0;
+    la.words = 0;
     unsigned long long remaining = ctl->needs_total;
     uint32_t t0 = 0;
     unsigned long long k = 0;
@@ -1132,6 +1137,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         ctl->windows = k + 1;
         ctl->n_log = ctl->needs_total - remaining;
     }
+    acc.words += wave_sum64(la.words);
     if (lane == 0) {
         atomicMax(&ctl->cstar, acc.cstar);
         if (acc.clashes) atomicAdd(&ctl->clashes, acc.clashes);
