@@ -144,16 +144,21 @@ __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tm
             tn = NONE32;
             e = 0;
             s = 0;
-            for (uint32_t b = lane; b < nb; b += 64) {
-                const uint64_t a = __hip_atomic_load(&slot[(uint64_t)b * XSLOT_WORDS], __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
+            // the abort flag and the slots are loaded together, one round trip
+            // per spin (lanes past the last workgroup reread its slot and are
+            // ignored, so no load sits under a branch)
+            const uint32_t ab = __hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (uint32_t b0 = 0; b0 < nb; b0 += 64) {
+                const uint64_t a = __hip_atomic_load(&slot[(uint64_t)min(b0 + lane, nb - 1u) * XSLOT_WORDS],
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (b0 + lane >= nb) continue;
                 if ((a & STAG_MASK) != tag) all = false;
                 tn = min(tn, (uint32_t)a);
                 e |= (uint32_t)(a >> 51) & 1u;
                 s += (a >> 32) & 0x7FFFFull;
             }
             if (__ballot(!all) == 0) break;
-            if (__hip_atomic_load(&ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+            if (ab) {
                 ok = 0;
                 break;
             }
@@ -290,12 +295,19 @@ __device__ uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, u
         uint32_t row = NONE32, first = NONE32;
         bool done = false;
         for (uint64_t w0 = cu >> 6; w0 < wend && !done; w0 += SCAN_STEP) {
+            // all loads of a step are issued before any is used: a load past
+            // the range rereads its last word and is masked out (a load under
+            // a branch would make the compiler wait for it where the branches
+            // join)
             uint64_t x[SCAN_STEP];
 #pragma unroll
             for (uint32_t k = 0; k < SCAN_STEP; k++) {
-                const uint64_t w = w0 + k;
-                x[k] = w < wend ? hs[w] & nd[w] : 0ull;
+                const uint64_t w = min<uint64_t>(w0 + k, wend - 1);
+                x[k] = hs[w] & nd[w];
             }
+#pragma unroll
+            for (uint32_t k = 1; k < SCAN_STEP; k++)
+                if (w0 + k >= wend) x[k] = 0ull;
             x[0] &= NONE64 << (w0 == (cu >> 6) ? (cu & 63u) : 0u);
             words += min<uint64_t>(SCAN_STEP, wend - w0);
 #pragma unroll
@@ -317,12 +329,19 @@ __device__ uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, u
         }
         sh.cur[i] = first == NONE32 ? max(cu, hi) : first;
         uint32_t best = row, from = 0, slot = 0;
-        // earlier arrivals kept below the cursor
+        // earlier arrivals kept below the cursor (their needs words loaded
+        // together, word 0 for an empty entry)
+        uint64_t pw[PEND];
+#pragma unroll
+        for (uint32_t e = 0; e < PEND; e++) {
+            const uint32_t c = sh.pend[i][e];
+            pw[e] = nd[(c == NONE32 ? 0u : c) >> 6];
+        }
 #pragma unroll
         for (uint32_t e = 0; e < PEND; e++) {
             const uint32_t c = sh.pend[i][e];
             if (c == NONE32 || c >= best) continue;
-            if (!((nd[c >> 6] >> (c & 63u)) & 1ull)) {
+            if (!((pw[e] >> (c & 63u)) & 1ull)) {
                 sh.pend[i][e] = NONE32;
                 continue;
             }
@@ -368,12 +387,22 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     if (!resident || first_window) load_group_state(ly, sz, gp, sh);
     // arrivals at the group's sources inside the window, from the entries
     // published at t0 (the source's in-links, pair p of source j)
-    for (uint32_t p = tid; p < gp.nP; p += ST) {
-        const uint64_t e = ly.snap[ly.sw.p_slot[gp.pbase + p]];
-        const uint32_t b = (uint32_t)e;
-        const bool in = e != NONE64 && b >= t0 && (uint64_t)b < t1;
-        sh.arr_t[p] = in ? b : NONE32;
-        sh.arr_c[p] = (uint32_t)(e >> 32);
+    // (four pairs per thread in flight: slot indices, then the entries)
+    for (uint32_t p0 = tid; p0 < gp.nP; p0 += 4u * ST) {
+        uint32_t sl[4];
+        uint64_t e[4];
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++) sl[k] = ly.sw.p_slot[gp.pbase + min(p0 + k * ST, gp.nP - 1u)];
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++) e[k] = ly.snap[sl[k]];
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++) {
+            const uint32_t p = p0 + k * ST, b = (uint32_t)e[k];
+            if (p >= gp.nP) continue;
+            const bool in = e[k] != NONE64 && b >= t0 && (uint64_t)b < t1;
+            sh.arr_t[p] = in ? b : NONE32;
+            sh.arr_c[p] = (uint32_t)(e[k] >> 32);
+        }
     }
     for (uint32_t i = tid; i < gp.nL; i += ST) sh.amask[i] = 0ull;
     __syncthreads();
@@ -393,8 +422,13 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             c[k] = v[k] ? sh.arr_c[p] : 0u;
             row[k] = ly.needs + (uint64_t)(v[k] ? sh.ldst[i] : 0u) * sz.Wp;
         }
+        // unconditional loads (row 0, word 0 for an empty item), so that all
+        // four are in flight together
+        uint64_t nw[4];
 #pragma unroll
-        for (uint32_t k = 0; k < 4; k++) v[k] = v[k] && ((row[k][c[k] >> 6] >> (c[k] & 63u)) & 1ull);
+        for (uint32_t k = 0; k < 4; k++) nw[k] = row[k][c[k] >> 6];
+#pragma unroll
+        for (uint32_t k = 0; k < 4; k++) v[k] = v[k] && ((nw[k] >> (c[k] & 63u)) & 1ull);
 #pragma unroll
         for (uint32_t k = 0; k < 4; k++)
             if (v[k]) {
