@@ -75,10 +75,27 @@ def test_random_medium_parity(seed):
 
 def test_more_destinations_than_waves_parity():
     """A 50 x 44 mesh (2200 devices): more destinations than the matching
-    kernel has wavefronts on one MI355X (256 workgroups of 8), so waves
-    take several destinations per window and keep their state in memory."""
+    kernel has wavefronts on one MI355X (at most 256 workgroups of 4), so
+    waves take several destinations per window and keep their state in
+    memory."""
     topo = W.mesh2d(50, 44)
     rng = W.SplitMix64(7)
     members = sorted(rng.shuffle(range(2200))[:16])
     coll = W.all_gather(2200, members, 4, 1 << 16)
     _compare(W.Workload("mesh50x44_allgather16", topo, coll, 11), "non-resident mesh")
+
+
+def test_needs_rows_in_device_memory_parity():
+    """524,288 chunks on a 300-NPU ring: a needs row is 8,192 words (64 KiB),
+    so next to the matching kernel's static LDS one row fits per workgroup,
+    and 300 destinations do not fit in 256 one-wave workgroups.  The kernel
+    then keeps every wave on one destination but reads the needs rows from
+    device memory (the path without LDS copies).  Only the first 600 chunks
+    have a destination (the next NPU on the ring), so the oracle stays
+    quick; the others have a holder and no destination."""
+    n, C = 300, 1 << 19
+    topo = W.ring(n)
+    src = [c % n for c in range(C)]
+    dests = [[(c + 1) % n] if c < 600 else [] for c in range(C)]
+    coll = W.collective_from_lists(n, C, 1 << 12, src, dests, [range(n)])
+    _compare(W.Workload("ring300_c524288_sparse", topo, coll, 5), "needs rows in device memory")
