@@ -55,6 +55,7 @@ constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in 
 constexpr uint32_t SWEEPS_LDS = 8;   // the same with the needs row in LDS (only holds words are loaded)
 constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
 constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
+constexpr uint32_t FEW_PICKS = 8;       // up to this many picking links compare picks lane to lane
 constexpr uint32_t POLL_BATCH = 4;      // exchange slots one polling lane loads per batch (256 workgroups)
 
 static_assert(MAXIN == 64, "one lane per in-link");
@@ -69,7 +70,7 @@ extern __shared__ __attribute__((aligned(16))) uint64_t needs_lds[];
 // one destination for the whole run, the per-link part persists across
 // windows (no reload).
 struct alignas(16) WaveShared {
-    uint32_t src[MAXIN], srcoff[MAXIN], tim[MAXIN], link[MAXIN];
+    uint32_t src[MAXIN], srcoff[MAXIN], tim[MAXIN];
     uint32_t cur[MAXIN], pick[MAXIN], mode[MAXIN], kind[MAXIN];
     uint32_t cum[MAXIN + 1];
     uint32_t arr_end[PAIRS], arr_c[PAIRS];
@@ -375,7 +376,7 @@ struct Acc {
 // One wavefront's destination: uniform values and this lane's in-link.
 struct Dest {
     uint32_t d, base, n, pairs;
-    uint32_t src, tim;          // this lane's in-link (lane < n)
+    uint32_t src, tim, lid;     // this lane's in-link (lane < n): source, time, link id
     uint32_t busy, infl, idle;  // its state
     uint32_t ready;             // the cursor points at a candidate found ahead of time
     uint32_t ready_c;           // that candidate while it is valid (NONE32 when not kept)
@@ -397,6 +398,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
     ds.log = ly.dest_log[d];
     ds.src = 0;
     ds.tim = 0;
+    ds.lid = 0;
     ds.busy = 0;
     ds.infl = NONE32;
     ds.idle = 0;
@@ -415,7 +417,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
         ws.src[lane] = ds.src;
         ws.srcoff[lane] = ly.in_off[ds.src];
         ws.tim[lane] = ds.tim;
-        ws.link[lane] = ly.slot_link[sl];
+        ds.lid = ly.slot_link[sl];
         ws.cur[lane] = ly.cur[sl];
         ws.cum[lane] = ly.slot_cum[sl];
     }
@@ -911,34 +913,45 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             const bool act = mine && md != M_IDLE;
             if (!__ballot(act)) break;
             // clash resolution among d's in-links: fastest link, then lowest id.
-            // Picks are hashed into a table of lane ids; a lane alone in its
-            // slot has no rival and wins.  Lanes sharing a slot are grouped by
-            // equal pick, and each group keeps its smallest (time, link id).
-            if (mine) ws.pick[lane] = act ? pk : NONE32;
+            // With few picking links every pick is compared with every other
+            // one, read from its lane.  Otherwise picks are hashed into a
+            // table of lane ids; a lane alone in its slot has no rival and
+            // wins; lanes sharing a slot are grouped by equal pick, and each
+            // group keeps its smallest (time, link id).
+            const uint64_t actm = __ballot(act);
+            const bool few = __popcll(actm) <= FEW_PICKS;
+            const uint64_t key = act ? (((uint64_t)ds.tim << 32) | ds.lid) : NONE64;
             const uint32_t hs = act ? (pk * 2654435761u) >> 22 : 0u;
-            if (act) ws.clash_lane[hs] = (uint8_t)lane;
-            wave_sync();
-            bool rival = false;
-            if (act && ws.clash_lane[hs] != lane) {
-                rival = true;
-                ws.clash_hit[hs] = 1;
-            }
-            wave_sync();
-            if (act && ws.clash_hit[hs]) rival = true;
-            bool win = act && !rival;
-            uint64_t contested = __ballot(rival);
-            if (contested) {
+            bool win = act;
+            if (few) {
+                for (uint64_t m = actm; m; m &= m - 1) {
+                    const uint32_t j = (uint32_t)__builtin_ffsll((long long)m) - 1u;
+                    if (readlane32(pk, j) == pk && readlane64(key, j) < key) win = false;
+                }
+            } else {
+                if (act) ws.clash_lane[hs] = (uint8_t)lane;
                 wave_sync();
-                if (rival) ws.clash_hit[hs] = 0;
-                const uint64_t key = act ? (((uint64_t)ds.tim << 32) | ws.link[lane]) : NONE64;
-                while (contested) {
-                    const int j = __builtin_ffsll((long long)contested) - 1;
-                    const uint32_t v = readlane32(pk, (uint32_t)j);
-                    const uint64_t g = __ballot(act && pk == v);
-                    const bool in_g = (g >> lane) & 1ull;
-                    const uint64_t kmin = wave_min64(in_g ? key : NONE64);
-                    if (in_g) win = key == kmin;
-                    contested &= ~g;
+                bool rival = false;
+                if (act && ws.clash_lane[hs] != lane) {
+                    rival = true;
+                    ws.clash_hit[hs] = 1;
+                }
+                wave_sync();
+                if (act && ws.clash_hit[hs]) rival = true;
+                win = act && !rival;
+                uint64_t contested = __ballot(rival);
+                if (contested) {
+                    wave_sync();
+                    if (rival) ws.clash_hit[hs] = 0;
+                    while (contested) {
+                        const int j = __builtin_ffsll((long long)contested) - 1;
+                        const uint32_t v = readlane32(pk, (uint32_t)j);
+                        const uint64_t g = __ballot(act && pk == v);
+                        const bool in_g = (g >> lane) & 1ull;
+                        const uint64_t kmin = wave_min64(in_g ? key : NONE64);
+                        if (in_g) win = key == kmin;
+                        contested &= ~g;
+                    }
                 }
             }
             const uint64_t wins = __ballot(win);
@@ -963,7 +976,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     __hip_atomic_store(&snap0[sl], ((uint64_t)pk << 32) | e32, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
                     const unsigned long long q = ds.log + n_send + lane_prefix(wins, lane);
-                    ly.skey[0][q] = ((uint64_t)t << 32) | ws.link[lane];
+                    ly.skey[0][q] = ((uint64_t)t << 32) | ds.lid;
                     ly.sval[0][q] = pk;
                     if (md == M_FULL) {
                         ws.cur[lane] = pk + 1;
@@ -983,13 +996,21 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             if (__ballot(overflow)) acc.err = 1;
             wave_sync();
             // a candidate found ahead of time is gone once its chunk is
-            // delivered: winners stamp their chunk's hash slot with the round,
-            // and a stamped slot drops the candidate (a hash collision only
-            // drops one that is still valid, which costs a scan)
-            if (win) ws.dlv_round[hs] = (uint16_t)acc.rounds;
-            wave_sync();
-            if (ds.ready_c != NONE32 && ws.dlv_round[(ds.ready_c * 2654435761u) >> 22] == (uint16_t)acc.rounds)
-                ds.ready_c = NONE32;
+            // delivered.  With few picks it is compared with the winners'
+            // picks; otherwise winners stamp their chunk's hash slot with the
+            // round, and a stamped slot drops the candidate (a hash collision
+            // only drops one that is still valid, which costs a scan)
+            if (few) {
+                bool gone = false;
+                for (uint64_t m = wins; m; m &= m - 1)
+                    gone |= readlane32(pk, (uint32_t)__builtin_ffsll((long long)m) - 1u) == ds.ready_c;
+                if (gone) ds.ready_c = NONE32;
+            } else {
+                if (win) ws.dlv_round[hs] = (uint16_t)acc.rounds;
+                wave_sync();
+                if (ds.ready_c != NONE32 && ws.dlv_round[(ds.ready_c * 2654435761u) >> 22] == (uint16_t)acc.rounds)
+                    ds.ready_c = NONE32;
+            }
             // the delivered chunks are no longer needed: clear their flags
             // (each entry is compared with the winners' picks, read from
             // their lanes)
