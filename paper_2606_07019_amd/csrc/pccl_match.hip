@@ -140,7 +140,6 @@ struct OpAdd64 { __device__ uint64_t operator()(uint64_t a, uint64_t b) const { 
 
 __device__ inline uint32_t wave_min(uint32_t v) { return dpp_reduce(v, NONE32, OpMin()); }
 __device__ inline uint32_t wave_max(uint32_t v) { return dpp_reduce(v, 0u, OpMax()); }
-__device__ inline uint32_t wave_sum(uint32_t v) { return dpp_reduce(v, 0u, OpAdd()); }
 __device__ inline unsigned long long wave_sum64(unsigned long long v) { return dpp_reduce64(v, 0ull, OpAdd64()); }
 __device__ inline uint64_t wave_min64(uint64_t v) { return dpp_reduce64(v, NONE64, OpMin64()); }
 
@@ -371,6 +370,9 @@ struct Acc {
     uint32_t cstar;    // latest transfer end committed by this wave
     uint32_t err;      // this wave recorded an error
     unsigned long long sent, rounds, clashes, words;
+    // per-lane parts, reduced once at the end of the kernel
+    unsigned long long lane_words;  // word positions this lane's scans passed
+    uint32_t lane_cstar;            // latest end of a transfer this lane committed
 };
 
 // One wavefront's destination: uniform values and this lane's in-link.
@@ -869,7 +871,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     pos = sp;
                 }
             }
-            acc.words += wave_sum(scanned);
+            acc.lane_words += scanned;
             uint64_t cmask = __ballot(scanning);
             while (cmask) {
                 // continue after the probed words (from the cursor when none were probed)
@@ -992,7 +994,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             }
             n_send += (uint32_t)__popcll(wins);
             acc.clashes += (unsigned long long)__popcll(losers);
-            acc.cstar = max(acc.cstar, wave_max(ce));
+            acc.lane_cstar = max(acc.lane_cstar, ce);
             if (__ballot(overflow)) acc.err = 1;
             wave_sync();
             // a candidate found ahead of time is gone once its chunk is
@@ -1102,7 +1104,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         wave_sync();
     }
-    Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull};
+    Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull, 0ull, 0u};
     LookAhead la;
     la.cur = NONE32;
     la.n_arr = la.n_unf = 0;
@@ -1158,7 +1160,8 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         ctl->windows = k + 1;
         ctl->n_log = ctl->needs_total - remaining;
     }
-    acc.words += wave_sum64(la.words);
+    acc.words += wave_sum64(acc.lane_words + la.words);
+    acc.cstar = max(acc.cstar, wave_max(acc.lane_cstar));
     if (lane == 0) {
         atomicMax(&ctl->cstar, acc.cstar);
         if (acc.clashes) atomicAdd(&ctl->clashes, acc.clashes);
