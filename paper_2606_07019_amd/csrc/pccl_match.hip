@@ -201,11 +201,11 @@ __device__ inline bool any4(uint4 a) { return (a.x | a.y | a.z | a.w) != 0u; }
 // twice as many sweeps are in flight per round trip.
 template <bool MIRROR>
 __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
-                                                         uint32_t cur, uint64_t Wp, uint64_t &words)
+                                                         uint32_t cur, uint64_t Ws, uint64_t &words)
 {
     constexpr uint32_t SW = MIRROR ? SWEEPS_LDS : SWEEPS;
     const uint32_t lane = threadIdx.x & 63;
-    const uint32_t w0 = cur >> 6, wp = (uint32_t)Wp;
+    const uint32_t w0 = cur >> 6, wp = (uint32_t)Ws;
     if (w0 >= wp) return NONE32;
     for (uint32_t wb = w0 & ~1u; wb < wp; wb += 128 * SW) {
         uint4 a[SW];
@@ -248,7 +248,7 @@ __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restr
             }
         }
     }
-    words += Wp - w0;
+    words += Ws - w0;
     return NONE32;
 }
 
@@ -471,7 +471,7 @@ struct LookAhead {
 };
 
 template <bool MIRROR>
-__device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, const WaveShared &ws,
+__device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, uint64_t Ws, const WaveShared &ws,
                                                  const Dest &ds, const uint64_t *nd, bool mine, uint32_t n_arr,
                                                  uint32_t n_unf, LookAhead &la)
 {
@@ -481,14 +481,14 @@ __device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, 
     la.n_unf = n_unf;
     if (!(mine && ds.infl != NONE32 && !ds.ready)) return;
     const uint32_t cur = ws.cur[lane];
-    if ((cur >> 6) >= Wp) return;
+    if ((cur >> 6) >= Ws) return;
     la.cur = cur;
     const uint64_t pos = (cur >> 6) & ~1u;
     const uint64_t *h = ly.holds + (uint64_t)ds.src * Wp;
 #pragma unroll
     for (uint32_t u = 0; u < LA_WORDS / 2; u++) {
         const uint64_t idx = pos + 2 * u;
-        if (idx < Wp) {
+        if (idx < Ws) {
             la.hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
             if constexpr (!MIRROR) la.nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
         } else {
@@ -499,7 +499,7 @@ __device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, 
 }
 
 template <bool MIRROR>
-__device__ __forceinline__ void look_ahead_finish(uint64_t Wp, WaveShared &ws, Dest &ds, const uint64_t *nd, bool mine,
+__device__ __forceinline__ void look_ahead_finish(uint64_t Ws, WaveShared &ws, Dest &ds, const uint64_t *nd, bool mine,
                                                   LookAhead &la)
 {
     const uint32_t lane = threadIdx.x & 63;
@@ -516,7 +516,7 @@ __device__ __forceinline__ void look_ahead_finish(uint64_t Wp, WaveShared &ws, D
             // commit can have changed it since the holds words were loaded)
 #pragma unroll
             for (uint32_t u = 0; u < LA_WORDS / 2; u++)
-                la.nv[u] = pos + 2 * u < Wp ? *reinterpret_cast<const uint4 *>(nd + pos + 2 * u) : make_uint4(0, 0, 0, 0);
+                la.nv[u] = pos + 2 * u < Ws ? *reinterpret_cast<const uint4 *>(nd + pos + 2 * u) : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
         for (int u = (int)(LA_WORDS / 2) - 1; u >= 0; u--) {
@@ -542,7 +542,7 @@ __device__ __forceinline__ void look_ahead_finish(uint64_t Wp, WaveShared &ws, D
         // only the probed words are known empty: a listed arrival beyond
         // them does not let the cursor skip unprobed words
         const uint64_t end_w = pos + LA_WORDS;
-        const uint32_t probed = end_w >= Wp ? (uint32_t)(Wp * 64) : (uint32_t)(end_w * 64);
+        const uint32_t probed = end_w >= Ws ? (uint32_t)(Ws * 64) : (uint32_t)(end_w * 64);
         const uint32_t pk = ws.pick[lane];
         const uint64_t w0 = la.cur >> 6;
         if (pk < probed) {
@@ -552,7 +552,7 @@ __device__ __forceinline__ void look_ahead_finish(uint64_t Wp, WaveShared &ws, D
             la.words += (pk >> 6) + 1 - w0;
         } else {
             ws.cur[lane] = probed;
-            la.words += min(end_w, Wp) - w0;
+            la.words += min(end_w, Ws) - w0;
         }
     }
     la.cur = NONE32;
@@ -567,8 +567,10 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t n = ds.n, d = ds.d;
     if (n == 0) return;
-    const uint64_t Wp = sz.Wp, L = sz.L;
-    const uint32_t END = (uint32_t)(Wp * 64);
+    // Wp: row stride; Ws: where scans end (bits past the last chunk are zero
+    // in both rows, so no candidate lies beyond the row's own words)
+    const uint64_t Wp = sz.Wp, Ws = (sz.W + 1) & ~1ull, L = sz.L;
+    const uint32_t END = (uint32_t)(Ws * 64);
     uint64_t *nd;
     if constexpr (MIRROR) nd = needs_lds + (uint64_t)(threadIdx.x >> 6) * Wp;
     else nd = ly.needs + (uint64_t)d * Wp;
@@ -618,7 +620,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         }
     }
     // the look-ahead issued at the end of the last window
-    if (resident) look_ahead_finish<MIRROR>(Wp, ws, ds, nd, mine, la);
+    if (resident) look_ahead_finish<MIRROR>(Ws, ws, ds, nd, mine, la);
 
     // arrivals at the sources of d's in-links that d needs: this window's
     // (snapshot k-1, ends in [t0, t1)) and last window's (snapshot k-2,
@@ -756,7 +758,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     p = cur;
                     scanned = 1;
                 } else {
-                    scanning = w0 < Wp;
+                    scanning = w0 < Ws;
                     pos = w0 & ~1ull;
                 }
             }
@@ -766,7 +768,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
 #pragma unroll
                 for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
                     const uint64_t idx = pos + 2 * u;
-                    if (idx < Wp) {
+                    if (idx < Ws) {
                         hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
                         nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
                     } else {
@@ -789,9 +791,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     scanning = false;
                 } else {
                     pos += PROBE_WORDS;
-                    if (pos >= Wp) {
+                    if (pos >= Ws) {
                         scanning = false;
-                        scanned = (uint32_t)(Wp - w0);
+                        scanned = (uint32_t)(Ws - w0);
                     }
                 }
             }
@@ -830,7 +832,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
 #pragma unroll
                         for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
                             const uint64_t idx = base + 2 * u;
-                            if (idx < Wp) {
+                            if (idx < Ws) {
                                 hv[u] = *reinterpret_cast<const uint4 *>(hj + idx);
                                 nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
                             } else {
@@ -852,7 +854,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                             live = false;
                         } else {
                             gpos += (uint64_t)G * PROBE_WORDS;
-                            if (gpos >= Wp) live = false;
+                            if (gpos >= Ws) live = false;
                         }
                     }
                 }
@@ -860,7 +862,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     // word positions these steps passed: through the pick's word, or the probed range
                     ws.seg_p[j] = gp;
                     ws.seg_pos[j] = live ? (uint32_t)gpos : NONE32;
-                    ws.pick[j] = (uint32_t)((gp != NONE32 ? (uint64_t)(gp >> 6) + 1 : min(gpos, Wp)) - max(gstart, gw0));
+                    ws.pick[j] = (uint32_t)((gp != NONE32 ? (uint64_t)(gp >> 6) + 1 : min(gpos, Ws)) - max(gstart, gw0));
                 }
                 wave_sync();
                 if (scanning) {
@@ -880,7 +882,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint32_t sj = readlane32(ds.src, (uint32_t)j);
                 const uint32_t from = max((uint32_t)(readlane64(pos, (uint32_t)j) * 64), ws.cur[j]);
                 uint64_t w = 0;
-                const uint32_t pj = wave_first_candidate<MIRROR>(ly.holds + (uint64_t)sj * Wp, nd, from, Wp, w);
+                const uint32_t pj = wave_first_candidate<MIRROR>(ly.holds + (uint64_t)sj * Wp, nd, from, Ws, w);
                 if ((int)lane == j) p = pj;
                 acc.words += w;
             }
@@ -1055,9 +1057,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         t_prev = t;
     }
 
-    look_ahead_issue<MIRROR>(ly, Wp, ws, ds, nd, mine, n_arr, n_unf, la);
+    look_ahead_issue<MIRROR>(ly, Wp, Ws, ws, ds, nd, mine, n_arr, n_unf, la);
     ds.n_arr_prev = n_arr;
-    if (!resident) look_ahead_finish<MIRROR>(Wp, ws, ds, nd, mine, la);
+    if (!resident) look_ahead_finish<MIRROR>(Ws, ws, ds, nd, mine, la);
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
     ds.log += n_send;
     acc.sent += n_send;
