@@ -42,7 +42,10 @@ __device__ inline uint64_t tail_mask(uint64_t k, const Sizes &sz)
 // Conditions (Sec. 4.1): for every set bit of the NPU-centric bitmaps,
 // count precondition holders per chunk, mark chunks that are needed
 // somewhere, and check that pre/post bits sit on members of the chunk's
-// process group.  Grid: x over words, y over NPU rows.
+// process group.  Grid: x over words, y over NPU rows.  The per-bit updates
+// are atomics whose results are not used (a second holder is found by
+// k_chunk_check), so a word's updates are in flight together; with a single
+// process group the membership of the row is checked once per word.
 __global__ void k_conditions(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t *post,
                              const uint16_t *cg)
 {
@@ -53,23 +56,26 @@ __global__ void k_conditions(Layout ly, Sizes sz, const uint64_t *pre, const uin
     if (!(p | q)) return;
     const uint64_t tm = tail_mask(k, sz);
     if ((p | q) & ~tm) record_error(ly.ctl, ST_EINVAL, sz.C, v, BAD_TAIL);
-    for (uint64_t x = (p | q) & tm; x; x &= x - 1) {
-        const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
-        const uint32_t g = cg ? cg[c] : 0u;
-        if (g >= sz.G) {
-            record_error(ly.ctl, ST_EINVAL, c, v, BAD_GROUP);
-            continue;
+    const uint64_t bits = (p | q) & tm;
+    if (!cg) {
+        if (bits && !((ly.group_masks[v >> 6] >> (v & 63)) & 1ull))
+            record_error(ly.ctl, ST_EINVAL, (uint32_t)(k * 64 + __builtin_ctzll(bits)), v, BAD_MEMBER);
+    } else {
+        for (uint64_t x = bits; x; x &= x - 1) {
+            const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
+            const uint32_t g = cg[c];
+            if (g >= sz.G) {
+                record_error(ly.ctl, ST_EINVAL, c, v, BAD_GROUP);
+                continue;
+            }
+            if (!((ly.group_masks[(uint64_t)g * sz.WN + (v >> 6)] >> (v & 63)) & 1ull))
+                record_error(ly.ctl, ST_EINVAL, c, v, BAD_MEMBER);
         }
-        if (!((ly.group_masks[(uint64_t)g * sz.WN + (v >> 6)] >> (v & 63)) & 1ull))
-            record_error(ly.ctl, ST_EINVAL, c, v, BAD_MEMBER);
     }
     for (uint64_t x = p & tm; x; x &= x - 1) {
         const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
-        const uint32_t old = atomicAdd(&ly.holder_cnt[c], 1u);
-        if (old & CNT_MASK)
-            record_error(ly.ctl, ST_EINVAL, c, v, TWO_HOLDERS);
-        else
-            ly.chunk_src[c] = v;
+        atomicAdd(&ly.holder_cnt[c], 1u);
+        ly.chunk_src[c] = v;  // the one holder (several are an error, reported below)
     }
     for (uint64_t x = q & tm; x; x &= x - 1) {
         const uint32_t c = (uint32_t)(k * 64 + __builtin_ctzll(x));
@@ -83,6 +89,7 @@ __global__ void k_chunk_check(Layout ly, Sizes sz)
     if (c >= sz.C) return;
     const uint32_t h = ly.holder_cnt[c];
     if ((h & FLAG_POST) && !(h & CNT_MASK)) record_error(ly.ctl, ST_EINVAL, (uint32_t)c, 0, NO_HOLDER);
+    if ((h & CNT_MASK) > 1u) record_error(ly.ctl, ST_EINVAL, (uint32_t)c, ly.chunk_src[c], TWO_HOLDERS);
     if ((h & CNT_MASK) == 1u) ly.src_index[ly.chunk_src[c]] = 1u;
 }
 

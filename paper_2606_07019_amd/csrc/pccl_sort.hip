@@ -5,7 +5,11 @@
 namespace pccl {
 namespace {
 
+constexpr uint32_t SORT_PER = SORT_TILE / SORT_THREADS;  // elements of a tile per thread
+
 // Per-tile digit histogram, stored tile-major: hist[tile * 256 + digit].
+// A thread's keys are loaded together (indices past n reread the last key
+// and are not counted), so the tile costs one memory round trip.
 __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles)
 {
     __shared__ uint32_t cnt[256];
@@ -14,45 +18,61 @@ __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, in
     __syncthreads();
     const uint64_t *key = ly.skey[ly.ctl->sort_cur];
     const uint64_t base = (uint64_t)tile * SORT_TILE;
-    for (uint32_t e = tid; e < SORT_TILE; e += SORT_THREADS) {
-        uint64_t i = base + e;
-        if (i < n) atomicAdd(&cnt[(key[i] >> shift) & 255u], 1u);
-    }
+    uint32_t dg[SORT_PER];
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++)
+        dg[u] = (uint32_t)(key[min(base + u * SORT_THREADS + tid, n - 1)] >> shift) & 255u;
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++)
+        if (base + u * SORT_THREADS + tid < n) atomicAdd(&cnt[dg[u]], 1u);
     __syncthreads();
     ly.hist[(uint64_t)tile * 256 + tid] = cnt[tid];
 }
 
-// Exclusive scan of the histogram (one workgroup, one thread per digit),
-// in (digit, tile) order, and the skip decision: a pass whose digit is the
-// same for every element is a no-op.
-__global__ void __launch_bounds__(256) k_scan(Layout ly, uint64_t n, uint32_t tiles)
+// Exclusive scan of the histogram (one workgroup), in (digit, tile) order,
+// and the skip decision: a pass whose digit is the same for every element
+// is a no-op.  Four threads per digit each take a quarter of the tiles, so
+// a thread has few dependent loads to wait for.
+constexpr uint32_t SCAN_SPLIT = 4;
+
+__global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n, uint32_t tiles)
 {
-    __shared__ uint32_t part[256];
+    __shared__ uint32_t part[SCAN_SPLIT][256];
+    __shared__ uint32_t pre[256];
     __shared__ uint32_t skip;
-    const uint32_t d = threadIdx.x;
+    const uint32_t d = threadIdx.x & 255u, q = threadIdx.x >> 8;
+    const uint32_t per = (tiles + SCAN_SPLIT - 1) / SCAN_SPLIT;
+    const uint32_t t0 = min(q * per, tiles), t1 = min(t0 + per, tiles);
     uint32_t tot = 0;
-#pragma unroll 8
-    for (uint32_t t = 0; t < tiles; t++) tot += ly.hist[(uint64_t)t * 256 + d];
-    part[d] = tot;
-    if (d == 0) skip = 0;
+#pragma unroll 16
+    for (uint32_t t = t0; t < t1; t++) tot += ly.hist[(uint64_t)t * 256 + d];
+    part[q][d] = tot;
+    if (threadIdx.x == 0) skip = 0;
     __syncthreads();
-    if (tot == (uint32_t)n) skip = 1;
+    uint32_t all = 0;
+    for (uint32_t r = 0; r < SCAN_SPLIT; r++) all += part[r][d];
+    if (q == 0) {
+        pre[d] = all;
+        if (all == (uint32_t)n) skip = 1;
+    }
+    __syncthreads();
     for (uint32_t off = 1; off < 256; off <<= 1) {
-        const uint32_t v = d >= off ? part[d - off] : 0;
+        const uint32_t v = (q == 0 && d >= off) ? pre[d - off] : 0u;
         __syncthreads();
-        part[d] += v;
+        if (q == 0) pre[d] += v;
         __syncthreads();
     }
-    uint32_t run = part[d] - tot;
-#pragma unroll 8
-    for (uint32_t t = 0; t < tiles; t++) {
-        const uint64_t i = (uint64_t)t * 256 + d;
-        const uint32_t v = ly.hist[i];
-        ly.hist[i] = run;
+    uint32_t run = pre[d] - all;  // exclusive prefix over digits
+    for (uint32_t r = 0; r < q; r++) run += part[r][d];
+#pragma unroll 16
+    for (uint32_t t = t0; t < t1; t++) {
+        const uint64_t x = (uint64_t)t * 256 + d;
+        const uint32_t v = ly.hist[x];
+        ly.hist[x] = run;
         run += v;
     }
     __syncthreads();
-    if (d == 0) {
+    if (threadIdx.x == 0) {
         const uint32_t cur = ly.ctl->sort_cur;
         ly.ctl->sort_src = cur;
         ly.ctl->sort_skip = skip;
@@ -79,16 +99,24 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
     __syncthreads();
     const uint64_t base = (uint64_t)tile * SORT_TILE;
     const uint64_t lt = (1ull << lane) - 1ull;
-    for (uint32_t e0 = 0; e0 < SORT_TILE; e0 += SORT_THREADS) {
+    // the tile's keys and values are loaded together (indices past n reread
+    // the last element and are not written), one memory round trip
+    uint64_t kk[SORT_PER];
+    uint32_t vv[SORT_PER];
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++) {
+        const uint64_t i = min(base + u * SORT_THREADS + tid, n - 1);
+        kk[u] = kin[i];
+        vv[u] = vin[i];
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++) {
+        const uint32_t e0 = u * SORT_THREADS;
+        if (base + e0 >= n) continue;  // uniform: the rest of the tile is past n
         const uint64_t i = base + e0 + tid;
         const bool valid = i < n;
-        uint64_t k = 0;
-        uint32_t v = 0, dg = 0;
-        if (valid) {
-            k = kin[i];
-            v = vin[i];
-            dg = (uint32_t)(k >> shift) & 255u;
-        }
+        const uint64_t k = kk[u];
+        const uint32_t v = vv[u], dg = valid ? (uint32_t)(k >> shift) & 255u : 0u;
         uint64_t same = __ballot(valid);
         for (int b = 0; b < 8; b++) {
             const bool bit = (dg >> b) & 1u;
@@ -113,7 +141,6 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
         }
         run[tid] += add;
         __syncthreads();
-        if (base + e0 + SORT_THREADS >= n) break;
     }
 }
 
@@ -163,7 +190,7 @@ hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_
     if (tiles > max_tiles) return hipErrorInvalidValue;
     for (int b = byte_lo; b < byte_hi; b++) {
         k_hist<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
-        k_scan<<<1, 256, 0, st>>>(ly, n, tiles);
+        k_scan<<<1, 256 * SCAN_SPLIT, 0, st>>>(ly, n, tiles);
         k_scatter<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
     }
     return hipGetLastError();
