@@ -80,27 +80,26 @@ __global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n
     }
 }
 
-// Stable scatter: a tile is consumed in order, 256 elements at a time; the
-// rank of an element among equal digits of its wave comes from 8 ballots
-// (one per digit bit), the offset of its wave from LDS counts.
+// Stable scatter of one tile.  Element e = 256 u + tid of the tile is step u
+// of its thread.  Every wave ranks its elements among equal digits of the
+// same step with 8 ballots (one per digit bit) and records, per step and
+// digit, how many it holds; after one barrier a thread per digit turns the
+// counts, in (step, wave) order, into destination offsets; after a second
+// barrier every element is written to offset + rank.  A thread's 16 keys
+// and values are loaded together (indices past n reread the last element
+// and are not written).
 __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n, int shift, uint32_t tiles)
 {
     if (ly.ctl->sort_skip) return;
-    __shared__ uint32_t run[256];
-    __shared__ uint32_t wc[SORT_THREADS / 64][256];
+    constexpr uint32_t NW = SORT_THREADS / 64;
+    __shared__ uint32_t off[SORT_PER][NW][256];  // counts, then offsets, per (step, wave, digit)
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, tile = blockIdx.x;
     const uint32_t src = ly.ctl->sort_src;
     const uint64_t *kin = ly.skey[src];
     const uint32_t *vin = ly.sval[src];
     uint64_t *kout = ly.skey[src ^ 1u];
     uint32_t *vout = ly.sval[src ^ 1u];
-    run[tid] = ly.hist[(uint64_t)tile * 256 + tid];
-    for (uint32_t w = 0; w < SORT_THREADS / 64; w++) wc[w][tid] = 0;
-    __syncthreads();
     const uint64_t base = (uint64_t)tile * SORT_TILE;
-    const uint64_t lt = (1ull << lane) - 1ull;
-    // the tile's keys and values are loaded together (indices past n reread
-    // the last element and are not written), one memory round trip
     uint64_t kk[SORT_PER];
     uint32_t vv[SORT_PER];
 #pragma unroll
@@ -109,14 +108,17 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
         kk[u] = kin[i];
         vv[u] = vin[i];
     }
+    const uint32_t run0 = ly.hist[(uint64_t)tile * 256 + tid];
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++)
+        for (uint32_t w = 0; w < NW; w++) off[u][w][tid] = 0;
+    __syncthreads();
+    const uint64_t lt = (1ull << lane) - 1ull;
+    uint8_t rk[SORT_PER];
 #pragma unroll
     for (uint32_t u = 0; u < SORT_PER; u++) {
-        const uint32_t e0 = u * SORT_THREADS;
-        if (base + e0 >= n) continue;  // uniform: the rest of the tile is past n
-        const uint64_t i = base + e0 + tid;
-        const bool valid = i < n;
-        const uint64_t k = kk[u];
-        const uint32_t v = vv[u], dg = valid ? (uint32_t)(k >> shift) & 255u : 0u;
+        const bool valid = base + u * SORT_THREADS + tid < n;
+        const uint32_t dg = (uint32_t)(kk[u] >> shift) & 255u;
         uint64_t same = __ballot(valid);
         for (int b = 0; b < 8; b++) {
             const bool bit = (dg >> b) & 1u;
@@ -124,23 +126,27 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
             same &= bit ? bb : ~bb;
         }
         const uint32_t r = __popcll(same & lt);
-        if (valid && r == 0) wc[wave][dg] = __popcll(same);
-        __syncthreads();
-        if (valid) {
-            uint32_t pre = run[dg];
-            for (uint32_t w = 0; w < wave; w++) pre += wc[w][dg];
-            const uint32_t dst = pre + r;
-            kout[dst] = k;
-            vout[dst] = v;
+        rk[u] = (uint8_t)r;
+        if (valid && r == 0) off[u][wave][dg] = __popcll(same);
+    }
+    __syncthreads();
+    // thread tid = digit: running offsets over (step, wave) in element order
+    uint32_t run = run0;
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++)
+        for (uint32_t w = 0; w < NW; w++) {
+            const uint32_t c = off[u][w][tid];
+            off[u][w][tid] = run;
+            run += c;
         }
-        __syncthreads();
-        uint32_t add = 0;
-        for (uint32_t w = 0; w < SORT_THREADS / 64; w++) {
-            add += wc[w][tid];
-            wc[w][tid] = 0;
-        }
-        run[tid] += add;
-        __syncthreads();
+    __syncthreads();
+#pragma unroll
+    for (uint32_t u = 0; u < SORT_PER; u++) {
+        if (base + u * SORT_THREADS + tid >= n) continue;
+        const uint32_t dg = (uint32_t)(kk[u] >> shift) & 255u;
+        const uint32_t dst = off[u][wave][dg] + rk[u];
+        kout[dst] = kk[u];
+        vout[dst] = vv[u];
     }
 }
 
