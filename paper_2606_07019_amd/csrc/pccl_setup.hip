@@ -248,9 +248,10 @@ __global__ void k_needs(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t
         uint32_t u = v;
         for (uint32_t hop = 0; hop < sz.D && u != s && u < sz.D; hop++) {
             unsigned long long *w = (unsigned long long *)&ly.needs[(uint64_t)u * sz.Wp + (r >> 6)];
-            if (hop > 0 && (*w & bit)) break;
-            atomicOr(w, bit);
-            u = par[u];
+            const uint32_t next = par[u];
+            // a relay bit another walk already set: that walk covers the rest
+            if ((atomicOr(w, bit) & bit) && hop > 0) break;
+            u = next;
         }
     }
 }
