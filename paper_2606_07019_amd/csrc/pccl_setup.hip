@@ -122,6 +122,8 @@ __global__ void __launch_bounds__(1024) k_compact_sources(Layout ly, Sizes sz)
     if (tid == 1023) ly.ctl->n_sources = part[1023];
 }
 
+constexpr uint32_t SP_BATCH = 8;  // links whose loads one thread issues together
+
 // Shortest paths from one source per workgroup (Alg. 3 ShortestPath over
 // the alpha-beta link times): Bellman-Ford relaxation with the distances in
 // LDS, then the parent of each device = the smallest-id in-neighbour on a
@@ -138,14 +140,27 @@ __global__ void __launch_bounds__(256) k_shortest_paths(Layout ly, Sizes sz)
     for (uint32_t it = 0; it < sz.D; it++) {
         if (tid == 0) changed = 0;
         __syncthreads();
-        for (uint32_t e = tid; e < sz.L; e += blockDim.x) {
-            const unsigned long long du = dist[ly.lsrc[e]];
-            if (du == NONE64) continue;
-            const unsigned long long nd = du + ly.ltime[e];
-            const uint32_t v = ly.ldst[e];
-            if (nd < dist[v]) {
-                atomicMin(&dist[v], nd);
-                changed = 1;
+        // eight links per thread loaded together (indices past L reread the
+        // last link and are skipped)
+        for (uint32_t e0 = tid; e0 < sz.L; e0 += SP_BATCH * blockDim.x) {
+            uint32_t ls[SP_BATCH], ld[SP_BATCH], lt[SP_BATCH];
+#pragma unroll
+            for (uint32_t k = 0; k < SP_BATCH; k++) {
+                const uint32_t e = min(e0 + k * blockDim.x, sz.L - 1u);
+                ls[k] = ly.lsrc[e];
+                ld[k] = ly.ldst[e];
+                lt[k] = ly.ltime[e];
+            }
+#pragma unroll
+            for (uint32_t k = 0; k < SP_BATCH; k++) {
+                if (e0 + k * blockDim.x >= sz.L) continue;
+                const unsigned long long du = dist[ls[k]];
+                if (du == NONE64) continue;
+                const unsigned long long nd = du + lt[k];
+                if (nd < dist[ld[k]]) {
+                    atomicMin(&dist[ld[k]], nd);
+                    changed = 1;
+                }
             }
         }
         __syncthreads();
@@ -158,10 +173,21 @@ __global__ void __launch_bounds__(256) k_shortest_paths(Layout ly, Sizes sz)
         ly.sp_dist[(uint64_t)b * sz.D + v] = dv;
         uint32_t par = NONE32;
         if (v != s && dv != NONE64) {
-            for (uint32_t i = ly.in_off[v]; i < ly.in_off[v + 1]; i++) {
-                const uint32_t u = ly.slot_src[i];
-                const unsigned long long du = dist[u];
-                if (du != NONE64 && du + ly.slot_time[i] == dv && u < par) par = u;
+            const uint32_t i0 = ly.in_off[v], i1 = ly.in_off[v + 1];
+            for (uint32_t i = i0; i < i1; i += SP_BATCH) {
+                uint32_t su[SP_BATCH], st[SP_BATCH];
+#pragma unroll
+                for (uint32_t k = 0; k < SP_BATCH; k++) {
+                    const uint32_t x = min(i + k, i1 - 1u);
+                    su[k] = ly.slot_src[x];
+                    st[k] = ly.slot_time[x];
+                }
+#pragma unroll
+                for (uint32_t k = 0; k < SP_BATCH; k++) {
+                    if (i + k >= i1) continue;
+                    const unsigned long long du = dist[su[k]];
+                    if (du != NONE64 && du + st[k] == dv && su[k] < par) par = su[k];
+                }
             }
         }
         ly.sp_parent[(uint64_t)b * sz.D + v] = par;
