@@ -284,9 +284,11 @@ pccl_status pccl_get_setup(pccl_ctx *ctx, uint32_t *link_time_ns, uint32_t *chun
  * events recorded on the library's stream around its three stages: setup
  * (conditions to initial bitmaps), matching (the persistent event-loop
  * kernel) and output (canonical sort and reversal).  scan_words counts the
- * 64-bit words of the two rows the intersect read (from a link's cursor
- * through the word holding its pick, or to the row end when it found
- * none).  Any pointer may be NULL.
+ * word positions of the two rows the intersect passed (from a link's cursor
+ * through the word holding its pick, or to the end of the row's own
+ * ceil(chunks / 64) words when it found none), including the positions a
+ * busy link's look-ahead passed; each position is one 64-bit word of each
+ * row.  Any pointer may be NULL.
  */
 pccl_status pccl_get_profile(pccl_ctx *ctx, double *setup_ms, double *match_ms, double *output_ms,
                              uint64_t *scan_words);
