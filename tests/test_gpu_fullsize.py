@@ -47,7 +47,7 @@ def test_full_size_matches_oracle(k):
         s.close()
 
 
-@pytest.mark.parametrize("k", [3, 5])
+@pytest.mark.parametrize("k", [3, 4, 5])
 def test_repeat_runs_identical(k):
     # the schedule must not depend on workgroup timing
     print(f"[repeat] config {k}", flush=True)
