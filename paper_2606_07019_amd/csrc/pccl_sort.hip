@@ -152,6 +152,97 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
 
 __global__ void k_sort_reset(Layout ly) { ly.ctl->sort_cur = 0; }
 
+// The whole sort of at most one tile (SORT_TILE elements) in one workgroup:
+// keys and values stay in LDS for all passes (ping-pong), each pass counts
+// digits, scans them and scatters stably (ranks among equal digits by
+// ballots per 256-element step, as in k_scatter); a pass whose digit is the
+// same for every element is skipped.  The result is written back to the
+// current buffer (buffer 0 after a reset), so the buffer index does not
+// change.  Only the ceil(n / 256) steps that hold elements are worked.
+__global__ void __launch_bounds__(SORT_THREADS) k_sort_small(Layout ly, uint32_t n, int byte_lo, int byte_hi,
+                                                             bool reset_cur)
+{
+    constexpr uint32_t NW = SORT_THREADS / 64;
+    __shared__ uint64_t key[2][SORT_TILE];
+    __shared__ uint32_t val[2][SORT_TILE];
+    __shared__ uint32_t cnt[256];
+    __shared__ uint16_t wc[SORT_PER][NW][256];  // counts, then offsets (below SORT_TILE)
+    static_assert(SORT_TILE <= 65536, "offsets are 16-bit");
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t cur = reset_cur ? 0u : ly.ctl->sort_cur;
+    if (reset_cur && tid == 0) ly.ctl->sort_cur = 0;
+    const uint32_t steps = (n + SORT_THREADS - 1) / SORT_THREADS;
+    for (uint32_t e = tid; e < n; e += SORT_THREADS) {
+        key[0][e] = ly.skey[cur][e];
+        val[0][e] = ly.sval[cur][e];
+    }
+    uint32_t b = 0;  // buffer holding the current order
+    const uint64_t lt = (1ull << lane) - 1ull;
+    for (int by = byte_lo; by < byte_hi; by++) {
+        const int shift = 8 * by;
+        cnt[tid] = 0;
+        for (uint32_t u = 0; u < steps; u++)
+            for (uint32_t w = 0; w < NW; w++) wc[u][w][tid] = 0;
+        __syncthreads();
+        // ranks among equal digits inside each (step, wave), and their counts
+        uint8_t rk[SORT_PER];
+#pragma unroll
+        for (uint32_t u = 0; u < SORT_PER; u++) {
+            if (u >= steps) break;
+            const uint32_t e = u * SORT_THREADS + tid;
+            const bool valid = e < n;
+            const uint32_t dg = valid ? (uint32_t)(key[b][e] >> shift) & 255u : 0u;
+            uint64_t same = __ballot(valid);
+            for (int bit = 0; bit < 8; bit++) {
+                const bool x = (dg >> bit) & 1u;
+                const uint64_t bb = __ballot(x);
+                same &= x ? bb : ~bb;
+            }
+            const uint32_t r = __popcll(same & lt);
+            rk[u] = (uint8_t)r;
+            if (valid && r == 0) {
+                wc[u][wave][dg] = (uint16_t)__popcll(same);
+                atomicAdd(&cnt[dg], (uint32_t)__popcll(same));
+            }
+        }
+        // one digit for every element: the pass is a no-op
+        if (__syncthreads_or(cnt[tid] == n)) continue;
+        // exclusive scan of the digit counts (Hillis-Steele), then offsets
+        // per (step, wave) in element order for digit tid
+        uint32_t v = cnt[tid];
+        __syncthreads();
+        for (uint32_t off = 1; off < 256; off <<= 1) {
+            const uint32_t x = tid >= off ? cnt[tid - off] : 0u;
+            __syncthreads();
+            cnt[tid] += x;
+            __syncthreads();
+        }
+        uint32_t run = cnt[tid] - v;
+        for (uint32_t u = 0; u < steps; u++)
+            for (uint32_t w = 0; w < NW; w++) {
+                const uint32_t c = wc[u][w][tid];
+                wc[u][w][tid] = (uint16_t)run;
+                run += c;
+            }
+        __syncthreads();
+#pragma unroll
+        for (uint32_t u = 0; u < SORT_PER; u++) {
+            const uint32_t e = u * SORT_THREADS + tid;
+            if (e >= n) break;
+            const uint32_t dg = (uint32_t)(key[b][e] >> shift) & 255u;
+            const uint32_t dst = wc[u][wave][dg] + rk[u];
+            key[b ^ 1u][dst] = key[b][e];
+            val[b ^ 1u][dst] = val[b][e];
+        }
+        b ^= 1u;
+        __syncthreads();
+    }
+    for (uint32_t e = tid; e < n; e += SORT_THREADS) {
+        ly.skey[cur][e] = key[b][e];
+        ly.sval[cur][e] = val[b][e];
+    }
+}
+
 // Send log -> schedule.  Log key = t_start << 32 | link, value = rank.
 // `add_cstar` shifts start times by the copy schedule's collective time
 // (the All-Gather half of an All-Reduce).
@@ -188,6 +279,10 @@ __global__ void k_reverse_keys(Layout ly, uint64_t n)
 hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_hi, uint32_t max_tiles,
                             bool reset_cur, hipStream_t st)
 {
+    if (n && n <= SORT_TILE) {
+        k_sort_small<<<1, SORT_THREADS, 0, st>>>(ly, (uint32_t)n, byte_lo, byte_hi, reset_cur);
+        return hipGetLastError();
+    }
     if (reset_cur) {
         k_sort_reset<<<1, 1, 0, st>>>(ly);
     }

@@ -99,3 +99,17 @@ def test_needs_rows_in_device_memory_parity():
     dests = [[(c + 1) % n] if c < 600 else [] for c in range(C)]
     coll = W.collective_from_lists(n, C, 1 << 12, src, dests, [range(n)])
     _compare(W.Workload("ring300_c524288_sparse", topo, coll, 5), "needs rows in device memory")
+
+
+@pytest.mark.parametrize("n_chunks,n_dest", [(4096, 1), (4097, 1), (4095, 2), (2048, 2), (2049, 2)])
+def test_sort_tile_boundary_parity(n_chunks, n_dest):
+    """Chunk and transfer counts around one sort tile (4,096 elements): up to
+    a tile, a sort runs in one workgroup with all passes in LDS; above it,
+    in tiles with a kernel per step.  Chunks start round-robin on a 16-NPU
+    ring and go to the next n_dest NPUs, so the priority sort sorts
+    n_chunks keys and the output sort n_chunks * n_dest transfers."""
+    n = 16
+    src = [c % n for c in range(n_chunks)]
+    dests = [[(c + k) % n for k in range(1, n_dest + 1)] for c in range(n_chunks)]
+    coll = W.collective_from_lists(n, n_chunks, 1 << 14, src, dests, [range(n)])
+    _compare(W.Workload(f"ring16_c{n_chunks}_d{n_dest}", W.ring(n), coll, n_chunks), "sort tile boundary")
