@@ -192,7 +192,8 @@ pccl_status pccl_workspace_bytes(pccl_ctx *ctx, uint64_t max_sends, size_t *out_
  * Hands over the device workspace (caller-owned, 256-byte aligned, at least
  * the size pccl_workspace_bytes returned for `max_sends`) and the HIP stream
  * to run on (NULL = the default stream).  The library allocates no device
- * memory of its own.  The workspace must not be used by the caller while a
+ * memory of its own (a context holds one small pinned host block, from its
+ * first synthesize call, for reading the device's counters).  The workspace must not be used by the caller while a
  * synthesize call runs.  PCCL_ENOMEM if `bytes` is too small.
  */
 pccl_status pccl_set_workspace(pccl_ctx *ctx, void *device_ptr, size_t bytes,
@@ -282,8 +283,9 @@ pccl_status pccl_get_setup(pccl_ctx *ctx, uint32_t *link_time_ns, uint32_t *chun
 /*
  * Timing and work counters of the last synthesize call, measured with HIP
  * events recorded on the library's stream around its three stages: setup
- * (conditions to initial bitmaps), matching (the persistent event-loop
- * kernel) and output (canonical sort and reversal).  scan_words counts the
+ * (conditions to initial bitmaps, and the copy of the delivery count to the
+ * host), matching (the persistent event-loop kernel) and output (canonical
+ * sort and reversal, queued while the matching kernel runs).  scan_words counts the
  * word positions of the two rows the intersect passed (from a link's cursor
  * through the word holding its pick, or to the end of the row's own
  * ceil(chunks / 64) words when it found none), including the positions a

@@ -56,13 +56,16 @@ struct pccl_ctx {
     Sizes sz{};
     int grid = 0, wpb = 0;  // matching kernel: workgroups, waves per workgroup
     bool mirror = false;    // matching kernel keeps each destination's needs row in LDS
-    // stage timing
+    // stage timing; ev[1] also marks that the setup's counts have reached `pin`
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     float stage_ms[3] = {0.f, 0.f, 0.f};
+    // pinned host copies of the control block: [0] after the setup, [1] at the end
+    Control *pin = nullptr;
     ~pccl_ctx()
     {
         for (hipEvent_t e : ev)
             if (e) (void)hipEventDestroy(e);
+        if (pin) (void)hipHostFree(pin);
     }
     // results
     std::unordered_map<uint64_t, uint64_t> receipt;  // (chunk << 32 | device) -> (link << 32 | t_start), copy schedule
@@ -765,28 +768,35 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     hipStream_t st = c->stream;
     for (hipEvent_t &e : c->ev)
         if (!e) HIP_OR_FAIL(c, hipEventCreate(&e));
+    if (!c->pin) HIP_OR_FAIL(c, hipHostMalloc((void **)&c->pin, 2 * sizeof(Control), hipHostMallocDefault));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[0], st));
     HIP_OR_FAIL(c, launch_setup(c->ly, c->sz, c->pre, c->post, c->chunk_group, c->seed, st));
+    // the setup's delivery count sizes the output stage; the host reads it
+    // while the matching kernel runs and queues the output kernels behind it
+    HIP_OR_FAIL(c, hipMemcpyAsync(&c->pin[0], c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[1], st));
     if (c->sw_active)
         HIP_OR_FAIL(c, launch_match_sw(c->ly, c->sz, st, c->sw_grid));
     else
         HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb, c->mirror));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
-    HIP_OR_FAIL(c, hipMemcpyAsync(&c->ctl_host, c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
+    HIP_OR_FAIL(c, hipEventSynchronize(c->ev[1]));
+    const Control s0 = c->pin[0];
+    const bool out_queued = !s0.error && s0.needs_total <= c->max_sends;
+    if (out_queued) HIP_OR_FAIL(c, launch_output(c->ly, c->sz, c->op, s0.needs_total, st));
+    HIP_OR_FAIL(c, hipEventRecord(c->ev[3], st));
+    HIP_OR_FAIL(c, hipMemcpyAsync(&c->pin[1], c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
     HIP_OR_FAIL(c, hipStreamSynchronize(st));
+    c->ctl_host = c->pin[1];
     const Control &h = c->ctl_host;
     if (h.abort) return fail(c, PCCL_EINTERNAL, "matching kernel barrier timed out");
     if (h.error) return device_error(c, h);
-    if (h.n_log != h.needs_total)
+    if (h.n_log != h.needs_total || !out_queued || h.needs_total != s0.needs_total)
         return fail(c, PCCL_EINTERNAL, "logged %llu transfers for %llu deliveries", (unsigned long long)h.n_log,
                     (unsigned long long)h.needs_total);
     const uint64_t n = h.n_log;
     if (c->op == PCCL_OP_ALLREDUCE && 2ull * h.cstar > 0xFFFFFFFFull)
         return fail(c, PCCL_ERANGE, "all-reduce time does not fit in 32 bits");
-    HIP_OR_FAIL(c, launch_output(c->ly, c->sz, c->op, n, h.cstar, st));
-    HIP_OR_FAIL(c, hipEventRecord(c->ev[3], st));
-    HIP_OR_FAIL(c, hipStreamSynchronize(st));
     for (int i = 0; i < 3; i++) HIP_OR_FAIL(c, hipEventElapsedTime(&c->stage_ms[i], c->ev[i], c->ev[i + 1]));
     c->n_copy = n;
     c->n_sends = c->op == PCCL_OP_ALLREDUCE ? 2 * n : n;

@@ -168,11 +168,13 @@ int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds)
 size_t match_static_lds();  // static LDS bytes of the matching kernel
 hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
 int match_sw_max_grid(int device);
-hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st);
+hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st);
 // LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;
 // the sorted order ends up in buffer ly.ctl->sort_cur (read it on the device).
+// time_gate: the bytes are start-time bytes (key bits 32..63) and a byte
+// past the device's collective time is skipped.
 hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_hi, uint32_t max_tiles,
-                            bool reset_cur, hipStream_t st);
+                            bool reset_cur, hipStream_t st, bool time_gate = false);
 constexpr uint32_t SORT_TILE = 4096;      // elements per radix-sort tile
 constexpr uint32_t SORT_THREADS = 256;
 

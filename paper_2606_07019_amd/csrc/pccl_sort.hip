@@ -7,11 +7,28 @@ namespace {
 
 constexpr uint32_t SORT_PER = SORT_TILE / SORT_THREADS;  // elements of a tile per thread
 
+// A pass with tgate >= 0 sorts a byte of the start time and runs only if the
+// collective time has bits at or above tgate (start times are below it), so
+// the number of time bytes follows the device's collective time without a
+// host round trip.  tgate < 0: the pass always runs.
+__device__ inline bool pass_active(const Layout &ly, int tgate)
+{
+    return tgate < 0 || (ly.ctl->cstar >> tgate) != 0u;
+}
+
+// The send log is complete: the output kernels, which index tables by the
+// logged values, run only then (otherwise the call reports an error).
+__device__ inline bool log_complete(const Layout &ly)
+{
+    return !ly.ctl->error && !ly.ctl->abort && ly.ctl->n_log == ly.ctl->needs_total;
+}
+
 // Per-tile digit histogram, stored tile-major: hist[tile * 256 + digit].
 // A thread's keys are loaded together (indices past n reread the last key
 // and are not counted), so the tile costs one memory round trip.
-__global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles)
+__global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles, int tgate)
 {
+    if (!pass_active(ly, tgate)) return;
     __shared__ uint32_t cnt[256];
     const uint32_t tid = threadIdx.x, tile = blockIdx.x;
     cnt[tid] = 0;
@@ -35,11 +52,18 @@ __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, in
 // a thread has few dependent loads to wait for.
 constexpr uint32_t SCAN_SPLIT = 4;
 
-__global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n, uint32_t tiles)
+__global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n, uint32_t tiles, int tgate)
 {
     __shared__ uint32_t part[SCAN_SPLIT][256];
     __shared__ uint32_t pre[256];
     __shared__ uint32_t skip;
+    if (!pass_active(ly, tgate)) {
+        if (threadIdx.x == 0) {
+            ly.ctl->sort_src = ly.ctl->sort_cur;
+            ly.ctl->sort_skip = 1;
+        }
+        return;
+    }
     const uint32_t d = threadIdx.x & 255u, q = threadIdx.x >> 8;
     const uint32_t per = (tiles + SCAN_SPLIT - 1) / SCAN_SPLIT;
     const uint32_t t0 = min(q * per, tiles), t1 = min(t0 + per, tiles);
@@ -159,8 +183,10 @@ __global__ void k_sort_reset(Layout ly) { ly.ctl->sort_cur = 0; }
 // same for every element is skipped.  The result is written back to the
 // current buffer (buffer 0 after a reset), so the buffer index does not
 // change.  Only the ceil(n / 256) steps that hold elements are worked.
+// time_gate: byte b of the range is a start-time byte and runs only if the
+// collective time reaches it (pass_active with tgate = 8 (b - byte_lo)).
 __global__ void __launch_bounds__(SORT_THREADS) k_sort_small(Layout ly, uint32_t n, int byte_lo, int byte_hi,
-                                                             bool reset_cur)
+                                                             bool reset_cur, bool time_gate)
 {
     constexpr uint32_t NW = SORT_THREADS / 64;
     __shared__ uint64_t key[2][SORT_TILE];
@@ -179,6 +205,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_sort_small(Layout ly, uint32_t
     uint32_t b = 0;  // buffer holding the current order
     const uint64_t lt = (1ull << lane) - 1ull;
     for (int by = byte_lo; by < byte_hi; by++) {
+        if (!pass_active(ly, time_gate ? 8 * (by - byte_lo) : -1)) break;
         const int shift = 8 * by;
         cnt[tid] = 0;
         for (uint32_t u = 0; u < steps; u++)
@@ -249,7 +276,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_sort_small(Layout ly, uint32_t
 __global__ void k_out_copy(Layout ly, uint64_t n, uint64_t out_off, uint32_t add_cstar, uint32_t flags)
 {
     uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
+    if (i >= n || !log_complete(ly)) return;
     const uint32_t cur = ly.ctl->sort_cur;
     const uint64_t k = ly.skey[cur][i];
     const uint32_t r = ly.sval[cur][i];
@@ -266,7 +293,7 @@ __global__ void k_out_copy(Layout ly, uint64_t n, uint64_t out_off, uint32_t add
 __global__ void k_reverse_keys(Layout ly, uint64_t n)
 {
     uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
+    if (i >= n || !log_complete(ly)) return;
     const uint32_t cur = ly.ctl->sort_cur;
     const uint64_t k = ly.skey[cur][i];
     const uint32_t l = (uint32_t)k, t = (uint32_t)(k >> 32);
@@ -277,10 +304,10 @@ __global__ void k_reverse_keys(Layout ly, uint64_t n)
 }  // namespace
 
 hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_hi, uint32_t max_tiles,
-                            bool reset_cur, hipStream_t st)
+                            bool reset_cur, hipStream_t st, bool time_gate)
 {
     if (n && n <= SORT_TILE) {
-        k_sort_small<<<1, SORT_THREADS, 0, st>>>(ly, (uint32_t)n, byte_lo, byte_hi, reset_cur);
+        k_sort_small<<<1, SORT_THREADS, 0, st>>>(ly, (uint32_t)n, byte_lo, byte_hi, reset_cur, time_gate);
         return hipGetLastError();
     }
     if (reset_cur) {
@@ -290,8 +317,9 @@ hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_
     const uint32_t tiles = (uint32_t)((n + SORT_TILE - 1) / SORT_TILE);
     if (tiles > max_tiles) return hipErrorInvalidValue;
     for (int b = byte_lo; b < byte_hi; b++) {
-        k_hist<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
-        k_scan<<<1, 256 * SCAN_SPLIT, 0, st>>>(ly, n, tiles);
+        const int tgate = time_gate ? 8 * (b - byte_lo) : -1;
+        k_hist<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles, tgate);
+        k_scan<<<1, 256 * SCAN_SPLIT, 0, st>>>(ly, n, tiles, tgate);
         k_scatter<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
     }
     return hipGetLastError();
@@ -309,12 +337,15 @@ static int bytes_for(uint64_t maxval)
 
 // Output stage: the send log (n entries, key t_start << 32 | link, value
 // rank) is in sort buffer 0.  Writes the canonical schedule to ly.out.
-hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, uint32_t cstar, hipStream_t st)
+// n is the number of deliveries the setup counted; the kernels may be
+// queued before the matching kernel has run, so the collective time is
+// read on the device and nothing is written unless the log is complete.
+hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st)
 {
     // only the significant bytes of the link id (low word) and of the start
     // time (high word, start times are below the collective time) are sorted
     const int link_bytes = bytes_for(sz.L ? sz.L - 1 : 0);
-    const int time_bytes = bytes_for(cstar);
+    const int time_bytes = 4;  // passes past the collective time's bytes are gated off
     const int threads = 256;
     const uint64_t blocks = (n + threads - 1) / threads;
     hipError_t e;
@@ -322,7 +353,7 @@ hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, 
         // forward schedule sorted by (t_start, link)
         e = radix_sort_pairs(ly, n, 0, link_bytes, sz.max_tiles, true, st);
         if (e != hipSuccess) return e;
-        e = radix_sort_pairs(ly, n, 4, 4 + time_bytes, sz.max_tiles, false, st);
+        e = radix_sort_pairs(ly, n, 4, 4 + time_bytes, sz.max_tiles, false, st, true);
         if (e != hipSuccess) return e;
         if (n) {
             if (op == 0)
@@ -337,7 +368,7 @@ hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, 
         if (n) k_reverse_keys<<<blocks, threads, 0, st>>>(ly, n);
         e = radix_sort_pairs(ly, n, 0, link_bytes, sz.max_tiles, false, st);
         if (e != hipSuccess) return e;
-        e = radix_sort_pairs(ly, n, 4, 4 + time_bytes, sz.max_tiles, false, st);
+        e = radix_sort_pairs(ly, n, 4, 4 + time_bytes, sz.max_tiles, false, st, true);
         if (e != hipSuccess) return e;
         if (n) k_out_copy<<<blocks, threads, 0, st>>>(ly, n, 0, 0, 1);
     }
