@@ -159,7 +159,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.skey[1] = cv.take<uint64_t>(nsort);
     ly.sval[0] = cv.take<uint32_t>(nsort);
     ly.sval[1] = cv.take<uint32_t>(nsort);
-    ly.hist = cv.take<uint32_t>(256ull * sz.max_tiles);
+    ly.hist = cv.take<uint32_t>(256ull * hist_stride(sz.max_tiles));
     ly.holds = cv.take<uint64_t>(D * sz.Wp);
     ly.needs = cv.take<uint64_t>(D * sz.Wp);
     ly.busy = cv.take<uint32_t>(L);

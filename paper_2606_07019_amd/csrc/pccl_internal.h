@@ -53,8 +53,8 @@ struct Control {
     uint32_t abort;          // set when a window exchange wait times out
     uint32_t cstar;          // collective time of the copy schedule
     uint32_t sort_cur;       // radix sort: buffer holding the current order
-    uint32_t sort_src;       // radix sort: buffer read by the pending scatter
-    uint32_t sort_skip;      // radix sort: pending pass is a no-op
+    uint32_t sort_buf[9];    // radix sort: buffer holding the order before pass i of a sort
+    uint32_t sort_skip;      // radix sort (scan kernel): the pending pass is a no-op
     uint32_t pad[1];
 };
 
@@ -134,7 +134,7 @@ struct Layout {
     // sort buffers (chunk order first, then the send log)
     uint64_t *skey[2];     // [max(C, 2*max_sends)]
     uint32_t *sval[2];
-    uint32_t *hist;        // [256 * max_tiles]
+    uint32_t *hist;        // [256 * hist_stride(max_tiles)], digit-major
     // matching state
     uint64_t *holds, *needs;  // [D * Wp]
     uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
@@ -177,5 +177,8 @@ hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_
                             bool reset_cur, hipStream_t st, bool time_gate = false);
 constexpr uint32_t SORT_TILE = 4096;      // elements per radix-sort tile
 constexpr uint32_t SORT_THREADS = 256;
+// row length of the digit-major tile histogram (a multiple of 4 tiles, so a
+// row is read in 16-byte loads)
+inline __host__ __device__ uint32_t hist_stride(uint32_t tiles) { return (tiles + 3u) & ~3u; }
 
 }  // namespace pccl

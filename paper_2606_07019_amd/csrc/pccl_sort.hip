@@ -23,17 +23,33 @@ __device__ inline bool log_complete(const Layout &ly)
     return !ly.ctl->error && !ly.ctl->abort && ly.ctl->n_log == ly.ctl->needs_total;
 }
 
-// Per-tile digit histogram, stored tile-major: hist[tile * 256 + digit].
-// A thread's keys are loaded together (indices past n reread the last key
-// and are not counted), so the tile costs one memory round trip.
-__global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles, int tgate)
+// Buffer holding the order before pass `pass` of a sort.  Pass 0 takes it
+// from sort_cur (buffer 0 after a reset); later passes from sort_buf, which
+// each pass's scatter writes for the next one, so no kernel rewrites a
+// field the blocks of the same kernel read.
+__device__ inline uint32_t pass_src(const Layout &ly, uint32_t pass, bool reset)
 {
+    return pass ? ly.ctl->sort_buf[pass] : (reset ? 0u : ly.ctl->sort_cur);
+}
+
+// Per-tile digit histogram, stored digit-major, hist[digit * stride + tile]
+// (stride = hist_stride(tiles)), for scatters that read a digit's row, or
+// tile-major, hist[tile * 256 + digit], for the scan kernel (coalesced over
+// digits).  A thread's keys are loaded together (indices past n reread the
+// last key and are not counted), so the tile costs one memory round trip.
+// Pass 0 also records the sort's start buffer.
+template <bool DIGIT_MAJOR>
+__global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, int shift, uint32_t tiles, int tgate,
+                                                       uint32_t pass, bool reset)
+{
+    const uint32_t tid = threadIdx.x, tile = blockIdx.x;
+    const uint32_t src = pass_src(ly, pass, reset);
+    if (pass == 0 && tile == 0 && tid == 0) ly.ctl->sort_buf[0] = src;
     if (!pass_active(ly, tgate)) return;
     __shared__ uint32_t cnt[256];
-    const uint32_t tid = threadIdx.x, tile = blockIdx.x;
     cnt[tid] = 0;
     __syncthreads();
-    const uint64_t *key = ly.skey[ly.ctl->sort_cur];
+    const uint64_t *key = ly.skey[src];
     const uint64_t base = (uint64_t)tile * SORT_TILE;
     uint32_t dg[SORT_PER];
 #pragma unroll
@@ -43,27 +59,24 @@ __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, in
     for (uint32_t u = 0; u < SORT_PER; u++)
         if (base + u * SORT_THREADS + tid < n) atomicAdd(&cnt[dg[u]], 1u);
     __syncthreads();
-    ly.hist[(uint64_t)tile * 256 + tid] = cnt[tid];
+    ly.hist[DIGIT_MAJOR ? (uint64_t)tid * hist_stride(tiles) + tile : (uint64_t)tile * 256 + tid] = cnt[tid];
 }
 
-// Exclusive scan of the histogram (one workgroup), in (digit, tile) order,
-// and the skip decision: a pass whose digit is the same for every element
-// is a no-op.  Four threads per digit each take a quarter of the tiles, so
-// a thread has few dependent loads to wait for.
+// Sorts of more than OWN_PREFIX_TILES tiles scan the histogram in a kernel
+// of its own (one workgroup) instead of every tile reading its digit's whole
+// row, which grows with the square of the tile count.
+constexpr uint32_t OWN_PREFIX_TILES = 256;
 constexpr uint32_t SCAN_SPLIT = 4;
 
+// Exclusive scan of the tile-major histogram in (digit, tile) order, in
+// place, and the skip decision (some digit holds every element).  Four
+// threads per digit each take a quarter of the tiles, so a thread has few
+// dependent loads to wait for; a wave's loads cover 64 adjacent digits.
 __global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n, uint32_t tiles, int tgate)
 {
+    if (!pass_active(ly, tgate)) return;
     __shared__ uint32_t part[SCAN_SPLIT][256];
     __shared__ uint32_t pre[256];
-    __shared__ uint32_t skip;
-    if (!pass_active(ly, tgate)) {
-        if (threadIdx.x == 0) {
-            ly.ctl->sort_src = ly.ctl->sort_cur;
-            ly.ctl->sort_skip = 1;
-        }
-        return;
-    }
     const uint32_t d = threadIdx.x & 255u, q = threadIdx.x >> 8;
     const uint32_t per = (tiles + SCAN_SPLIT - 1) / SCAN_SPLIT;
     const uint32_t t0 = min(q * per, tiles), t1 = min(t0 + per, tiles);
@@ -71,15 +84,13 @@ __global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n
 #pragma unroll 16
     for (uint32_t t = t0; t < t1; t++) tot += ly.hist[(uint64_t)t * 256 + d];
     part[q][d] = tot;
-    if (threadIdx.x == 0) skip = 0;
     __syncthreads();
     uint32_t all = 0;
     for (uint32_t r = 0; r < SCAN_SPLIT; r++) all += part[r][d];
-    if (q == 0) {
-        pre[d] = all;
-        if (all == (uint32_t)n) skip = 1;
-    }
-    __syncthreads();
+    if (q == 0) pre[d] = all;
+    const bool skip = __syncthreads_or(all == (uint32_t)n);
+    if (threadIdx.x == 0) ly.ctl->sort_skip = skip;
+    if (skip) return;
     for (uint32_t off = 1; off < 256; off <<= 1) {
         const uint32_t v = (q == 0 && d >= off) ? pre[d - off] : 0u;
         __syncthreads();
@@ -95,30 +106,39 @@ __global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n
         ly.hist[x] = run;
         run += v;
     }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t cur = ly.ctl->sort_cur;
-        ly.ctl->sort_src = cur;
-        ly.ctl->sort_skip = skip;
-        ly.ctl->sort_cur = skip ? cur : cur ^ 1u;
-    }
 }
 
-// Stable scatter of one tile.  Element e = 256 u + tid of the tile is step u
-// of its thread.  Every wave ranks its elements among equal digits of the
-// same step with 8 ballots (one per digit bit) and records, per step and
-// digit, how many it holds; after one barrier a thread per digit turns the
-// counts, in (step, wave) order, into destination offsets; after a second
-// barrier every element is written to offset + rank.  A thread's 16 keys
-// and values are loaded together (indices past n reread the last element
-// and are not written).
-__global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n, int shift, uint32_t tiles)
+// Stable scatter of one tile.  Thread tid owns digit tid: it reads the
+// digit's histogram row (16-byte loads, issued with the tile's keys) and
+// sums the counts of the tiles before this one and of all tiles; a
+// wave-level scan of the totals over digits gives the digit's base, so the
+// tile's first destination for the digit is base + earlier tiles' count.
+// A pass whose digit is the same for every element (some total equals n) is
+// a no-op; every block takes that decision alike.  Element e = 256 u + tid
+// of the tile is step u of its thread.  Every wave ranks its elements among
+// equal digits of the same step with 8 ballots (one per digit bit) and
+// records, per step and digit, how many it holds; after one barrier a
+// thread per digit turns the counts, in (step, wave) order, into
+// destination offsets; after a second barrier every element is written to
+// offset + rank.  Block 0 records the result buffer for the next pass and
+// in sort_cur (read only after the sort).  Without OWN_PREFIX, k_scan has
+// turned the tile-major histogram into each (tile, digit)'s first
+// destination and decided the skip.
+template <bool OWN_PREFIX>
+__global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n, int shift, uint32_t tiles, int tgate,
+                                                          uint32_t pass)
 {
-    if (ly.ctl->sort_skip) return;
     constexpr uint32_t NW = SORT_THREADS / 64;
+    constexpr uint32_t COL_UNROLL = 32;  // 16-byte histogram loads in flight per thread
     __shared__ uint32_t off[SORT_PER][NW][256];  // counts, then offsets, per (step, wave, digit)
+    __shared__ uint32_t wsum[NW];
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, tile = blockIdx.x;
-    const uint32_t src = ly.ctl->sort_src;
+    const uint32_t src = ly.ctl->sort_buf[pass];
+    const bool lead = tile == 0 && tid == 0;
+    if (!pass_active(ly, tgate) || (!OWN_PREFIX && ly.ctl->sort_skip)) {
+        if (lead) ly.ctl->sort_buf[pass + 1] = ly.ctl->sort_cur = src;
+        return;
+    }
     const uint64_t *kin = ly.skey[src];
     const uint32_t *vin = ly.sval[src];
     uint64_t *kout = ly.skey[src ^ 1u];
@@ -132,11 +152,37 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
         kk[u] = kin[i];
         vv[u] = vin[i];
     }
-    const uint32_t run0 = ly.hist[(uint64_t)tile * 256 + tid];
+    // digit tid over the tiles: before this one, and all
+    const uint32_t hs = hist_stride(tiles);
+    const uint4 *col = reinterpret_cast<const uint4 *>(ly.hist + (uint64_t)tid * hs);
+    uint32_t before = 0, total = 0;
+    if (!OWN_PREFIX) before = ly.hist[(uint64_t)tile * 256 + tid];
+#pragma unroll COL_UNROLL
+    for (uint32_t q = 0; q < (OWN_PREFIX ? hs / 4 : 0u); q++) {
+        const uint4 v = col[q];
+        const uint32_t t = 4 * q;
+        const uint32_t x0 = t < tiles ? v.x : 0u, x1 = t + 1 < tiles ? v.y : 0u;
+        const uint32_t x2 = t + 2 < tiles ? v.z : 0u, x3 = t + 3 < tiles ? v.w : 0u;
+        total += x0 + x1 + x2 + x3;
+        before += (t < tile ? x0 : 0u) + (t + 1 < tile ? x1 : 0u) + (t + 2 < tile ? x2 : 0u) +
+                  (t + 3 < tile ? x3 : 0u);
+    }
 #pragma unroll
     for (uint32_t u = 0; u < SORT_PER; u++)
         for (uint32_t w = 0; w < NW; w++) off[u][w][tid] = 0;
-    __syncthreads();
+    // inclusive scan of the totals over the wave's 64 digits
+    uint32_t inc = total;
+    for (uint32_t o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    if (__syncthreads_or(OWN_PREFIX && total == (uint32_t)n)) {
+        if (lead) ly.ctl->sort_buf[pass + 1] = ly.ctl->sort_cur = src;
+        return;
+    }
+    uint32_t run0 = inc - total + before;  // without OWN_PREFIX: total = inc = 0
+    for (uint32_t w = 0; w < wave; w++) run0 += wsum[w];
     const uint64_t lt = (1ull << lane) - 1ull;
     uint8_t rk[SORT_PER];
 #pragma unroll
@@ -172,6 +218,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
         kout[dst] = kk[u];
         vout[dst] = vv[u];
     }
+    if (lead) ly.ctl->sort_buf[pass + 1] = ly.ctl->sort_cur = src ^ 1u;
 }
 
 __global__ void k_sort_reset(Layout ly) { ly.ctl->sort_cur = 0; }
@@ -310,17 +357,23 @@ hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_
         k_sort_small<<<1, SORT_THREADS, 0, st>>>(ly, (uint32_t)n, byte_lo, byte_hi, reset_cur, time_gate);
         return hipGetLastError();
     }
-    if (reset_cur) {
-        k_sort_reset<<<1, 1, 0, st>>>(ly);
+    if (n == 0 || byte_hi <= byte_lo) {
+        if (reset_cur) k_sort_reset<<<1, 1, 0, st>>>(ly);
+        return hipGetLastError();
     }
-    if (n == 0) return hipGetLastError();
     const uint32_t tiles = (uint32_t)((n + SORT_TILE - 1) / SORT_TILE);
-    if (tiles > max_tiles) return hipErrorInvalidValue;
+    if (tiles > max_tiles || byte_hi - byte_lo > 8) return hipErrorInvalidValue;
     for (int b = byte_lo; b < byte_hi; b++) {
         const int tgate = time_gate ? 8 * (b - byte_lo) : -1;
-        k_hist<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles, tgate);
-        k_scan<<<1, 256 * SCAN_SPLIT, 0, st>>>(ly, n, tiles, tgate);
-        k_scatter<<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles);
+        const uint32_t pass = (uint32_t)(b - byte_lo);
+        if (tiles <= OWN_PREFIX_TILES) {
+            k_hist<true><<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles, tgate, pass, reset_cur);
+            k_scatter<true><<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles, tgate, pass);
+        } else {
+            k_hist<false><<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles, tgate, pass, reset_cur);
+            k_scan<<<1, 256 * SCAN_SPLIT, 0, st>>>(ly, n, tiles, tgate);
+            k_scatter<false><<<tiles, SORT_THREADS, 0, st>>>(ly, n, 8 * b, tiles, tgate, pass);
+        }
     }
     return hipGetLastError();
 }
