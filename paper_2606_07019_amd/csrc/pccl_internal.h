@@ -134,7 +134,7 @@ struct Layout {
     // sort buffers (chunk order first, then the send log)
     uint64_t *skey[2];     // [max(C, 2*max_sends)]
     uint32_t *sval[2];
-    uint32_t *hist;        // [256 * hist_stride(max_tiles)], digit-major
+    uint32_t *hist;        // [256 * hist_stride(max_tiles)]: tile-major 32-bit or digit-major 16-bit counts
     // matching state
     uint64_t *holds, *needs;  // [D * Wp]
     uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
@@ -177,8 +177,8 @@ hipError_t radix_sort_pairs(const Layout &ly, uint64_t n, int byte_lo, int byte_
                             bool reset_cur, hipStream_t st, bool time_gate = false);
 constexpr uint32_t SORT_TILE = 4096;      // elements per radix-sort tile
 constexpr uint32_t SORT_THREADS = 256;
-// row length of the digit-major tile histogram (a multiple of 4 tiles, so a
-// row is read in 16-byte loads)
-inline __host__ __device__ uint32_t hist_stride(uint32_t tiles) { return (tiles + 3u) & ~3u; }
+// row length of the digit-major tile histogram, 16-bit counts (a multiple
+// of 8 tiles, so a row is read in 16-byte loads)
+inline __host__ __device__ uint32_t hist_stride(uint32_t tiles) { return (tiles + 7u) & ~7u; }
 
 }  // namespace pccl

@@ -32,10 +32,11 @@ __device__ inline uint32_t pass_src(const Layout &ly, uint32_t pass, bool reset)
     return pass ? ly.ctl->sort_buf[pass] : (reset ? 0u : ly.ctl->sort_cur);
 }
 
-// Per-tile digit histogram, stored digit-major, hist[digit * stride + tile]
-// (stride = hist_stride(tiles)), for scatters that read a digit's row, or
-// tile-major, hist[tile * 256 + digit], for the scan kernel (coalesced over
-// digits).  A thread's keys are loaded together (indices past n reread the
+// Per-tile digit histogram, stored digit-major with 16-bit counts (a tile
+// holds at most 4,096 of a digit), hist16[digit * stride + tile] (stride =
+// hist_stride(tiles); the last tile zeroes the row's padding), for
+// scatters that read a digit's row, or tile-major with 32-bit counts,
+// hist[tile * 256 + digit], for the scan kernel (coalesced over digits).  A thread's keys are loaded together (indices past n reread the
 // last key and are not counted), so the tile costs one memory round trip.
 // Pass 0 also records the sort's start buffer.
 template <bool DIGIT_MAJOR>
@@ -59,7 +60,14 @@ __global__ void __launch_bounds__(SORT_THREADS) k_hist(Layout ly, uint64_t n, in
     for (uint32_t u = 0; u < SORT_PER; u++)
         if (base + u * SORT_THREADS + tid < n) atomicAdd(&cnt[dg[u]], 1u);
     __syncthreads();
-    ly.hist[DIGIT_MAJOR ? (uint64_t)tid * hist_stride(tiles) + tile : (uint64_t)tile * 256 + tid] = cnt[tid];
+    if (DIGIT_MAJOR) {
+        uint16_t *row = reinterpret_cast<uint16_t *>(ly.hist) + (uint64_t)tid * hist_stride(tiles);
+        row[tile] = (uint16_t)cnt[tid];
+        if (tile == tiles - 1)
+            for (uint32_t t = tiles; t < hist_stride(tiles); t++) row[t] = 0;
+    } else {
+        ly.hist[(uint64_t)tile * 256 + tid] = cnt[tid];
+    }
 }
 
 // Sorts of more than OWN_PREFIX_TILES tiles scan the histogram in a kernel
@@ -108,8 +116,40 @@ __global__ void __launch_bounds__(256 * SCAN_SPLIT) k_scan(Layout ly, uint64_t n
     }
 }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// A digit's counts over the tiles before `tile` and over all tiles, from its
+// 16-bit row of nq 16-byte words (8 tiles each, padding zero).  All N loads
+// are issued before any is used (indices past the row reread its last word
+// and are not counted), so the row costs one memory round trip.
+template <uint32_t N>
+__device__ inline void row_sums(const uint4 *col, uint32_t nq, uint32_t tile, uint32_t &before, uint32_t &total)
+{
+    const u16x2 ones = {1, 1};
+    uint4 v[N];
+#pragma unroll
+    for (uint32_t q = 0; q < N; q++) v[q] = col[min(q, nq - 1)];
+#pragma unroll
+    for (uint32_t q = 0; q < N; q++) {
+        const uint32_t w[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+        uint32_t sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; i++) sum = __builtin_amdgcn_udot2(__builtin_bit_cast(u16x2, w[i]), ones, sum, false);
+        const uint32_t t = 8 * q;
+        total += q < nq ? sum : 0u;
+        uint32_t part = 0;  // counts of the tiles before `tile` among these 8 (a uniform branch)
+        if (t + 8 <= tile) {
+            part = sum;
+        } else if (t < tile) {
+#pragma unroll
+            for (uint32_t i = 0; i < 8; i++) part += t + i < tile ? (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu : 0u;
+        }
+        before += q < nq ? part : 0u;
+    }
+}
+
 // Stable scatter of one tile.  Thread tid owns digit tid: it reads the
-// digit's histogram row (16-byte loads, issued with the tile's keys) and
+// digit's 16-bit histogram row (16-byte loads, issued with the tile's keys) and
 // sums the counts of the tiles before this one and of all tiles; a
 // wave-level scan of the totals over digits gives the digit's base, so the
 // tile's first destination for the digit is base + earlier tiles' count.
@@ -129,7 +169,6 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
                                                           uint32_t pass)
 {
     constexpr uint32_t NW = SORT_THREADS / 64;
-    constexpr uint32_t COL_UNROLL = 32;  // 16-byte histogram loads in flight per thread
     __shared__ uint32_t off[SORT_PER][NW][256];  // counts, then offsets, per (step, wave, digit)
     __shared__ uint32_t wsum[NW];
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, tile = blockIdx.x;
@@ -154,18 +193,17 @@ __global__ void __launch_bounds__(SORT_THREADS) k_scatter(Layout ly, uint64_t n,
     }
     // digit tid over the tiles: before this one, and all
     const uint32_t hs = hist_stride(tiles);
-    const uint4 *col = reinterpret_cast<const uint4 *>(ly.hist + (uint64_t)tid * hs);
     uint32_t before = 0, total = 0;
-    if (!OWN_PREFIX) before = ly.hist[(uint64_t)tile * 256 + tid];
-#pragma unroll COL_UNROLL
-    for (uint32_t q = 0; q < (OWN_PREFIX ? hs / 4 : 0u); q++) {
-        const uint4 v = col[q];
-        const uint32_t t = 4 * q;
-        const uint32_t x0 = t < tiles ? v.x : 0u, x1 = t + 1 < tiles ? v.y : 0u;
-        const uint32_t x2 = t + 2 < tiles ? v.z : 0u, x3 = t + 3 < tiles ? v.w : 0u;
-        total += x0 + x1 + x2 + x3;
-        before += (t < tile ? x0 : 0u) + (t + 1 < tile ? x1 : 0u) + (t + 2 < tile ? x2 : 0u) +
-                  (t + 3 < tile ? x3 : 0u);
+    if (OWN_PREFIX) {
+        const uint4 *col =
+            reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(ly.hist) + (uint64_t)tid * hs);
+        static_assert(OWN_PREFIX_TILES <= 256, "a row is at most 32 loads");
+        if (hs <= 64)
+            row_sums<8>(col, hs / 8, tile, before, total);
+        else
+            row_sums<32>(col, hs / 8, tile, before, total);
+    } else {
+        before = ly.hist[(uint64_t)tile * 256 + tid];
     }
 #pragma unroll
     for (uint32_t u = 0; u < SORT_PER; u++)
