@@ -129,6 +129,8 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     sz.WN = words(c->N);
     sz.max_sends = max_sends;
     sz.tmin = c->tmin;
+    const uint64_t hb = (uint64_t)sz.D * sz.Wp * sizeof(uint64_t);
+    sz.hbytes = hb < (1ull << 31) ? (uint32_t)hb : 0u;
     const uint64_t nsort = std::max<uint64_t>(c->C, max_sends);
     sz.max_tiles = (uint32_t)((nsort + SORT_TILE - 1) / SORT_TILE);
     if (sz.max_tiles == 0) sz.max_tiles = 1;
@@ -674,7 +676,8 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     int lds_cu = 0;
     HIP_OR_FAIL(c, hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, c->device));
     const size_t lds_static = match_static_lds(), row_bytes = (size_t)c->sz.Wp * sizeof(uint64_t);
-    for (int w = wpb; w >= 1 && lds_static > 0; w--) {
+    // (that kernel reads the holds rows through one buffer descriptor)
+    for (int w = wpb; w >= 1 && lds_static > 0 && c->sz.hbytes > 0; w--) {
         const size_t dyn = (size_t)w * row_bytes;
         if (lds_static + dyn > (size_t)lds_cu) continue;
         const int gmax = std::min<int>(match_max_grid(c->device, w, true, dyn), (int)MAX_MATCH_GRID);

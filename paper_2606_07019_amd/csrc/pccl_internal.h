@@ -156,6 +156,7 @@ struct Sizes {
     uint64_t max_sends;
     uint32_t tmin; // smallest link time (window length)
     uint32_t max_tiles;
+    uint32_t hbytes;  // bytes of the holds bitmap (D rows of Wp words) when below 2 GiB, else 0
 };
 
 // ---- launchers (each defined in the translation unit that holds its kernels)

@@ -190,6 +190,21 @@ __device__ inline uint32_t first4(uint4 a)
 
 __device__ inline bool any4(uint4 a) { return (a.x | a.y | a.z | a.w) != 0u; }
 
+// Two words of the holds bitmap at word index w (row * Wp + word), read with
+// the cache policy of an agent-scope atomic load (sc1): coherent with the
+// folds other workgroups make, so the kernel that reads holds rows only this
+// way needs no cache invalidation after each window exchange.  The buffer
+// descriptor spans the bitmap (`bytes`, below 2 GiB); a read past its end
+// returns zeros.
+constexpr int BUF_RSRC_WORD3 = 0x00020000;  // gfx9 buffer descriptor: 32-bit data format, raw access
+constexpr int CPOL_SC1 = 16;                // cache policy bit sc1
+__device__ __forceinline__ uint4 holds_load4(const uint64_t *holds, uint32_t bytes, uint32_t w)
+{
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t *>(holds), (short)0, (int)bytes, BUF_RSRC_WORD3);
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)(w * 8u), 0, CPOL_SC1));
+}
+
 // Bitset intersect + select for one link, by a whole wave: the first set bit
 // at position >= cur of holds[src] & needs[dst], in priority order.  Each
 // lane loads 16 bytes of each row per sweep (four sweeps in flight, 8 KiB
@@ -200,7 +215,8 @@ __device__ inline bool any4(uint4 a) { return (a.x | a.y | a.z | a.w) != 0u; }
 // With the needs row in LDS (MIRROR) only the holds words are loaded, and
 // twice as many sweeps are in flight per round trip.
 template <bool MIRROR>
-__device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
+__device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ holds, uint32_t hbytes,
+                                                         const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
                                                          uint32_t cur, uint64_t Ws, uint64_t &words)
 {
     constexpr uint32_t SW = MIRROR ? SWEEPS_LDS : SWEEPS;
@@ -213,10 +229,11 @@ __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restr
             // every load is issued before any is used (a load past the row
             // end reads its last piece and is masked out)
             uint4 hv[SW];
+            const uint32_t hrow = (uint32_t)(h - holds);
 #pragma unroll
             for (uint32_t u = 0; u < SW; u++) {
                 const uint32_t idx = wb + 128 * u + 2 * lane;
-                hv[u] = *reinterpret_cast<const uint4 *>(h + min(idx, wp - 2u));
+                hv[u] = holds_load4(holds, hbytes, hrow + min(idx, wp - 2u));
             }
 #pragma unroll
             for (uint32_t u = 0; u < SW; u++) {
@@ -266,8 +283,11 @@ __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restr
 // snapshot entries and the holds folds) are agent-scope atomics, coherent
 // without an L2 write-back; every wave waits for their completion before the
 // workgroup barrier, so they are performed before the slots are written.
-// After the wait, an acquire fence makes this compute unit's later plain
-// loads miss any line cached before the other workgroups wrote it.
+// After the wait, the kernel that keeps needs rows in device memory takes an
+// agent-scope acquire fence, so that its later plain loads miss any line
+// cached before the other workgroups wrote it; the kernel with needs rows in
+// LDS reads holds rows and snapshot entries only with coherent loads (the
+// sc1 cache policy) and skips that cache invalidation.
 struct Exchange {
     uint32_t tn;              // start of the next window (earliest transfer end), NONE32 if none
     uint32_t err;             // some workgroup recorded an error
@@ -300,6 +320,7 @@ __device__ void window_publish(uint64_t *xslot, uint32_t gen, uint32_t tmin, uns
 }
 
 // Second half: wait for every workgroup's slots and reduce them.
+template <bool COHERENT>
 __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint32_t gen, Exchange &ex)
 {
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
@@ -347,8 +368,11 @@ __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint
             }
             __builtin_amdgcn_s_sleep(1);
         }
-        // acquire: this compute unit's caches drop lines other workgroups wrote
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        // acquire: this compute unit's caches drop lines other workgroups
+        // wrote; a kernel that reads those lines only with coherent loads
+        // orders its later loads after the wait without that invalidation
+        if constexpr (COHERENT) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        else __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         tn = wave_min(tn);
         e = __ballot(e != 0) ? 1u : 0u;
         s = wave_sum64(s);
@@ -471,7 +495,8 @@ struct LookAhead {
 };
 
 template <bool MIRROR>
-__device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, uint64_t Ws, const WaveShared &ws,
+__device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint32_t hbytes, uint64_t Wp, uint64_t Ws,
+                                                 const WaveShared &ws,
                                                  const Dest &ds, const uint64_t *nd, bool mine, uint32_t n_arr,
                                                  uint32_t n_unf, LookAhead &la)
 {
@@ -489,7 +514,8 @@ __device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint64_t Wp, 
     for (uint32_t u = 0; u < LA_WORDS / 2; u++) {
         const uint64_t idx = pos + 2 * u;
         if (idx < Ws) {
-            la.hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
+            if constexpr (MIRROR) la.hv[u] = holds_load4(ly.holds, hbytes, (uint32_t)(ds.src * Wp + idx));
+            else la.hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
             if constexpr (!MIRROR) la.nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
         } else {
             la.hv[u] = make_uint4(0, 0, 0, 0);
@@ -559,6 +585,16 @@ __device__ __forceinline__ void look_ahead_finish(uint64_t Ws, WaveShared &ws, D
     wave_sync();
 }
 
+// A snapshot entry another workgroup wrote: with COHERENT, an agent-scope
+// atomic load (the kernel that reads this way invalidates no caches after the
+// window exchange), else a plain load after the exchange's acquire fence.
+template <bool COHERENT>
+__device__ __forceinline__ uint64_t snap_load(const uint64_t *p)
+{
+    if constexpr (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else return *p;
+}
+
 // All events of window [t0, t1) for one destination, by one wavefront.
 template <bool MIRROR>
 __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws, Dest &ds, uint32_t k,
@@ -588,7 +624,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         if (resident) {
             r = ds.fold;
         } else if (k >= 2) {
-            const uint64_t e = snap2[sl];
+            const uint64_t e = snap_load<MIRROR>(&snap2[sl]);
             if (e != NONE64 && (uint32_t)e < t0) r = (uint32_t)(e >> 32);
         }
         if (r != NONE32)
@@ -615,8 +651,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         e2[u] = NONE64;
         const uint32_t pr = ds.pair[u];
         if (k >= 1 && pr != NONE32) {
-            e1[u] = snap1[pr >> 8];
-            if (k >= 2 && !carry) e2[u] = snap2[pr >> 8];
+            e1[u] = snap_load<MIRROR>(&snap1[pr >> 8]);
+            if (k >= 2 && !carry) e2[u] = snap_load<MIRROR>(&snap2[pr >> 8]);
         }
     }
     // the look-ahead issued at the end of the last window
@@ -769,7 +805,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
                     const uint64_t idx = pos + 2 * u;
                     if (idx < Ws) {
-                        hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
+                        if constexpr (MIRROR) hv[u] = holds_load4(ly.holds, sz.hbytes, (uint32_t)(ds.src * Wp + idx));
+                        else hv[u] = *reinterpret_cast<const uint4 *>(h + idx);
                         nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
                     } else {
                         hv[u] = make_uint4(0, 0, 0, 0);
@@ -814,12 +851,14 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 uint32_t j = 0;
                 uint64_t gw0 = 0, gpos = 0, gstart = 0;
                 const uint64_t *hj = ly.holds;
+                uint32_t hjrow = 0;
                 if (act) {
                     j = ws.seg_j[g];
                     const uint32_t cj = ws.cur[j];
                     gw0 = cj >> 6;
                     gpos = gstart = ws.seg_pos[j];
-                    hj = ly.holds + (uint64_t)ws.src[j] * Wp;
+                    hjrow = (uint32_t)(ws.src[j] * Wp);
+                    hj = ly.holds + hjrow;
                 }
                 bool live = act;
                 uint32_t gp = NONE32;
@@ -833,7 +872,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                         for (uint32_t u = 0; u < PROBE_WORDS / 2; u++) {
                             const uint64_t idx = base + 2 * u;
                             if (idx < Ws) {
-                                hv[u] = *reinterpret_cast<const uint4 *>(hj + idx);
+                                if constexpr (MIRROR) hv[u] = holds_load4(ly.holds, sz.hbytes, hjrow + (uint32_t)idx);
+                                else hv[u] = *reinterpret_cast<const uint4 *>(hj + idx);
                                 nv[u] = *reinterpret_cast<const uint4 *>(nd + idx);
                             } else {
                                 hv[u] = make_uint4(0, 0, 0, 0);
@@ -882,7 +922,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 const uint32_t sj = readlane32(ds.src, (uint32_t)j);
                 const uint32_t from = max((uint32_t)(readlane64(pos, (uint32_t)j) * 64), ws.cur[j]);
                 uint64_t w = 0;
-                const uint32_t pj = wave_first_candidate<MIRROR>(ly.holds + (uint64_t)sj * Wp, nd, from, Ws, w);
+                const uint32_t pj =
+                    wave_first_candidate<MIRROR>(ly.holds, sz.hbytes, ly.holds + (uint64_t)sj * Wp, nd, from, Ws, w);
                 if ((int)lane == j) p = pj;
                 acc.words += w;
             }
@@ -1057,7 +1098,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         t_prev = t;
     }
 
-    look_ahead_issue<MIRROR>(ly, Wp, Ws, ws, ds, nd, mine, n_arr, n_unf, la);
+    look_ahead_issue<MIRROR>(ly, sz.hbytes, Wp, Ws, ws, ds, nd, mine, n_arr, n_unf, la);
     ds.n_arr_prev = n_arr;
     if (!resident) look_ahead_finish<MIRROR>(Ws, ws, ds, nd, mine, la);
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
@@ -1144,7 +1185,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         Exchange ex;
         window_publish(ly.xslot, (uint32_t)k, bmin, bsent, berr);
-        if (!window_wait(ctl, ly.xslot, sh, (uint32_t)k, ex)) break;
+        if (!window_wait<MIRROR>(ctl, ly.xslot, sh, (uint32_t)k, ex)) break;
         remaining -= ex.sent;
         if (ex.err || remaining == 0) break;
         if (ex.tn == NONE32) {
