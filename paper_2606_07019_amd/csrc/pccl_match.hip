@@ -1125,7 +1125,9 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     const unsigned long long max_windows = ctl->needs_total + 2ull;
     // every wave owns at most one destination: its state stays on chip
     const bool resident = sz.D <= nwaves;
-    if (MIRROR && !resident) {
+    // (the host picks that kernel only with one destination per wave and a
+    // holds bitmap the buffer descriptor spans)
+    if (MIRROR && (!resident || sz.hbytes == 0)) {
         if (blockIdx.x == 0 && tid == 0) record_error(ctl, ST_EINTERNAL, 2, 0, 0);
         return;
     }
