@@ -55,6 +55,7 @@ struct pccl_ctx {
     Layout ly{};
     Sizes sz{};
     int grid = 0, wpb = 0;  // matching kernel: workgroups, waves per workgroup
+    uint32_t alone = 0;     // heaviest destinations dealt to a workgroup of their own
     bool mirror = false;    // matching kernel keeps each destination's needs row in LDS
     // stage timing; ev[1] also marks that the setup's counts have reached `pin`
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
@@ -408,8 +409,13 @@ void deal_destinations(pccl_ctx *c)
     });
     const uint32_t passes = (D + nw - 1) / nw;
     c->wave_dest.assign((size_t)std::max(passes, 1u) * nw, NONE32);
-    for (uint32_t i = 0; i < D; i++) {
-        const uint32_t r = i / nw, j = i % nw, w = (j % nb) * wpb + j / nb;
+    // the `alone` heaviest take wave 0 of the first workgroups (one pass,
+    // by construction of the grid), the others are dealt over the rest
+    const uint32_t h = c->alone, nb2 = nb - h;
+    for (uint32_t i = 0; i < h; i++) c->wave_dest[(size_t)i * wpb] = byweight[i];
+    for (uint32_t i = h; i < D; i++) {
+        const uint32_t q = i - h, n2 = nb2 * wpb;
+        const uint32_t r = q / n2, j = q % n2, w = (h + j % nb2) * wpb + j / nb2;
         c->wave_dest[(size_t)r * nw + w] = byweight[i];
     }
 }
@@ -689,9 +695,26 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     }
     c->wpb = wpb;
     const size_t dyn = c->mirror ? (size_t)wpb * row_bytes : 0;
-    c->grid = std::min<int>(std::min<int>(match_max_grid(c->device, wpb, c->mirror, dyn), (int)MAX_MATCH_GRID),
-                            (int)((D1 + wpb - 1) / wpb));
+    const int gmax = std::min<int>(match_max_grid(c->device, wpb, c->mirror, dyn), (int)MAX_MATCH_GRID);
+    c->grid = std::min<int>(gmax, (int)((D1 + wpb - 1) / wpb));
     if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+    // destinations with at least four times the mean arrival pairs get a
+    // workgroup (so a compute unit) of their own when the grid has room for
+    // it and every other destination still gets a wave: their wave then has
+    // the unit's memory pipeline and LDS to itself
+    c->alone = 0;
+    if (wpb > 1 && c->D > 0) {
+        uint64_t tot = 0;
+        for (uint32_t v = 0; v < c->D; v++) tot += c->dest_pairs[v];
+        uint32_t h = 0;
+        for (uint32_t v = 0; v < c->D; v++)
+            if ((uint64_t)c->dest_pairs[v] * c->D >= 4 * tot && c->dest_pairs[v] > 0) h++;
+        const uint64_t g = h + ((uint64_t)c->D - h + wpb - 1) / wpb;
+        if (h > 0 && g <= (uint64_t)gmax) {
+            c->alone = h;
+            c->grid = (int)g;
+        }
+    }
     deal_destinations(c);
     if (c->sw_active) {
         c->sw_grid = std::min<int>(std::min<int>(match_sw_max_grid(c->device), (int)MAX_MATCH_GRID),
