@@ -408,6 +408,7 @@ struct Dest {
     uint32_t ready_c;           // that candidate while it is valid (NONE32 when not kept)
     uint32_t fold;              // chunk delivered into d in the previous window, still to fold
     uint32_t n_arr_prev;        // length of the previous window's arrival list (kept in LDS)
+    uint32_t n_unf_prev;        // length of the previous window's list of unfolded arrivals
     unsigned long long log;     // next send-log slot of d
     // arrival pairs p = 64 u + lane: slot of the source's in-link, and the
     // in-link of d it feeds (slot << 8 | j; NONE32 past the last pair)
@@ -432,6 +433,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
     ds.ready_c = NONE32;
     ds.fold = NONE32;
     ds.n_arr_prev = 0;
+    ds.n_unf_prev = 0;
     if (lane < ds.n) {
         const uint32_t sl = ds.base + lane;
         ds.src = ly.slot_src[sl];
@@ -1098,13 +1100,35 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
         t_prev = t;
     }
 
-    look_ahead_issue<MIRROR>(ly, sz.hbytes, Wp, Ws, ws, ds, nd, mine, n_arr, n_unf, la);
+    // a resident wave issues the look-ahead after the window exchange is
+    // published (look_ahead_late), so the publish does not wait for it
+    if (!resident) look_ahead_issue<MIRROR>(ly, sz.hbytes, Wp, Ws, ws, ds, nd, mine, n_arr, n_unf, la);
     ds.n_arr_prev = n_arr;
+    ds.n_unf_prev = n_unf;
     if (!resident) look_ahead_finish<MIRROR>(Ws, ws, ds, nd, mine, la);
     acc.tmin = min(acc.tmin, wave_min(mine && ds.infl != NONE32 ? ds.busy : NONE32));
     ds.log += n_send;
     acc.sent += n_send;
     wave_sync();
+}
+
+// The look-ahead of a resident wave, issued once its workgroup has published
+// the window: its loads travel during the exchange instead of delaying the
+// publish.  Holds rows read this late hold at most the arrivals of the window
+// just ended beyond what they held at its end (other workgroups fold those at
+// the start of the next window), and the window's arrival lists, which the
+// look-ahead adds, contain them already; so the result is the same.
+template <bool MIRROR>
+__device__ __forceinline__ void look_ahead_late(const Layout &ly, const Sizes &sz, const WaveShared &ws,
+                                                const Dest &ds, LookAhead &la)
+{
+    if (ds.n == 0) return;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint64_t Wp = sz.Wp, Ws = (sz.W + 1) & ~1ull;
+    const uint64_t *nd;
+    if constexpr (MIRROR) nd = needs_lds + (uint64_t)(threadIdx.x >> 6) * Wp;
+    else nd = ly.needs + (uint64_t)ds.d * Wp;
+    look_ahead_issue<MIRROR>(ly, sz.hbytes, Wp, Ws, ws, ds, nd, lane < ds.n, ds.n_arr_prev, ds.n_unf_prev, la);
 }
 
 // MIRROR: every wave owns one destination for the whole run and keeps its
@@ -1187,6 +1211,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         Exchange ex;
         window_publish(ly.xslot, (uint32_t)k, bmin, bsent, berr);
+        if (resident && mine_d != NONE32) look_ahead_late<MIRROR>(ly, sz, ws, ds, la);
         if (!window_wait<MIRROR>(ctl, ly.xslot, sh, (uint32_t)k, ex)) break;
         remaining -= ex.sent;
         if (ex.err || remaining == 0) break;
