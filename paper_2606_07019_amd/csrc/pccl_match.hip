@@ -302,8 +302,9 @@ struct BlockShared {
     Exchange ex;
 };
 
-// First half: publish this workgroup's slots once every wave's writes and
-// atomics of the window have completed.
+// First half: publish this workgroup's slot.  Called by every thread after
+// the workgroup barrier that follows each wave's wait for the completion of
+// its writes and atomics of the window.
 constexpr uint64_t XTAG_MASK = 0xFFFull << 52;
 static_assert((uint64_t)MAX_DEVICES_SP * MAX_IN_LINKS < (1u << 19), "a window's transfers fit in 19 bits");
 
@@ -311,8 +312,6 @@ __device__ void window_publish(uint64_t *xslot, uint32_t gen, uint32_t tmin, uns
 {
     const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFu) << 52;
     uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    __syncthreads();
     if (threadIdx.x == 0)
         __hip_atomic_store(&slot[(uint64_t)blockIdx.x * XSLOT_WORDS],
                            tag | ((uint64_t)(err ? 1u : 0u) << 51) | ((uint64_t)(sent & 0x7FFFFu) << 32) | tmin,
@@ -1201,6 +1200,9 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
             sh.red_err[wave] = acc.err;
             sh.red_sent[wave] = acc.sent - sent0;
         }
+        // the window's writes and atomics of this wave are performed before
+        // the barrier, so the slot written after it publishes all of them
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
         __syncthreads();
         uint32_t bmin = NONE32, berr = 0;
         unsigned long long bsent = 0;
