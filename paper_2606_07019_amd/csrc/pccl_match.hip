@@ -1213,7 +1213,18 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         Exchange ex;
         window_publish(ly.xslot, (uint32_t)k, bmin, bsent, berr);
-        if (resident && mine_d != NONE32) look_ahead_late<MIRROR>(ly, sz, ws, ds, la);
+        if (resident && mine_d != NONE32) {
+            look_ahead_late<MIRROR>(ly, sz, ws, ds, la);
+            // waves that do not poll the exchange finish it while they wait
+            // (it reads nothing the exchange changes); the call at the next
+            // window's start then finds nothing left to do
+            if (wave != 0 && ds.n > 0) {
+                const uint64_t *nd;
+                if constexpr (MIRROR) nd = needs_lds + (uint64_t)wave * sz.Wp;
+                else nd = ly.needs + (uint64_t)ds.d * sz.Wp;
+                look_ahead_finish<MIRROR>((sz.W + 1) & ~1ull, ws, ds, nd, lane < ds.n, la);
+            }
+        }
         if (!window_wait<MIRROR>(ctl, ly.xslot, sh, (uint32_t)k, ex)) break;
         remaining -= ex.sent;
         if (ex.err || remaining == 0) break;
