@@ -105,6 +105,55 @@ def test_priority_longest_condition_goes_first():
     assert r.collective_time == 2 * T
 
 
+# ---------------------------------------------------------------- tree parent on ties
+@pytest.mark.parametrize("pairs", [[(0, 1), (0, 2), (1, 3), (2, 3)],
+                                   [(0, 2), (0, 1), (2, 3), (1, 3)]])
+def test_parent_tie_smallest_device_id(pairs):
+    # Diamond 0 -> {1, 2} -> 3 with equal link times; process group {0, 3},
+    # one chunk 0 -> 3.  Both two-hop paths are shortest (Alg. 3
+    # ShortestPath); the path-filtering step of Sec. 4.3 keeps one tree path,
+    # the one through the smaller device id, so NPU 1 relays and NPU 2 never
+    # sees the chunk.  The second link order puts the links of device 2
+    # first, so a rule keyed on link order instead of device id fails.
+    topo = W.make_topology(4, 0, pairs, 3, 1)
+    coll = single_chunk(4, 0, [3], chunk_bytes=2, members=[0, 3])
+    r = run(wl_of(topo, coll))
+    T = 5
+    l01 = pairs.index((0, 1))
+    l13 = pairs.index((1, 3))
+    np.testing.assert_array_equal(r.sends[np.lexsort((r.sends[:, 0], r.sends[:, 2]))],
+                                  [[l01, 0, 0, 0], [l13, 0, T, 0]])
+    assert r.collective_time == 2 * T
+
+
+def _assert_uplink_first(topo, sends, per_node, n_npus):
+    # Rail cluster All-to-All, chunk c = n i + j from NPU i to NPU j.  For
+    # j in another node and with another local index, the paths i -> switch
+    # (local i) -> (node j, local i) -> j and i -> (node i, local j) ->
+    # switch (local j) -> j take the same time; the smallest-id tight parent
+    # of j is the NPU (node j, local i), not the switch (switch ids follow
+    # every NPU), so every chunk goes up its source's own rail first.
+    src, dst = topo.src[sends[:, 0]].astype(np.int64), topo.dst[sends[:, 0]].astype(np.int64)
+    up = dst >= n_npus
+    chunk_src = sends[:, 1].astype(np.int64) // n_npus
+    assert up.any()
+    np.testing.assert_array_equal(src[up], chunk_src[up])
+    np.testing.assert_array_equal(dst[up], n_npus + chunk_src[up] % per_node)
+
+
+def test_rail_cluster_routes_uplink_first_small():
+    nodes, per = 4, 4
+    n = nodes * per
+    topo = W.switch2level(nodes, per)
+    wl = wl_of(topo, W.a2a_bitmaps(n, 128 << 10))
+    r = run(wl)
+    check_copy_schedule(wl.topo, wl.coll, r.sends, r.collective_time)
+    _assert_uplink_first(topo, r.sends, per, n)
+    # inter-node chunks cross exactly one uplink each
+    up = topo.dst[r.sends[:, 0]] >= n
+    assert int(up.sum()) == n * (n - per)
+
+
 # ---------------------------------------------------------------- clash rule
 def test_clash_fastest_link_wins():
     # Chunk 0 starts on NPU 0 and must reach {1, 2, 3}.  At t = 1 both 1 and
@@ -207,10 +256,13 @@ def test_config4_structure():
     # (destination node, same local index) -> destination; one holder per
     # in-neighbour, so no clashes, no wasted relays, 745,472 transfers, and
     # each uplink carries 504 chunks of 4,622 ns.
-    r = run(W.config4())
+    wl = W.config4()
+    r = run(wl)
     assert len(r.sends) == 745472
     assert r.stats["clashes"] == 0 and r.stats["wasted"] == 0
     assert r.collective_time >= 504 * 4622
+    # chunk (i, j) enters switch 512 + (i mod 8): the uplink goes first
+    _assert_uplink_first(wl.topo, r.sends, 8, 512)
 
 
 def test_allreduce_is_reversed_then_forward():
