@@ -20,7 +20,7 @@ from . import oracle as O
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "alg3.c")
-LIB = os.path.join(HERE, "libalg3.so")
+LIB = os.path.join(HERE, "libalg3_san.so" if O.SANITIZE else "libalg3.so")
 
 
 class _Send(ctypes.Structure):
@@ -30,7 +30,7 @@ class _Send(ctypes.Structure):
 def build(force: bool = True) -> str:
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, SRC])
+        subprocess.check_call(["gcc"] + O.cflags() + ["-std=c11", "-shared", "-fPIC", "-o", tmp, SRC])
         os.replace(tmp, LIB)
     return LIB
 

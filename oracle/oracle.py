@@ -16,7 +16,18 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "pccl_oracle.c")
-LIB = os.path.join(HERE, "libpccl_oracle.so")
+# PCCL_ORACLE_SANITIZE=1 builds and loads a copy under AddressSanitizer and
+# UndefinedBehaviorSanitizer instead (the process must preload libasan; see
+# tests/test_sanitizers.py)
+SANITIZE = os.environ.get("PCCL_ORACLE_SANITIZE", "") not in ("", "0")
+LIB = os.path.join(HERE, "libpccl_oracle_san.so" if SANITIZE else "libpccl_oracle.so")
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=undefined"]
+
+
+def cflags() -> list:
+    return SAN_FLAGS if SANITIZE else ["-O2"]
+
 
 STATUS = {0: "OK", 1: "EINVAL", 2: "EUNREACHABLE", 3: "ERANGE", 4: "ENOMEM",
           5: "EDEVICE", 6: "ESTATE", 7: "EUNSUPPORTED", 8: "EDEADLOCK", 9: "EINTERNAL"}
@@ -28,7 +39,7 @@ MODE_SKIP_IDLE = 1
 def build(force: bool = True) -> str:
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", tmp, SRC])
+        subprocess.check_call(["gcc"] + cflags() + ["-std=c11", "-shared", "-fPIC", "-o", tmp, SRC])
         os.replace(tmp, LIB)
     return LIB
 
