@@ -25,14 +25,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
-# Algorithmic bytes of the matching kernel, per launch:
-# 16 B per scanned word position (one 8-byte word of the source's holds row
-# and one of the destination's needs row) plus, per committed transfer, the
-# needs-word read-modify-write (16 B), the holds-word fold at arrival (16 B),
-# the send-log record (12 B), the link state written back (16 B) and the
-# snapshot entry (8 B): 68 B.
+# Algorithmic bytes of the matching kernel, per launch: 16 B per scanned
+# word position (one 8-byte word of the source's holds row and one of the
+# destination's needs row) plus 96 B per committed transfer (the two words
+# holding its bit, the needs-word read-modify-write, the holds-word set at
+# arrival, link state, the send record and one atomic).
 BYTES_PER_SCANNED_WORD = 16
-BYTES_PER_MATCH = 68
+BYTES_PER_MATCH = 96
 
 
 COUNTERS = os.path.join(ROOT, "profiles", "k_match_switch2level_512_a2a_hbm_counters.md")
@@ -84,9 +83,43 @@ def cpu_baseline(wl, budget_s: float = 30.0):
             "seconds": dt, "n_sends": len(r.sends), "collective_time_ns": r.collective_time}
 
 
+def end_to_end(wl, Synthesizer, torch, n_expected, runs: int = 5):
+    """Synthesis from host bitmaps to a host schedule: pccl_set_collective
+    (the library copies the host pre/postconditions), pccl_set_workspace,
+    pccl_synthesize (upload, setup, matching, output) and pccl_get_schedule
+    into host memory.  One warm-up, then the median of `runs`; HIP
+    initialisation and module loading are outside (the context exists)."""
+    import numpy as np
+    from paper_2606_07019_amd import pccl as P
+    syn = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed, device=0)
+    c = wl.coll
+    host = np.zeros((n_expected, 4), np.uint32)
+    times = []
+    try:
+        for i in range(runs + 1):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            P.pccl_set_collective(syn.h, c.n_chunks, c.chunk_bytes, c.pre, c.post, c.group_masks,
+                                  c.chunk_group, c.op)
+            P.pccl_set_workspace(syn.h, syn.ws.data_ptr(), syn.ws.numel(), syn.max_sends, syn.stream.cuda_stream)
+            got, _ = P.pccl_synthesize(syn.h)
+            P.pccl_get_schedule(syn.h, host.ctypes.data, got)
+            dt = time.perf_counter() - t0
+            if got != n_expected:
+                raise RuntimeError("end-to-end synthesis gave another schedule size")
+            if i:
+                times.append(dt)
+    finally:
+        syn.close()
+    med = sorted(times)[len(times) // 2]
+    return {"seconds_median": med, "matches_per_s": n_expected / med, "runs": runs,
+            "schedule_bytes_to_host": int(host.nbytes), "bitmap_bytes_from_host": int(c.pre.nbytes + c.post.nbytes),
+            "what": "host pre/post bitmaps -> set_collective + set_workspace + synthesize -> schedule in host memory"}
+
+
 def sweep(args, W, Synthesizer, torch):
     """Synthesis wall time against the number of 128 KiB chunks per pair
-    (the collective-size experiment of Sec. 7) on both 64-NPU topologies."""
+    (the collective-size experiment of Sec. 6.1, Scalability) on both 64-NPU topologies."""
     steps = max(1, min(args.steps, 5))
     points = []
     for name, make in W.SWEEP_TOPOLOGIES.items():
@@ -113,7 +146,7 @@ def sweep(args, W, Synthesizer, torch):
             points.append(pt)
     last = points[-1]
     print(json.dumps({
-        "metric": "synthesis wall time vs chunks per pair, 64-NPU All-to-All (Sec. 7 collective size)",
+        "metric": "synthesis wall time vs chunks per pair, 64-NPU All-to-All (Sec. 6.1 collective size)",
         "value": last["matches_per_s"], "unit": "matches/s", "n_gpus": 1, "steps": steps, "warmup": 1,
         "ms_per_step": last["synthesis_ms"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "u64", "data": "synthetic",
@@ -274,6 +307,7 @@ def main():
                     "paper_topology": "2D Mesh / 3D Hypercube family (not this topology)"},
     }
     syn.close()
+    out["end_to_end"] = end_to_end(wl, Synthesizer, torch, n)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on the same workload ...")
         cb = cpu_baseline(wl)

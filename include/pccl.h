@@ -126,20 +126,26 @@ pccl_status pccl_load_topology(pccl_ctx *ctx, uint32_t n_npus, uint32_t n_switch
  * Sets the collective (paper Sec. 2.1 pre/postconditions, Sec. 2.2 process
  * groups, Sec. 4.1 conditions).
  *   n_chunks, chunk_bytes: C chunks of m bytes each (m >= 1).
- *   pre_bits, post_bits: DEVICE pointers to n_npus rows of ceil(C/64)
- *     uint64 words, LSB first (chunk c is bit c%64 of word c/64).  Row v of
- *     pre holds the chunks NPU v has before the collective, row v of post the
- *     chunks it must have after.  They are read by pccl_synthesize, so they
- *     must stay valid and unchanged until the last synthesize call.
+ *   pre_bits, post_bits: n_npus rows of ceil(C/64) uint64 words, LSB first
+ *     (chunk c is bit c%64 of word c/64), in host or device memory.  Row v
+ *     of pre holds the chunks NPU v has before the collective, row v of post
+ *     the chunks it must have after.
  *   group_masks: HOST pointer to n_groups rows of ceil(n_npus/64) words, the
- *     members of each process group (copied).
- *   chunk_group: DEVICE pointer to C uint16 group ids, or NULL when
+ *     members of each process group.
+ *   chunk_group: C uint16 group ids (host or device memory), or NULL when
  *     n_groups == 1.
- * Checked here: sizes and group masks (PCCL_EINVAL).  Checked on the device
- * by pccl_synthesize (PCCL_EINVAL): each chunk with a postcondition bit has
- * exactly one precondition holder, no chunk has two holders, pre/post bits
- * only at members of the chunk's group, no bits beyond chunk C-1, group ids
- * in range.  A link time alpha + ceil(m / bw) above 2^32-1 gives PCCL_ERANGE.
+ * Every array is copied before the call returns (the bitmaps into pinned
+ * host memory the context owns, uploaded to the workspace by the next
+ * synthesize call), so the caller may free or reuse them at once.  The call
+ * also plans the device work (matching-kernel launch shape, destination
+ * deal, switch tables); pccl_set_switch_model re-plans by itself when it
+ * comes after.  A previously bound workspace must be bound again.
+ * Checked here: sizes and group masks (PCCL_EINVAL); PCCL_EDEVICE if a
+ * copy fails.  Checked on the device by pccl_synthesize (PCCL_EINVAL): each
+ * chunk with a postcondition bit has exactly one precondition holder, no
+ * chunk has two holders, pre/post bits only at members of the chunk's group,
+ * no bits beyond chunk C-1, group ids in range.  A link time
+ * alpha + ceil(m / bw) above 2^32-1 gives PCCL_ERANGE.
  */
 pccl_status pccl_set_collective(pccl_ctx *ctx, uint32_t n_chunks, uint64_t chunk_bytes,
                                 const uint64_t *pre_bits, const uint64_t *post_bits,
@@ -184,7 +190,10 @@ pccl_status pccl_set_switch_model(pccl_ctx *ctx, uint32_t n_switches, const uint
  * Device workspace needed by pccl_synthesize for at most `max_sends`
  * copy-schedule transfers (0 = the safe bound C * (D - 1), D = all devices).
  * The number of copy transfers equals the number of (device, chunk) pairs
- * that must receive the chunk: destinations plus relays.
+ * that must receive the chunk: destinations plus relays.  The bound is an
+ * argument because the send log, the output and the sort buffers (44 bytes
+ * per transfer) scale with it: the safe bound of the 512-NPU All-to-All is
+ * 136 M transfers (6 GB), its exact count 745,472 (33 MB).
  */
 pccl_status pccl_workspace_bytes(pccl_ctx *ctx, uint64_t max_sends, size_t *out_bytes);
 
@@ -192,21 +201,24 @@ pccl_status pccl_workspace_bytes(pccl_ctx *ctx, uint64_t max_sends, size_t *out_
  * Hands over the device workspace (caller-owned, 256-byte aligned, at least
  * the size pccl_workspace_bytes returned for `max_sends`) and the HIP stream
  * to run on (NULL = the default stream).  The library allocates no device
- * memory of its own (a context holds one small pinned host block, from its
- * first synthesize call, for reading the device's counters).  The workspace must not be used by the caller while a
+ * memory of its own (a context holds pinned host memory: the copies of the
+ * inputs and of its small tables, and a 2 x 160-byte block for reading the
+ * device's counters).  The workspace must not be used by the caller while a
  * synthesize call runs.  PCCL_ENOMEM if `bytes` is too small.
  */
 pccl_status pccl_set_workspace(pccl_ctx *ctx, void *device_ptr, size_t bytes,
                                uint64_t max_sends, void *hip_stream);
 
 /*
- * Runs the whole synthesis on the device and waits for it: conditions,
- * shortest-path distances and relay devices (Alg. 3 distances; the
- * path-filtering step after Alg. 2), priority order (Alg. 3), the
- * event-stepped link-parallel matching (the BFS step of Alg. 2 applied to all
- * free links at once; link exclusivity of Sec. 4.4 and 4.6; chunk arrival
- * times of Sec. 4.6; NextAvailableTime of Alg. 1), and the canonical schedule
- * (sorted by start time, then link id; reversed for reduction ops).
+ * Runs the whole synthesis on the device and waits for it: the copy of the
+ * inputs into the workspace (on the first call after pccl_set_collective or
+ * pccl_set_workspace), conditions, shortest-path distances and relay devices
+ * (Alg. 3 distances; the path-filtering step after Alg. 2), priority order
+ * (Alg. 3), the event-stepped link-parallel matching (the BFS step of Alg. 2
+ * applied to all free links at once; link exclusivity of Sec. 4.4 and 4.6;
+ * chunk arrival times of Sec. 4.6; NextAvailableTime of Alg. 1), and the
+ * canonical schedule (sorted by start time, then link id; reversed for
+ * reduction ops).  Allocates nothing.
  * Outputs the number of sends and the collective time (latest transfer end).
  * The schedule stays in the workspace until the next synthesize call.
  * PCCL_ENOMEM if the collective needs more than max_sends transfers.
@@ -264,7 +276,10 @@ pccl_status pccl_export_program(pccl_ctx *ctx, pccl_step *steps, uint64_t step_c
  *              every transfer end up to the last transfer start),
  *   rounds  -- (event, destination) pick rounds that made at least one pick,
  *   clashes -- picks that lost a (destination, chunk) clash,
- *   windows -- synchronous look-ahead windows the device loop ran.
+ *   windows -- synchronous look-ahead windows the device loop ran (the
+ *              device's own step count: events inside one window of the
+ *              smallest link time need no grid-wide exchange, so this is
+ *              what bounds the matching time, not `events`).
  * Any pointer may be NULL.
  */
 pccl_status pccl_get_stats(pccl_ctx *ctx, uint64_t *events, uint64_t *rounds,

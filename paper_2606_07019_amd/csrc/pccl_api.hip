@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <exception>
+#include <mutex>
 #include <numeric>
 #include <string>
 #include <unordered_map>
@@ -27,11 +28,13 @@ struct pccl_ctx {
     std::vector<uint32_t> src, dst, alpha, bw;
     std::vector<uint32_t> in_off, slot_link, slot_src, slot_cum, dest_pairs, rev;
     std::vector<uint32_t> wave_dest;  // destination of (pass, wave) in the matching kernel
-    // collective
+    // collective; the pre/post bitmaps and chunk groups are copied into
+    // `pin_in` (pinned host memory: pre, then post, then the group ids)
     uint32_t C = 0, G = 0;
     uint64_t m = 0;
-    const uint64_t *pre = nullptr, *post = nullptr;
-    const uint16_t *chunk_group = nullptr;
+    bool multi_group = false;
+    char *pin_in = nullptr;
+    size_t pin_in_cap = 0;
     std::vector<uint64_t> gmask;
     int op = 0;
     std::vector<uint32_t> T, slot_time;
@@ -39,7 +42,7 @@ struct pccl_ctx {
     // switch model (Sec. 4.7)
     std::vector<uint32_t> sw_buf;  // per switch: buffer capacity, 0 = unlimited
     std::vector<uint8_t> sw_uni;   // per switch: 1 = no multicast
-    bool sw_model = false;         // some switch has a limit
+    bool sw_model = false;         // some switch has a limit or no multicast
     bool sw_built = false;         // tables below match the topology, model and chunk count
     bool sw_active = false;        // the switch-model matching kernel runs
     std::vector<uint32_t> swt;     // switch-model tables, uploaded as one region
@@ -47,8 +50,19 @@ struct pccl_ctx {
     uint64_t swo[18] = {};         // offsets of the tables inside swt (order of SwTab)
     uint32_t sw_groups = 0, sw_pool = 0, sw_nbt = 0;
     int sw_grid = 0;
+    // plan (made once per collective and switch model, before any workspace)
+    bool planned = false;
+    uint64_t plan_gen = 0;         // changes with every plan (static scratch ownership)
+    // pinned host image of the small per-topology arrays the kernels read
+    // (link and slot tables, destination deal, group masks, switch tables),
+    // built by the plan; IMG_PARTS pieces at img_off[k], img_len[k] bytes
+    char *pin_img = nullptr;
+    size_t pin_img_cap = 0;
+    size_t img_off[16] = {}, img_len[16] = {};
+    uint64_t serial = 0;           // unique per context
     // workspace
     char *ws = nullptr;
+    bool ws_static = false;        // the workspace is the library's static scratch
     size_t ws_bytes = 0;
     uint64_t max_sends = 0;
     hipStream_t stream = nullptr;
@@ -58,15 +72,20 @@ struct pccl_ctx {
     uint32_t alone = 0;     // heaviest destinations dealt to a workgroup of their own
     bool mirror = false;    // matching kernel keeps each destination's needs row in LDS
     // stage timing; ev[1] also marks that the setup's counts have reached `pin`
+    // (events and the pinned block are made by pccl_create, so that a
+    // synthesize call allocates nothing)
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     float stage_ms[3] = {0.f, 0.f, 0.f};
     // pinned host copies of the control block: [0] after the setup, [1] at the end
     Control *pin = nullptr;
     ~pccl_ctx()
     {
+        (void)hipSetDevice(device);
         for (hipEvent_t e : ev)
             if (e) (void)hipEventDestroy(e);
         if (pin) (void)hipHostFree(pin);
+        if (pin_in) (void)hipHostFree(pin_in);
+        if (pin_img) (void)hipHostFree(pin_img);
     }
     // results
     std::unordered_map<uint64_t, uint64_t> receipt;  // (chunk << 32 | device) -> (link << 32 | t_start), copy schedule
@@ -149,6 +168,9 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.slot_cum = cv.take<uint32_t>(L);
     ly.dest_pairs = cv.take<uint32_t>(D);
     ly.group_masks = cv.take<uint64_t>((uint64_t)c->G * sz.WN);
+    ly.pre = cv.take<uint64_t>(N * sz.W);
+    ly.post = cv.take<uint64_t>(N * sz.W);
+    ly.chunk_group = c->multi_group ? cv.take<uint16_t>(C) : nullptr;
     ly.chunk_src = cv.take<uint32_t>(C);
     ly.holder_cnt = cv.take<uint32_t>(C);
     ly.chunk_dist = cv.take<uint64_t>(C);
@@ -437,6 +459,147 @@ const char *einval_detail(uint32_t code)
     }
 }
 
+uint64_t row_words(uint32_t C)
+{
+    const uint64_t W = words(C);
+    return std::max<uint64_t>(ROW_ALIGN_WORDS, (W + ROW_ALIGN_WORDS - 1) / ROW_ALIGN_WORDS * ROW_ALIGN_WORDS);
+}
+
+// Pinned host memory of at least `bytes` in *buf (grown, never shrunk).
+pccl_status ensure_pinned(pccl_ctx *c, char **buf, size_t *cap, size_t bytes)
+{
+    if (*cap >= bytes && *buf) return PCCL_OK;
+    if (*buf) {
+        (void)hipHostFree(*buf);
+        *buf = nullptr;
+        *cap = 0;
+    }
+    const size_t n = std::max<size_t>(bytes, 256);
+    HIP_OR_FAIL(c, hipHostMalloc((void **)buf, n, hipHostMallocDefault));
+    *cap = n;
+    return PCCL_OK;
+}
+
+constexpr int IMG_PARTS = 13;
+
+// Everything that depends on the topology, the collective and the switch
+// model but not on the workspace: the switch tables, the matching kernel's
+// launch shape (waves per workgroup, needs rows in LDS, grid), the deal of
+// destinations to waves and the pinned image of the small arrays the kernels
+// read.  Made when the collective or the switch model is set, so that binding
+// a workspace only carves it and a synthesize call allocates nothing.
+pccl_status plan(pccl_ctx *c)
+{
+    c->planned = false;
+    c->have_ws = c->uploaded = c->have_result = false;
+    pccl_status st = build_switch_tables(c);
+    if (st != PCCL_OK) return st;
+    HIP_OR_FAIL(c, hipSetDevice(c->device));
+    const uint64_t Wp = row_words(c->C);
+    const uint64_t hb = (uint64_t)c->D * Wp * sizeof(uint64_t);
+    const bool desc_ok = hb < (1ull << 31);  // the LDS-row kernel reads holds through one buffer descriptor
+    // waves per workgroup: as few as keep the grid near MATCH_TARGET_GRID
+    // workgroups, so that few destinations still spread over many compute
+    // units while many destinations do not make the window exchange poll
+    // too many slots
+    const uint32_t D1 = std::max<uint32_t>(c->D, 1);
+    int wpb = (int)std::min<uint32_t>(MATCH_WAVES, std::max<uint32_t>(1, (D1 + MATCH_TARGET_GRID - 1) / MATCH_TARGET_GRID));
+    // needs rows in LDS: with as many of those waves as leave room for one
+    // row per wave and still give every destination a wave of its own
+    c->mirror = false;
+    int lds_cu = 0;
+    HIP_OR_FAIL(c, hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, c->device));
+    const size_t lds_static = match_static_lds(), row_bytes = (size_t)Wp * sizeof(uint64_t);
+    for (int w = wpb; w >= 1 && lds_static > 0 && desc_ok; w--) {
+        const size_t dyn = (size_t)w * row_bytes;
+        if (lds_static + dyn > (size_t)lds_cu) continue;
+        const int gmax = std::min<int>(match_max_grid(c->device, w, true, dyn), (int)MAX_MATCH_GRID);
+        if (gmax > 0 && (uint64_t)gmax * (uint64_t)w >= D1) {
+            wpb = w;
+            c->mirror = true;
+            break;
+        }
+    }
+    c->wpb = wpb;
+    const size_t dyn = c->mirror ? (size_t)wpb * row_bytes : 0;
+    const int gmax = std::min<int>(match_max_grid(c->device, wpb, c->mirror, dyn), (int)MAX_MATCH_GRID);
+    c->grid = std::min<int>(gmax, (int)((D1 + wpb - 1) / wpb));
+    if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+    // destinations with at least four times the mean arrival pairs get a
+    // workgroup (so a compute unit) of their own when the grid has room for
+    // it and every other destination still gets a wave: their wave then has
+    // the unit's memory pipeline and LDS to itself
+    c->alone = 0;
+    if (wpb > 1 && c->D > 0) {
+        uint64_t tot = 0;
+        for (uint32_t v = 0; v < c->D; v++) tot += c->dest_pairs[v];
+        uint32_t h = 0;
+        for (uint32_t v = 0; v < c->D; v++)
+            if ((uint64_t)c->dest_pairs[v] * c->D >= 4 * tot && c->dest_pairs[v] > 0) h++;
+        const uint64_t g = h + ((uint64_t)c->D - h + wpb - 1) / wpb;
+        if (h > 0 && g <= (uint64_t)gmax) {
+            c->alone = h;
+            c->grid = (int)g;
+        }
+    }
+    deal_destinations(c);
+    if (c->sw_active) {
+        c->sw_grid = std::min<int>(std::min<int>(match_sw_max_grid(c->device), (int)MAX_MATCH_GRID),
+                                   (int)c->sw_groups);
+        if (c->sw_grid <= 0) return fail(c, PCCL_EDEVICE, "switch-model matching kernel cannot be resident");
+        st = deal_switch_groups(c);
+        if (st != PCCL_OK) return st;
+    }
+    // the pinned image, in the order upload() copies it
+    const std::pair<const void *, size_t> parts[IMG_PARTS] = {
+        {c->src.data(), 4ull * c->L},         {c->dst.data(), 4ull * c->L},
+        {c->T.data(), 4ull * c->L},           {c->rev.data(), 4ull * c->L},
+        {c->in_off.data(), 4ull * (c->D + 1)}, {c->slot_link.data(), 4ull * c->L},
+        {c->slot_src.data(), 4ull * c->L},    {c->slot_time.data(), 4ull * c->L},
+        {c->slot_cum.data(), 4ull * c->L},    {c->dest_pairs.data(), 4ull * c->D},
+        {c->wave_dest.data(), 4ull * c->wave_dest.size()},
+        {c->gmask.data(), 8ull * c->gmask.size()},
+        {c->swt.data(), c->sw_active ? 4ull * c->swt.size() : 0ull}};
+    size_t total = 0;
+    for (int k = 0; k < IMG_PARTS; k++) {
+        c->img_off[k] = total;
+        c->img_len[k] = parts[k].second;
+        total += (parts[k].second + 255) & ~size_t(255);
+    }
+    st = ensure_pinned(c, &c->pin_img, &c->pin_img_cap, total);
+    if (st != PCCL_OK) return st;
+    for (int k = 0; k < IMG_PARTS; k++)
+        if (c->img_len[k]) std::memcpy(c->pin_img + c->img_off[k], parts[k].first, c->img_len[k]);
+    c->planned = true;
+    c->plan_gen++;
+    return PCCL_OK;
+}
+
+// Points the context at a workspace: carves the layout for `max_sends`
+// transfers.  The inputs are copied in by the next synthesize call.
+pccl_status bind_workspace(pccl_ctx *c, char *ptr, size_t bytes, uint64_t ms, hipStream_t st, bool is_static)
+{
+    Layout ly{};
+    Sizes sz{};
+    size_t need = 0;
+    carve(c, nullptr, ms, ly, sz, need);
+    if (bytes < need) {
+        if (is_static)
+            return fail(c, PCCL_ENOMEM, "the library's static scratch holds %zu bytes, this collective needs %zu "
+                        "(pass a tighter max_sends, or bring a workspace with pccl_set_workspace)", bytes, need);
+        return fail(c, PCCL_ENOMEM, "workspace has %zu bytes, needs %zu", bytes, need);
+    }
+    carve(c, ptr, ms, c->ly, c->sz, need);
+    c->ws = ptr;
+    c->ws_bytes = bytes;
+    c->max_sends = ms;
+    c->stream = st;
+    c->ws_static = is_static;
+    c->have_ws = true;
+    c->uploaded = c->have_result = false;
+    return PCCL_OK;
+}
+
 }  // namespace
 
 #define GUARD_BEGIN try {
@@ -464,6 +627,14 @@ pccl_status pccl_create(pccl_ctx **out, int hip_device, uint64_t tie_seed)
     pccl_ctx *c = new pccl_ctx();
     c->device = hip_device;
     c->seed = tie_seed;
+    // the stage events and the pinned control-block copies, made here so
+    // that synthesize calls allocate nothing
+    bool ok = hipHostMalloc((void **)&c->pin, 2 * sizeof(Control), hipHostMallocDefault) == hipSuccess;
+    for (hipEvent_t &e : c->ev) ok = ok && hipEventCreate(&e) == hipSuccess;
+    if (!ok) {
+        delete c;
+        return PCCL_EDEVICE;
+    }
     *out = c;
     return PCCL_OK;
     GUARD_END(nullptr)
@@ -544,7 +715,7 @@ pccl_status pccl_load_topology(pccl_ctx *c, uint32_t n_npus, uint32_t n_switches
     c->sw_uni.assign(n_switches, 0u);
     c->sw_model = c->sw_built = c->sw_active = false;
     c->have_topo = true;
-    c->have_coll = c->have_ws = c->uploaded = c->have_result = false;
+    c->have_coll = c->planned = c->have_ws = c->uploaded = c->have_result = false;
     return PCCL_OK;
     GUARD_END(c)
 }
@@ -586,23 +757,34 @@ pccl_status pccl_set_collective(pccl_ctx *c, uint32_t n_chunks, uint64_t chunk_b
             if (c->rev[l] == NONE32 || T[c->rev[l]] != T[l])
                 return fail(c, PCCL_EUNSUPPORTED, "link %u has no reverse link of equal time", l);
     }
+    // the caller's arrays are copied now (host or device memory), so they may
+    // be freed on return
+    const bool multi = n_groups > 1;
+    const size_t bm = (size_t)c->N * words(n_chunks) * sizeof(uint64_t);
+    const size_t cgb = multi ? (size_t)n_chunks * sizeof(uint16_t) : 0;
+    c->have_coll = c->planned = false;
+    c->have_ws = c->uploaded = c->have_result = false;
+    pccl_status st = ensure_pinned(c, &c->pin_in, &c->pin_in_cap, 2 * bm + cgb);
+    if (st != PCCL_OK) return st;
+    HIP_OR_FAIL(c, hipSetDevice(c->device));
+    if (bm) {
+        HIP_OR_FAIL(c, hipMemcpy(c->pin_in, pre_bits, bm, hipMemcpyDefault));
+        HIP_OR_FAIL(c, hipMemcpy(c->pin_in + bm, post_bits, bm, hipMemcpyDefault));
+    }
+    if (cgb) HIP_OR_FAIL(c, hipMemcpy(c->pin_in + 2 * bm, chunk_group, cgb, hipMemcpyDefault));
     std::vector<uint32_t> slot_time(c->L);
     for (uint32_t sl = 0; sl < c->L; sl++) slot_time[sl] = T[c->slot_link[sl]];
     c->C = n_chunks;
     c->m = chunk_bytes;
-    c->pre = pre_bits;
-    c->post = post_bits;
     c->G = n_groups;
-    c->chunk_group = chunk_group;
+    c->multi_group = multi;
     c->gmask.assign(group_masks, group_masks + (size_t)n_groups * WN);
     c->op = op;
     c->T.swap(T);
     c->slot_time.swap(slot_time);
     c->tmin = c->L ? tmin : 1;
     c->have_coll = true;
-    c->sw_built = false;
-    c->have_ws = c->uploaded = c->have_result = false;
-    return PCCL_OK;
+    return plan(c);
     GUARD_END(c)
 }
 
@@ -624,7 +806,7 @@ pccl_status pccl_set_switch_model(pccl_ctx *c, uint32_t n_switches, const uint32
     c->sw_model = any;
     c->sw_built = c->sw_active = false;
     c->have_ws = c->uploaded = c->have_result = false;
-    return PCCL_OK;
+    return c->have_coll ? plan(c) : PCCL_OK;
     GUARD_END(c)
 }
 
@@ -633,10 +815,7 @@ pccl_status pccl_workspace_bytes(pccl_ctx *c, uint64_t max_sends, size_t *out_by
     if (!c || !out_bytes) return PCCL_EINVAL;
     GUARD_BEGIN
     if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
-    if (!c->sw_built) {
-        const pccl_status st = build_switch_tables(c);
-        if (st != PCCL_OK) return st;
-    }
+    if (!c->planned) return fail(c, PCCL_ESTATE, "the last pccl_set_collective / pccl_set_switch_model failed");
     Layout ly{};
     Sizes sz{};
     size_t total = 0;
@@ -652,106 +831,35 @@ pccl_status pccl_set_workspace(pccl_ctx *c, void *device_ptr, size_t bytes, uint
     GUARD_BEGIN
     c->err.clear();
     if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
+    if (!c->planned) return fail(c, PCCL_ESTATE, "the last pccl_set_collective / pccl_set_switch_model failed");
     if (!device_ptr) return fail(c, PCCL_EINVAL, "null workspace");
     if (reinterpret_cast<uintptr_t>(device_ptr) & 255u) return fail(c, PCCL_EINVAL, "workspace not 256-byte aligned");
-    if (!c->sw_built) {
-        const pccl_status st = build_switch_tables(c);
-        if (st != PCCL_OK) return st;
-    }
-    const uint64_t ms = max_sends ? max_sends : safe_max_sends(c);
-    Layout ly{};
-    Sizes sz{};
-    size_t need = 0;
-    carve(c, nullptr, ms, ly, sz, need);
-    if (bytes < need) return fail(c, PCCL_ENOMEM, "workspace has %zu bytes, needs %zu", bytes, need);
-    carve(c, static_cast<char *>(device_ptr), ms, c->ly, c->sz, need);
-    c->ws = static_cast<char *>(device_ptr);
-    c->ws_bytes = bytes;
-    c->max_sends = ms;
-    c->stream = static_cast<hipStream_t>(hip_stream);
-    HIP_OR_FAIL(c, hipSetDevice(c->device));
-    // waves per workgroup: as few as keep the grid near MATCH_TARGET_GRID
-    // workgroups, so that few destinations still spread over many compute
-    // units while many destinations do not make the window exchange poll
-    // too many slots
-    const uint32_t D1 = std::max<uint32_t>(c->D, 1);
-    int wpb = (int)std::min<uint32_t>(MATCH_WAVES, std::max<uint32_t>(1, (D1 + MATCH_TARGET_GRID - 1) / MATCH_TARGET_GRID));
-    // needs rows in LDS: with as many of those waves as leave room for one
-    // row per wave and still give every destination a wave of its own
-    c->mirror = false;
-    int lds_cu = 0;
-    HIP_OR_FAIL(c, hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, c->device));
-    const size_t lds_static = match_static_lds(), row_bytes = (size_t)c->sz.Wp * sizeof(uint64_t);
-    // (that kernel reads the holds rows through one buffer descriptor)
-    for (int w = wpb; w >= 1 && lds_static > 0 && c->sz.hbytes > 0; w--) {
-        const size_t dyn = (size_t)w * row_bytes;
-        if (lds_static + dyn > (size_t)lds_cu) continue;
-        const int gmax = std::min<int>(match_max_grid(c->device, w, true, dyn), (int)MAX_MATCH_GRID);
-        if (gmax > 0 && (uint64_t)gmax * (uint64_t)w >= D1) {
-            wpb = w;
-            c->mirror = true;
-            break;
-        }
-    }
-    c->wpb = wpb;
-    const size_t dyn = c->mirror ? (size_t)wpb * row_bytes : 0;
-    const int gmax = std::min<int>(match_max_grid(c->device, wpb, c->mirror, dyn), (int)MAX_MATCH_GRID);
-    c->grid = std::min<int>(gmax, (int)((D1 + wpb - 1) / wpb));
-    if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
-    // destinations with at least four times the mean arrival pairs get a
-    // workgroup (so a compute unit) of their own when the grid has room for
-    // it and every other destination still gets a wave: their wave then has
-    // the unit's memory pipeline and LDS to itself
-    c->alone = 0;
-    if (wpb > 1 && c->D > 0) {
-        uint64_t tot = 0;
-        for (uint32_t v = 0; v < c->D; v++) tot += c->dest_pairs[v];
-        uint32_t h = 0;
-        for (uint32_t v = 0; v < c->D; v++)
-            if ((uint64_t)c->dest_pairs[v] * c->D >= 4 * tot && c->dest_pairs[v] > 0) h++;
-        const uint64_t g = h + ((uint64_t)c->D - h + wpb - 1) / wpb;
-        if (h > 0 && g <= (uint64_t)gmax) {
-            c->alone = h;
-            c->grid = (int)g;
-        }
-    }
-    deal_destinations(c);
-    if (c->sw_active) {
-        c->sw_grid = std::min<int>(std::min<int>(match_sw_max_grid(c->device), (int)MAX_MATCH_GRID),
-                                   (int)c->sw_groups);
-        if (c->sw_grid <= 0) return fail(c, PCCL_EDEVICE, "switch-model matching kernel cannot be resident");
-        const pccl_status st = deal_switch_groups(c);
-        if (st != PCCL_OK) return st;
-    }
-    c->have_ws = true;
-    c->uploaded = c->have_result = false;
-    return PCCL_OK;
+    c->have_ws = false;
+    return bind_workspace(c, static_cast<char *>(device_ptr), bytes, max_sends ? max_sends : safe_max_sends(c),
+                          static_cast<hipStream_t>(hip_stream), false);
     GUARD_END(c)
 }
 
+// Copies the plan's pinned image and the collective's inputs into the
+// workspace (pinned sources: plain DMA, no staging by the runtime).
 static pccl_status upload(pccl_ctx *c)
 {
     const Layout &ly = c->ly;
     hipStream_t st = c->stream;
-    auto put = [&](void *dst, const void *src, size_t bytes) -> hipError_t {
-        if (!bytes) return hipSuccess;
-        return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st);
-    };
-    const size_t L4 = sizeof(uint32_t) * c->L;
-    HIP_OR_FAIL(c, put(ly.lsrc, c->src.data(), L4));
-    HIP_OR_FAIL(c, put(ly.ldst, c->dst.data(), L4));
-    HIP_OR_FAIL(c, put(ly.ltime, c->T.data(), L4));
-    HIP_OR_FAIL(c, put(ly.lrev, c->rev.data(), L4));
-    HIP_OR_FAIL(c, put(ly.in_off, c->in_off.data(), sizeof(uint32_t) * (c->D + 1)));
-    HIP_OR_FAIL(c, put(ly.slot_link, c->slot_link.data(), L4));
-    HIP_OR_FAIL(c, put(ly.slot_src, c->slot_src.data(), L4));
-    HIP_OR_FAIL(c, put(ly.slot_time, c->slot_time.data(), L4));
-    HIP_OR_FAIL(c, put(ly.slot_cum, c->slot_cum.data(), L4));
-    HIP_OR_FAIL(c, put(ly.dest_pairs, c->dest_pairs.data(), sizeof(uint32_t) * c->D));
-    HIP_OR_FAIL(c, put(ly.wave_dest, c->wave_dest.data(), sizeof(uint32_t) * c->wave_dest.size()));
-    HIP_OR_FAIL(c, put(ly.group_masks, c->gmask.data(), sizeof(uint64_t) * c->gmask.size()));
-    if (c->sw_active) HIP_OR_FAIL(c, put(const_cast<uint32_t *>(ly.sw.grp), c->swt.data(), sizeof(uint32_t) * c->swt.size()));
-    HIP_OR_FAIL(c, hipStreamSynchronize(st));
+    void *dst[IMG_PARTS] = {ly.lsrc,     ly.ldst,     ly.ltime,     ly.lrev,     ly.in_off,     ly.slot_link, ly.slot_src,
+                            ly.slot_time, ly.slot_cum, ly.dest_pairs, ly.wave_dest, ly.group_masks,
+                            const_cast<uint32_t *>(ly.sw.grp)};
+    for (int k = 0; k < IMG_PARTS; k++)
+        if (c->img_len[k])
+            HIP_OR_FAIL(c, hipMemcpyAsync(dst[k], c->pin_img + c->img_off[k], c->img_len[k], hipMemcpyHostToDevice, st));
+    const size_t bm = (size_t)c->N * c->sz.W * sizeof(uint64_t);
+    if (bm) {
+        HIP_OR_FAIL(c, hipMemcpyAsync(ly.pre, c->pin_in, bm, hipMemcpyHostToDevice, st));
+        HIP_OR_FAIL(c, hipMemcpyAsync(ly.post, c->pin_in + bm, bm, hipMemcpyHostToDevice, st));
+    }
+    if (ly.chunk_group && c->C)
+        HIP_OR_FAIL(c, hipMemcpyAsync(ly.chunk_group, c->pin_in + 2 * bm, (size_t)c->C * sizeof(uint16_t),
+                                      hipMemcpyHostToDevice, st));
     c->uploaded = true;
     return PCCL_OK;
 }
@@ -779,24 +887,20 @@ static pccl_status device_error(pccl_ctx *c, const Control &h)
     }
 }
 
-pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective_time_ns)
+// The synthesis on the bound workspace.  Allocates nothing: the events and
+// the pinned control-block copies come from pccl_create, the inputs from the
+// pinned staging of pccl_set_collective and the plan.
+static pccl_status synthesize_bound(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective_time_ns)
 {
-    if (!c) return PCCL_EINVAL;
-    GUARD_BEGIN
-    c->err.clear();
     c->have_result = false;
-    if (!c->have_ws) return fail(c, PCCL_ESTATE, "set a workspace first");
     HIP_OR_FAIL(c, hipSetDevice(c->device));
+    hipStream_t st = c->stream;
+    HIP_OR_FAIL(c, hipEventRecord(c->ev[0], st));
     if (!c->uploaded) {
         pccl_status s = upload(c);
         if (s != PCCL_OK) return s;
     }
-    hipStream_t st = c->stream;
-    for (hipEvent_t &e : c->ev)
-        if (!e) HIP_OR_FAIL(c, hipEventCreate(&e));
-    if (!c->pin) HIP_OR_FAIL(c, hipHostMalloc((void **)&c->pin, 2 * sizeof(Control), hipHostMallocDefault));
-    HIP_OR_FAIL(c, hipEventRecord(c->ev[0], st));
-    HIP_OR_FAIL(c, launch_setup(c->ly, c->sz, c->pre, c->post, c->chunk_group, c->seed, st));
+    HIP_OR_FAIL(c, launch_setup(c->ly, c->sz, c->ly.pre, c->ly.post, c->ly.chunk_group, c->seed, st));
     // the setup's delivery count sizes the output stage; the host reads it
     // while the matching kernel runs and queues the output kernels behind it
     HIP_OR_FAIL(c, hipMemcpyAsync(&c->pin[0], c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
@@ -832,6 +936,16 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     if (n_sends) *n_sends = c->n_sends;
     if (collective_time_ns) *collective_time_ns = c->coll_time;
     return PCCL_OK;
+}
+
+pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective_time_ns)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    c->have_result = false;
+    if (!c->have_ws) return fail(c, PCCL_ESTATE, "set a workspace first");
+    return synthesize_bound(c, n_sends, collective_time_ns);
     GUARD_END(c)
 }
 

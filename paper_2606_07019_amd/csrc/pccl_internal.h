@@ -121,6 +121,9 @@ struct Layout {
     uint32_t *slot_cum;    // [L] prefix of source in-degrees inside the destination
     uint32_t *dest_pairs;  // [D] total of source in-degrees over the destination's in-links
     uint64_t *group_masks; // [G * WN]
+    // the collective's inputs, copied in from the context's host staging
+    uint64_t *pre, *post;  // [N * W] each, the caller's bitmap layout
+    uint16_t *chunk_group; // [C], null with one group
     // chunk setup
     uint32_t *chunk_src;   // [C]
     uint32_t *holder_cnt;  // [C] bit 31: has a postcondition bit

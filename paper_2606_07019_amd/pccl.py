@@ -1,9 +1,9 @@
 """Thin ctypes binding of libpccl.so (the C ABI in include/pccl.h).
 
 Argument marshalling only: every step of the synthesis runs in the library's
-HIP kernels.  PyTorch provides device memory (the workspace and the device
-copies of the bitmaps) and the stream.  There is no fallback: if the library
-is not built, or no GPU is present, the calls raise.
+HIP kernels.  PyTorch provides device memory (the workspace) and the stream.
+There is no fallback: if the library is not built, or no GPU is present, the
+calls raise.
 """
 
 from __future__ import annotations
@@ -113,15 +113,30 @@ def pccl_load_topology(h, n_npus, n_switches, link_src, link_dst, alpha_ns, bw_G
     _check(h, load_library().pccl_load_topology(h, n_npus, n_switches, L, *[_np_ptr(a) for a in arrs]))
 
 
-def pccl_set_collective(h, n_chunks, chunk_bytes, pre_bits_dev_ptr, post_bits_dev_ptr,
-                        group_masks, chunk_group_dev_ptr, op) -> None:
-    """pre/post/chunk_group are DEVICE pointers (ints); group_masks a host array."""
+def _host_or_ptr(a, dtype):
+    """A numpy array (host memory, kept alive by the caller's frame) or an
+    integer address (host or device memory) for the C call."""
+    if a is None:
+        return None, None
+    if isinstance(a, (int, np.integer)):
+        return ctypes.c_void_p(int(a)), None
+    arr = np.ascontiguousarray(a, dtype=dtype)
+    return _np_ptr(arr), arr
+
+
+def pccl_set_collective(h, n_chunks, chunk_bytes, pre_bits, post_bits, group_masks, chunk_group, op) -> None:
+    """pre_bits / post_bits / chunk_group: numpy arrays (host memory) or
+    integer addresses of host or device memory; the library copies them
+    before returning.  group_masks: a host array."""
     gm = np.ascontiguousarray(group_masks, dtype=np.uint64)
     if gm.ndim == 1:
         gm = gm[None, :]
+    pre_p, pre_a = _host_or_ptr(pre_bits, np.uint64)
+    post_p, post_a = _host_or_ptr(post_bits, np.uint64)
+    cg_p, cg_a = _host_or_ptr(chunk_group, np.uint16)
     _check(h, load_library().pccl_set_collective(
-        h, n_chunks, chunk_bytes, pre_bits_dev_ptr, post_bits_dev_ptr, _np_ptr(gm), gm.shape[0],
-        chunk_group_dev_ptr, op))
+        h, n_chunks, chunk_bytes, pre_p, post_p, _np_ptr(gm), gm.shape[0], cg_p, op))
+    del pre_a, post_a, cg_a
 
 
 def pccl_set_switch_model(h, n_switches, buffer_chunks=None, unicast=None) -> None:
@@ -220,14 +235,9 @@ class Synthesizer:
         sw_buffer, sw_unicast = getattr(topo, "sw_buffer", None), getattr(topo, "sw_unicast", None)
         if sw_buffer is not None or sw_unicast is not None:
             pccl_set_switch_model(self.h, topo.n_switches, sw_buffer, sw_unicast)
-        self.pre = torch.from_numpy(coll.pre.view(np.int64).copy()).to(self.dev)
-        self.post = torch.from_numpy(coll.post.view(np.int64).copy()).to(self.dev)
-        self.cg = None
-        if coll.chunk_group is not None:
-            self.cg = torch.from_numpy(coll.chunk_group.astype(np.int16).copy()).to(self.dev)
-        pccl_set_collective(self.h, coll.n_chunks, coll.chunk_bytes, self.pre.data_ptr(),
-                            self.post.data_ptr(), coll.group_masks,
-                            None if self.cg is None else self.cg.data_ptr(), coll.op)
+        # host arrays, copied by the library before the call returns
+        pccl_set_collective(self.h, coll.n_chunks, coll.chunk_bytes, coll.pre, coll.post,
+                            coll.group_masks, coll.chunk_group, coll.op)
         self.max_sends = max_sends
         nbytes = pccl_workspace_bytes(self.h, max_sends)
         self.ws = torch.empty(nbytes, dtype=torch.uint8, device=self.dev)

@@ -427,7 +427,7 @@ CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
 
 
 # --------------------------------------------------------------------------
-# Chunk-count sweep (Sec. 7, collective size): All-to-All on 64-NPU meshes
+# Chunk-count sweep (Sec. 6.1 Scalability, collective size): All-to-All on 64-NPU meshes
 # with k chunks of 128 KiB per (source, destination) pair
 # --------------------------------------------------------------------------
 

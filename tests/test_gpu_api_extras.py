@@ -119,3 +119,43 @@ def test_path_and_program_checks():
         assert short == 1 and not steps.any()                   # PCCL_EINVAL, nothing written
     finally:
         s.close()
+
+
+def test_inputs_may_be_freed_on_return():
+    # pccl_set_collective copies its arrays: device bitmaps freed and their
+    # memory overwritten, and host bitmaps scribbled over, after the call do
+    # not change the schedule (Sec. 2.1 pre/postconditions are inputs only)
+    import torch
+    from paper_2606_07019_amd import pccl as P
+    dev = torch.device("cuda", 0)
+    for wl in (W.config2(), W.random_small(1), W.mesh3x3_two_groups()):
+        print(f"[api] inputs copied: {wl.name}", flush=True)
+        t, c = wl.topo, wl.coll
+        ref = O.run_workload(wl)
+        h = P.pccl_create(0, wl.tie_seed)
+        try:
+            P.pccl_load_topology(h, t.n_npus, t.n_switches, t.src, t.dst, t.alpha_ns, t.bw_GBps)
+            pre = torch.from_numpy(c.pre.view(np.int64).copy()).to(dev)
+            post_host = c.post.copy()
+            cg = None
+            if c.chunk_group is not None:
+                cg = torch.from_numpy(c.chunk_group.astype(np.int16)).to(dev)
+            P.pccl_set_collective(h, c.n_chunks, c.chunk_bytes, pre.data_ptr(), post_host.ctypes.data,
+                                  c.group_masks, None if cg is None else cg.data_ptr(), c.op)
+            pre.fill_(-1)
+            if cg is not None:
+                cg.fill_(-1)
+            post_host[:] = 0
+            torch.cuda.synchronize()
+            del pre, cg
+            nb = P.pccl_workspace_bytes(h, 0)
+            ws = torch.full((nb,), 0xA5, dtype=torch.uint8, device=dev)
+            P.pccl_set_workspace(h, ws.data_ptr(), nb, 0, torch.cuda.current_stream(dev).cuda_stream)
+            for _ in range(2):
+                n, ct = P.pccl_synthesize(h)
+                assert (n, ct) == (len(ref.sends), ref.collective_time)
+                out = np.zeros((n, 4), np.uint32)
+                P.pccl_get_schedule(h, out.ctypes.data, n)
+                np.testing.assert_array_equal(out, ref.sends)
+        finally:
+            P.pccl_destroy(h)

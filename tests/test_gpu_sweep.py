@@ -1,4 +1,4 @@
-"""GPU parity on the chunk-count sweep (Sec. 7, collective size): All-to-All
+"""GPU parity on the chunk-count sweep (Sec. 6.1 Scalability, collective size): All-to-All
 on the 64-NPU 8x8 mesh and 4x4x4 grid with k chunks of 128 KiB per pair, up
 to k = 64 (262,144 chunks), compared element by element with the oracle."""
 
