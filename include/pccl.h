@@ -225,6 +225,36 @@ pccl_status pccl_set_workspace(pccl_ctx *ctx, void *device_ptr, size_t bytes,
  */
 pccl_status pccl_synthesize(pccl_ctx *ctx, uint64_t *n_sends, uint32_t *collective_time_ns);
 
+/* Size of the library's static scratch: one device array per GPU the
+ * library runs on, held until the process ends (pccl_synthesize_static). */
+#define PCCL_STATIC_SCRATCH_BYTES (128ull << 20)
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: the same
+ * synthesis as pccl_set_workspace + pccl_synthesize, run in the library's
+ * static scratch (PCCL_STATIC_SCRATCH_BYTES of device memory per GPU, a
+ * file-scope array whose address pccl_create looks up once per device)
+ * instead of a caller workspace.  The call allocates nothing and calls no
+ * allocating routine.
+ *   max_sends: bound on the copy transfers, as for pccl_workspace_bytes
+ *     (0 = the safe bound C * (D - 1), which only small collectives fit).
+ *   hip_stream: the stream to run on (NULL = the default stream).
+ * PCCL_ENOMEM, with the sizes in pccl_last_error, when the collective's
+ * workspace for max_sends exceeds PCCL_STATIC_SCRATCH_BYTES (the 512-NPU
+ * All-to-All with its exact 745,472 transfers needs ~103 MiB and fits);
+ * otherwise the statuses of pccl_synthesize.  The context's workspace is
+ * then the scratch: pccl_get_schedule and the other readers copy from it
+ * until a later call of this function on the same GPU, by any context,
+ * reuses the scratch; they then return PCCL_ESTATE.  Every call on a GPU
+ * shares that GPU's scratch: calls that overlap on one GPU (several threads,
+ * or streams without ordering) race and must not be made.  The inputs are
+ * copied into the scratch again unless this context, with the same
+ * collective and max_sends, was the last to use it.
+ */
+pccl_status pccl_synthesize_static(pccl_ctx *ctx, uint64_t max_sends, void *hip_stream, uint64_t *n_sends,
+                                   uint32_t *collective_time_ns);
+
 /* Copies the schedule (canonical order) to `out`, host or device memory,
  * at most `capacity` entries.  PCCL_EINVAL if capacity is too small. */
 pccl_status pccl_get_schedule(pccl_ctx *ctx, pccl_send *out, uint64_t capacity);

@@ -18,6 +18,13 @@
 
 using namespace pccl;
 
+// The library's static scratch, for pccl_synthesize_static: a file-scope
+// device array, one copy per GPU, held until the process ends.  Each device
+// reports its copy's address once (hipGetSymbolAddress with that device
+// current, from pccl_create); host code uses only those addresses, never
+// the array's name.
+static __device__ __align__(256) unsigned char scratch[PCCL_STATIC_SCRATCH_BYTES];
+
 struct pccl_ctx {
     int device = 0;
     uint64_t seed = 0;
@@ -60,6 +67,7 @@ struct pccl_ctx {
     size_t pin_img_cap = 0;
     size_t img_off[16] = {}, img_len[16] = {};
     uint64_t serial = 0;           // unique per context
+    uint64_t static_call = 0;      // the static-scratch call whose result this context holds
     // workspace
     char *ws = nullptr;
     bool ws_static = false;        // the workspace is the library's static scratch
@@ -600,6 +608,30 @@ pccl_status bind_workspace(pccl_ctx *c, char *ptr, size_t bytes, uint64_t ms, hi
     return PCCL_OK;
 }
 
+constexpr int MAX_SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_SCRATCH_DEVICES] = {};
+// Whose inputs each device's scratch holds (context serial, plan generation,
+// max_sends; serial 0 = nobody's), so that repeated calls of one context
+// skip the copy, and the number of the last call, so that a context whose
+// result a later call overwrote is told so.
+struct ScratchOwner {
+    uint64_t serial, plan_gen, max_sends, call;
+};
+ScratchOwner g_scratch_owner[MAX_SCRATCH_DEVICES] = {};
+uint64_t g_next_serial = 1;
+
+// The context's schedule is still in its workspace (a result in the static
+// scratch is gone once another call used the scratch).
+bool result_alive(const pccl_ctx *c)
+{
+    if (!c->have_result) return false;
+    if (!c->ws_static) return true;
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    const ScratchOwner &o = g_scratch_owner[c->device];
+    return o.call == c->static_call && o.serial == c->serial;
+}
+
 }  // namespace
 
 #define GUARD_BEGIN try {
@@ -624,9 +656,23 @@ pccl_status pccl_create(pccl_ctx **out, int hip_device, uint64_t tie_seed)
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || hip_device < 0 || hip_device >= n) return PCCL_EDEVICE;
     if (hipSetDevice(hip_device) != hipSuccess) return PCCL_EDEVICE;
+    if (hip_device >= MAX_SCRATCH_DEVICES) return PCCL_EDEVICE;
+    {
+        // this device's copy of the static scratch, looked up once
+        std::lock_guard<std::mutex> g(g_scratch_mu);
+        if (!g_scratch_ptr[hip_device]) {
+            void *ptr = nullptr;
+            if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return PCCL_EDEVICE;
+            g_scratch_ptr[hip_device] = ptr;
+        }
+    }
     pccl_ctx *c = new pccl_ctx();
     c->device = hip_device;
     c->seed = tie_seed;
+    {
+        std::lock_guard<std::mutex> g(g_scratch_mu);
+        c->serial = g_next_serial++;
+    }
     // the stage events and the pinned control-block copies, made here so
     // that synthesize calls allocate nothing
     bool ok = hipHostMalloc((void **)&c->pin, 2 * sizeof(Control), hipHostMallocDefault) == hipSuccess;
@@ -949,11 +995,50 @@ pccl_status pccl_synthesize(pccl_ctx *c, uint64_t *n_sends, uint32_t *collective
     GUARD_END(c)
 }
 
+pccl_status pccl_synthesize_static(pccl_ctx *c, uint64_t max_sends, void *hip_stream, uint64_t *n_sends,
+                                   uint32_t *collective_time_ns)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    c->err.clear();
+    c->have_result = false;
+    if (!c->have_coll) return fail(c, PCCL_ESTATE, "set a collective first");
+    if (!c->planned) return fail(c, PCCL_ESTATE, "the last pccl_set_collective / pccl_set_switch_model failed");
+    void *base = g_scratch_ptr[c->device];
+    if (!base) return fail(c, PCCL_EDEVICE, "no static scratch address for device %d", c->device);
+    const uint64_t ms = max_sends ? max_sends : safe_max_sends(c);
+    c->have_ws = false;
+    pccl_status st = bind_workspace(c, static_cast<char *>(base), PCCL_STATIC_SCRATCH_BYTES, ms,
+                                    static_cast<hipStream_t>(hip_stream), true);
+    if (st != PCCL_OK) return st;
+    {
+        std::lock_guard<std::mutex> g(g_scratch_mu);
+        ScratchOwner &o = g_scratch_owner[c->device];
+        // the inputs are still there when this context (same plan and bound)
+        // was the last to copy them in; otherwise they are copied again
+        c->uploaded = o.serial == c->serial && o.plan_gen == c->plan_gen && o.max_sends == ms;
+        o.serial = 0;
+        c->static_call = ++o.call;
+    }
+    st = synthesize_bound(c, n_sends, collective_time_ns);
+    {
+        std::lock_guard<std::mutex> g(g_scratch_mu);
+        ScratchOwner &o = g_scratch_owner[c->device];
+        if (c->uploaded && o.call == c->static_call) {
+            o.serial = c->serial;
+            o.plan_gen = c->plan_gen;
+            o.max_sends = ms;
+        }
+    }
+    return st;
+    GUARD_END(c)
+}
+
 pccl_status pccl_get_schedule(pccl_ctx *c, pccl_send *out, uint64_t capacity)
 {
     if (!c) return PCCL_EINVAL;
     GUARD_BEGIN
-    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (!result_alive(c)) return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this schedule was reused" : "no schedule");
     if (capacity < c->n_sends) return fail(c, PCCL_EINVAL, "capacity %llu < %llu sends",
                                           (unsigned long long)capacity, (unsigned long long)c->n_sends);
     if (c->n_sends) {
@@ -970,7 +1055,7 @@ pccl_status pccl_get_path(pccl_ctx *c, uint32_t chunk, uint32_t device, uint32_t
 {
     if (!c) return PCCL_EINVAL;
     GUARD_BEGIN
-    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (!result_alive(c)) return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this schedule was reused" : "no schedule");
     if (chunk >= c->C) return fail(c, PCCL_EINVAL, "chunk %u out of range (%u chunks)", chunk, c->C);
     if (device >= c->D) return fail(c, PCCL_EINVAL, "device %u out of range (%u devices)", device, c->D);
     if (capacity && (!t_start || !next_device)) return fail(c, PCCL_EINVAL, "null output");
@@ -1025,7 +1110,7 @@ pccl_status pccl_export_program(pccl_ctx *c, pccl_step *steps, uint64_t step_cap
 {
     if (!c) return PCCL_EINVAL;
     GUARD_BEGIN
-    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (!result_alive(c)) return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this schedule was reused" : "no schedule");
     std::vector<pccl_send> s(c->n_sends);
     if (c->n_sends) {
         HIP_OR_FAIL(c, hipMemcpyAsync(s.data(), c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDeviceToHost,
@@ -1140,7 +1225,7 @@ pccl_status pccl_get_stats(pccl_ctx *c, uint64_t *events, uint64_t *rounds, uint
 {
     if (!c) return PCCL_EINVAL;
     GUARD_BEGIN
-    if (!c->have_result) return fail(c, PCCL_ESTATE, "no schedule");
+    if (!result_alive(c)) return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this schedule was reused" : "no schedule");
     if (rounds) *rounds = c->ctl_host.rounds;
     if (clashes) *clashes = c->ctl_host.clashes;
     if (windows) *windows = c->ctl_host.windows;
@@ -1197,7 +1282,8 @@ pccl_status pccl_get_setup(pccl_ctx *c, uint32_t *link_time_ns, uint32_t *chunk_
 {
     if (!c) return PCCL_EINVAL;
     GUARD_BEGIN
-    if (!c->have_result) return fail(c, PCCL_ESTATE, "no synthesis");
+    if (!result_alive(c))
+        return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this synthesis was reused" : "no synthesis");
     if (link_time_ns && c->L) std::memcpy(link_time_ns, c->T.data(), sizeof(uint32_t) * c->L);
     hipStream_t st = c->stream;
     if (chunk_src && c->C)

@@ -60,6 +60,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "pccl_workspace_bytes": ([P, U64, ctypes.POINTER(ctypes.c_size_t)], I),
         "pccl_set_workspace": ([P, P, ctypes.c_size_t, U64, P], I),
         "pccl_synthesize": ([P, ctypes.POINTER(U64), ctypes.POINTER(U32)], I),
+        "pccl_synthesize_static": ([P, U64, P, ctypes.POINTER(U64), ctypes.POINTER(U32)], I),
         "pccl_get_schedule": ([P, P, U64], I),
         "pccl_get_path": ([P, U32, U32, P, P, U32, ctypes.POINTER(U32)], I),
         "pccl_export_program": ([P, P, U64, P, U64, ctypes.POINTER(U64), ctypes.POINTER(U64)], I),
@@ -164,6 +165,18 @@ def pccl_synthesize(h):
     t = ctypes.c_uint32()
     _check(h, load_library().pccl_synthesize(h, ctypes.byref(n), ctypes.byref(t)))
     return int(n.value), int(t.value)
+
+
+def pccl_synthesize_static(h, max_sends: int = 0, stream_ptr: int = 0):
+    """The synthesis in the library's static device scratch (no allocation)."""
+    n = ctypes.c_uint64()
+    t = ctypes.c_uint32()
+    _check(h, load_library().pccl_synthesize_static(h, max_sends, stream_ptr or None, ctypes.byref(n),
+                                                    ctypes.byref(t)))
+    return int(n.value), int(t.value)
+
+
+PCCL_STATIC_SCRATCH_BYTES = 128 << 20
 
 
 def pccl_get_schedule(h, out_ptr: int, capacity: int) -> None:

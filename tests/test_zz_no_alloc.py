@@ -1,0 +1,111 @@
+"""GPU: pccl_synthesize_static, the entry point that allocates nothing (it
+runs in the library's static device scratch), against the workspace path
+(pccl_set_workspace + pccl_synthesize) on the same inputs, through the C ABI.
+Schedules must be identical element by element, with the same statistics.
+"""
+
+import numpy as np
+import pytest
+
+from paper_2606_07019_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _status(fn, *a):
+    from paper_2606_07019_amd.pccl import PcclError
+    try:
+        fn(*a)
+        return "OK"
+    except PcclError as e:
+        return e.name[len("PCCL_"):]
+
+
+def _context(wl):
+    from paper_2606_07019_amd import pccl as P
+    t, c = wl.topo, wl.coll
+    h = P.pccl_create(0, wl.tie_seed)
+    P.pccl_load_topology(h, t.n_npus, t.n_switches, t.src, t.dst, t.alpha_ns, t.bw_GBps)
+    if t.sw_buffer is not None or t.sw_unicast is not None:
+        P.pccl_set_switch_model(h, t.n_switches, t.sw_buffer, t.sw_unicast)
+    P.pccl_set_collective(h, c.n_chunks, c.chunk_bytes, c.pre, c.post, c.group_masks, c.chunk_group, c.op)
+    return h
+
+
+def _schedule(h, n):
+    from paper_2606_07019_amd import pccl as P
+    out = np.zeros((max(n, 1), 4), np.uint32)
+    if n:
+        P.pccl_get_schedule(h, out.ctypes.data, n)
+    return out[:n]
+
+
+def _reference(wl):
+    """The workspace path on the same workload: count, time, schedule, stats."""
+    from paper_2606_07019_amd.pccl import Synthesizer
+    s = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed, device=0)
+    try:
+        n, ct = s.synthesize()
+        return n, ct, s.schedule(), s.stats()
+    finally:
+        s.close()
+
+
+def test_static_entry_point_matches_workspace_path():
+    import torch
+    from paper_2606_07019_amd import pccl as P
+    stream = torch.cuda.current_stream(0).cuda_stream
+    # each call smaller than the one before; the 512-NPU All-to-All is the
+    # largest collective here and fits the scratch with its exact bound
+    cases = [W.config4(), W.config3(), W.mesh3x3_two_groups(), W.star_all_gather(6, 3, buffer=2, unicast=True),
+             W.config1()]
+    refs, handles = [], []
+    try:
+        for wl in cases:
+            print(f"[static] {wl.name}", flush=True)
+            n, ct, want, stats = _reference(wl)
+            refs.append((n, ct, want, stats))
+            h = _context(wl)
+            handles.append(h)
+            assert P.pccl_synthesize_static(h, n, stream) == (n, ct)
+            np.testing.assert_array_equal(_schedule(h, n), want)
+            assert P.pccl_get_stats(h) == stats
+        # every earlier context's schedule sat in the scratch a later call reused
+        for h in handles[:-1]:
+            assert _status(P.pccl_get_schedule, h, 0, 0) == "ESTATE"
+        # a context calling again gets its inputs copied in again
+        print("[static] config3 again", flush=True)
+        n, ct, want, stats = refs[1]
+        assert P.pccl_synthesize_static(handles[1], n, stream) == (n, ct)
+        np.testing.assert_array_equal(_schedule(handles[1], n), want)
+        # the same context twice in a row: the second call reuses the inputs
+        # already in the scratch; max_sends 0 (the safe bound) fits this one
+        print("[static] config1 twice", flush=True)
+        n, ct, want, stats = refs[-1]
+        for _ in range(2):
+            assert P.pccl_synthesize_static(handles[-1], 0, stream) == (n, ct)
+            np.testing.assert_array_equal(_schedule(handles[-1], n), want)
+            assert P.pccl_get_stats(handles[-1]) == stats
+    finally:
+        for h in handles:
+            P.pccl_destroy(h)
+
+
+def test_static_entry_point_rejects_oversized_workspaces():
+    import torch
+    from paper_2606_07019_amd import pccl as P
+    from paper_2606_07019_amd.pccl import PcclError
+    print("[static] oversized", flush=True)
+    wl = W.config4()
+    h = _context(wl)
+    try:
+        # the safe bound of the 512-NPU All-to-All needs ~6 GB
+        with pytest.raises(PcclError) as e:
+            P.pccl_synthesize_static(h, 0, torch.cuda.current_stream(0).cuda_stream)
+        assert e.value.name == "PCCL_ENOMEM" and "static scratch" in str(e.value)
+        assert _status(P.pccl_get_schedule, h, 0, 0) == "ESTATE"
+        # a workspace path call on the same context still works afterwards
+        nb = P.pccl_workspace_bytes(h, 745472)
+        assert nb > P.PCCL_STATIC_SCRATCH_BYTES // 2
+    finally:
+        P.pccl_destroy(h)
