@@ -199,6 +199,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.infl = cv.take<uint32_t>(L);
     ly.cur = cv.take<uint32_t>(L);
     ly.lflags = cv.take<uint32_t>(L);
+    ly.lcnt = cv.take<uint32_t>(L);
     ly.snap = cv.take<uint64_t>(3 * L);
     ly.dest_log = cv.take<unsigned long long>(D);
     ly.xslot = cv.take<uint64_t>(2ull * MAX_MATCH_GRID * XSLOT_WORDS);

@@ -141,6 +141,7 @@ struct Layout {
     // matching state
     uint64_t *holds, *needs;  // [D * Wp]
     uint32_t *busy, *infl, *cur, *lflags;  // [L] by slot
+    uint32_t *lcnt;           // [L] by slot: bound on the link's candidates (source holds, destination needs)
     uint64_t *snap;           // [3 * L] by slot
     unsigned long long *dest_log;  // [D] next send-log slot of each destination
     uint64_t *xslot;          // [2 * MAX_MATCH_GRID * XSLOT_WORDS] window exchange slots of the matching kernel

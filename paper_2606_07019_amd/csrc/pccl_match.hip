@@ -73,6 +73,15 @@ struct alignas(16) WaveShared {
     uint32_t src[MAXIN], srcoff[MAXIN], tim[MAXIN];
     uint32_t cur[MAXIN], pick[MAXIN], mode[MAXIN], kind[MAXIN];
     uint32_t cum[MAXIN + 1];
+    // upper bound on each link's candidates (chunks its source holds that
+    // the destination needs): arrivals at the source that the destination
+    // needs add one, the link's own commits subtract one, a pick round that
+    // finds no candidate sets it to 0 (commits by other links are not
+    // subtracted, so it only over-counts)
+    uint32_t known[MAXIN];
+    // per pick round: the lowest listed candidate of each link (arrivals
+    // not yet in the source's row) and how many listed candidates it has
+    uint32_t xpick[MAXIN], xcnt[MAXIN];
     uint32_t arr_end[PAIRS], arr_c[PAIRS];
     uint32_t unf_c[PAIRS];
     uint8_t arr_j[PAIRS], unf_j[PAIRS], arr_need[PAIRS], unf_need[PAIRS];
@@ -447,6 +456,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
         ds.lid = ly.slot_link[sl];
         ws.cur[lane] = ly.cur[sl];
         ws.cum[lane] = ly.slot_cum[sl];
+        ws.known[lane] = ly.lcnt[sl];
     }
     if (lane == 0) ws.cum[ds.n] = ds.pairs;
     wave_sync();
@@ -475,6 +485,7 @@ __device__ void store_dest(const Layout &ly, WaveShared &ws, const Dest &ds)
         ly.infl[sl] = ds.infl;
         ly.cur[sl] = ws.cur[lane];
         ly.lflags[sl] = ds.idle | (ds.ready << 1);
+        ly.lcnt[sl] = ws.known[lane];
     }
     if (lane == 0) ly.dest_log[ds.d] = ds.log;
     wave_sync();
@@ -505,7 +516,8 @@ __device__ __forceinline__ void look_ahead_issue(const Layout &ly, uint32_t hbyt
     la.cur = NONE32;
     la.n_arr = n_arr;
     la.n_unf = n_unf;
-    if (!(mine && ds.infl != NONE32 && !ds.ready)) return;
+    // (a link with no candidate left has nothing to look for)
+    if (!(mine && ds.infl != NONE32 && !ds.ready && ws.known[threadIdx.x & 63] != 0)) return;
     const uint32_t cur = ws.cur[lane];
     if ((cur >> 6) >= Ws) return;
     la.cur = cur;
@@ -765,11 +777,22 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             if (ws.arr_end[q] != t || !ws.arr_need[q]) continue;
             const uint32_t j = ws.arr_j[q], c = ws.arr_c[q];
             const uint32_t kind = ws.kind[j];
+            atomicAdd(&ws.known[j], 1u);
             if (kind == K_BUSY) atomicMin(&ws.cur[j], c);
             else if (kind == K_IDLE) ws.mode[j] = M_ARR;
         }
         wave_sync();
-        if (mine) md = ws.mode[lane];
+        if (mine) {
+            md = ws.mode[lane];
+            // a freed link whose bound says no candidate is left goes idle
+            // without a scan, as a scan would have found
+            if (md == M_FULL && ws.known[lane] == 0) {
+                md = M_IDLE;
+                ds.idle = 1;
+                ws.cur[lane] = END;
+                ws.mode[lane] = M_IDLE;
+            }
+        }
 
         // pick rounds at time t
         while (true) {
@@ -785,7 +808,38 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             uint32_t p = NONE32, scanned = 0;
             bool scanning = false;
             uint64_t pos = 0, w0 = 0;
-            if (mine && md == M_FULL) {
+            // explicit candidates first: arrivals not yet in the source's
+            // row, the lowest and the number per link
+            if (mine) {
+                ws.xpick[lane] = NONE32;
+                ws.xcnt[lane] = 0;
+            }
+            wave_sync();
+            for (uint32_t q = lane; q < n_arr; q += 64) {
+                if (!ws.arr_need[q]) continue;
+                const uint32_t j = ws.arr_j[q], c = ws.arr_c[q], mj = ws.mode[j];
+                if (mj == M_FULL) {
+                    if (ws.arr_end[q] <= t && c >= ws.cur[j]) {
+                        atomicMin(&ws.xpick[j], c);
+                        atomicAdd(&ws.xcnt[j], 1u);
+                    }
+                } else if (mj == M_ARR) {
+                    if (ws.arr_end[q] == t) atomicMin(&ws.xpick[j], c);
+                }
+            }
+            for (uint32_t q = lane; q < n_unf; q += 64) {
+                if (!ws.unf_need[q]) continue;
+                const uint32_t j = ws.unf_j[q], c = ws.unf_c[q];
+                if (ws.mode[j] == M_FULL && c >= ws.cur[j]) {
+                    atomicMin(&ws.xpick[j], c);
+                    atomicAdd(&ws.xcnt[j], 1u);
+                }
+            }
+            wave_sync();
+            // when the link's bound does not exceed its listed candidates,
+            // every candidate is listed (candidates are the union of the
+            // row's and the listed ones) and the row needs no scan
+            if (mine && md == M_FULL && ws.known[lane] > ws.xcnt[lane]) {
                 const uint32_t cur = ws.cur[lane];
                 w0 = cur >> 6;
                 if (cur == ds.ready_c) {
@@ -928,31 +982,14 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 if ((int)lane == j) p = pj;
                 acc.words += w;
             }
-            // explicit candidates: arrivals not yet in the source's row
-            if (mine) ws.pick[lane] = (md == M_FULL) ? p : NONE32;
-            wave_sync();
-            for (uint32_t q = lane; q < n_arr; q += 64) {
-                if (!ws.arr_need[q]) continue;
-                const uint32_t j = ws.arr_j[q], c = ws.arr_c[q], mj = ws.mode[j];
-                if (mj == M_FULL) {
-                    if (ws.arr_end[q] <= t && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
-                } else if (mj == M_ARR) {
-                    if (ws.arr_end[q] == t) atomicMin(&ws.pick[j], c);
-                }
-            }
-            for (uint32_t q = lane; q < n_unf; q += 64) {
-                if (!ws.unf_need[q]) continue;
-                const uint32_t j = ws.unf_j[q], c = ws.unf_c[q];
-                if (ws.mode[j] == M_FULL && c >= ws.cur[j]) atomicMin(&ws.pick[j], c);
-            }
-            wave_sync();
             uint32_t pk = NONE32;
             if (mine && md != M_IDLE) {
-                pk = ws.pick[lane];
+                pk = min(md == M_FULL ? p : NONE32, ws.xpick[lane]);
                 if (pk == NONE32) {
                     md = M_IDLE;
                     ds.idle = 1;
                     ws.cur[lane] = END;
+                    ws.known[lane] = 0;
                 }
                 ws.mode[lane] = md;
             }
@@ -1024,6 +1061,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     const unsigned long long q = ds.log + n_send + lane_prefix(wins, lane);
                     ly.skey[0][q] = ((uint64_t)t << 32) | ds.lid;
                     ly.sval[0][q] = pk;
+                    const uint32_t kn = ws.known[lane];
+                    ws.known[lane] = kn ? kn - 1u : 0u;  // pk was one of its candidates
                     if (md == M_FULL) {
                         ws.cur[lane] = pk + 1;
                         md = M_IDLE;

@@ -282,6 +282,29 @@ __global__ void k_needs(Layout ly, Sizes sz, const uint64_t *pre, const uint64_t
     }
 }
 
+// Candidates of every link at the start (one wave per destination-major
+// slot): popcount(holds[src] & needs[dst]) over the rows.  The matching
+// kernel keeps this count as an upper bound (arrivals add, the link's own
+// commits subtract, a pick round that finds nothing resets it to 0), so a
+// freed link whose bound is 0 has no candidate and needs no scan.
+__global__ void __launch_bounds__(256) k_link_counts(Layout ly, Sizes sz)
+{
+    if (ly.ctl->error) return;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint64_t sl = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (sl >= sz.L) return;
+    const uint64_t Ws = (sz.W + 1) & ~1ull;
+    const uint64_t *h = ly.holds + (uint64_t)ly.slot_src[sl] * sz.Wp;
+    const uint64_t *n = ly.needs + (uint64_t)ly.ldst[ly.slot_link[sl]] * sz.Wp;
+    uint32_t c = 0;
+    for (uint64_t w = 2 * lane; w < Ws; w += 128) {
+        const uint4 a = *reinterpret_cast<const uint4 *>(h + w), b = *reinterpret_cast<const uint4 *>(n + w);
+        c += __popc(a.x & b.x) + __popc(a.y & b.y) + __popc(a.z & b.z) + __popc(a.w & b.w);
+    }
+    for (int off = 32; off; off >>= 1) c += (uint32_t)__shfl_xor((int)c, off);
+    if (lane == 0) ly.lcnt[sl] = c;
+}
+
 // Each destination gets a contiguous segment of the send log, as long as
 // the number of deliveries it needs (every delivery is one transfer into it).
 __global__ void __launch_bounds__(256) k_needs_count(Layout ly, Sizes sz)
@@ -381,6 +404,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
         k_holds<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
     }
     if (sz.W) k_needs<<<gw, T, 0, st>>>(ly, sz, pre, post);
+    if (sz.L) k_link_counts<<<blocks_for(sz.L, 4), 256, 0, st>>>(ly, sz);
     k_needs_count<<<sz.D, 256, 0, st>>>(ly, sz);
     k_log_offsets<<<1, 1024, 0, st>>>(ly, sz);
     k_init_match<<<blocks_for(std::max<uint64_t>(sz.L, 4ull * MAX_MATCH_GRID), T), T, 0, st>>>(ly, sz);

@@ -134,6 +134,32 @@ def test_full_size_buffered_rails_invariants():
     check_switch_model(wl.topo, wl.coll, sched)
 
 
+@pytest.mark.parametrize("nodes,per_node,buffer,unicast", [(64, 8, 64, 1), (64, 8, 16, 0)])
+def test_full_size_switch_model_digest(nodes, per_node, buffer, unicast):
+    """512-NPU All-to-All with 64 buffer places per unicast rail switch, and
+    with 16 places and multicast (Sec. 4.7): the schedule must be the one
+    the oracle wrote (tests/golden/make_switch_golden.py): digest, sampled
+    rows, collective time and statistics."""
+    import hashlib
+    import json
+    import os
+    wl = W.switch2level_model(nodes, per_node, buffer, bool(unicast))
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", f"switch_model_{wl.name}.json")
+    if not os.path.exists(path):
+        pytest.skip(f"no oracle digest for {wl.name}")
+    with open(path) as f:
+        g = json.load(f)
+    print(f"[switch fullsize] {wl.name}", flush=True)
+    status, sched, ct, st = _run_gpu(wl)
+    assert status == "PCCL_OK"
+    assert len(sched) == g["n_sends"] and ct == g["collective_time_ns"]
+    idx = np.array(g["sample_index"], dtype=np.int64)
+    np.testing.assert_array_equal(sched[idx], np.array(g["sample_rows"], dtype=np.uint32))
+    assert hashlib.sha256(np.ascontiguousarray(sched, dtype="<u4").tobytes()).hexdigest() == g["sha256"]
+    for key in ("events", "rounds", "clashes"):
+        assert st[key] == g["stats"][key], key
+
+
 @pytest.mark.parametrize("seed", list(range(200, 216)))
 def test_medium_random_switched_parity(seed):
     # 24-48 NPUs, 2-5 switches with random buffers / multicast, up to 300 chunks
