@@ -112,10 +112,14 @@ void pccl_destroy(pccl_ctx *ctx);
  * byte per ns).  All arrays are host memory of n_links entries and are copied.
  * PCCL_EINVAL: endpoint out of range, self loop, duplicate (src, dst) pair,
  * zero bandwidth, n_npus == 0.  PCCL_EUNSUPPORTED: more than 8000 devices
- * (NPUs plus switches), more than 64 in-links on one device (one wavefront
- * lane per in-link), or a device whose in-links' sources have more than 512
- * in-links in total (the per-destination arrival lists live in ~10 KB of
- * LDS per wavefront).
+ * (NPUs plus switches), more than 256 in-links on one device, a device with
+ * more than 512 in-links that feeds another, or a device whose in-links'
+ * sources have more than 2048 in-links in total.  (The matching kernel gives
+ * a device one wavefront, one lane per in-link and lists of up to 512
+ * arrival pairs in LDS; a device beyond 64 in-links or 512 pairs is split
+ * over the wavefronts of a workgroup of its own, at most four, which needs
+ * the needs rows in LDS: pccl_set_collective returns PCCL_EUNSUPPORTED when
+ * a row of the collective's chunks does not fit there.)
  */
 pccl_status pccl_load_topology(pccl_ctx *ctx, uint32_t n_npus, uint32_t n_switches,
                                uint32_t n_links, const uint32_t *link_src,

@@ -35,6 +35,11 @@ struct pccl_ctx {
     std::vector<uint32_t> src, dst, alpha, bw;
     std::vector<uint32_t> in_off, slot_link, slot_src, slot_cum, dest_pairs, rev;
     std::vector<uint32_t> wave_dest;  // destination of (pass, wave) in the matching kernel
+    std::vector<uint32_t> wave_part;  // its part when the destination is split over a workgroup's waves
+    std::vector<uint32_t> split;      // split destinations, each taking one workgroup (heaviest first)
+    std::vector<std::vector<uint32_t>> split_cuts;  // their parts: first in-link of each part, then the in-degree
+    bool resident = true;             // one destination (or part) per wave for the whole run
+    uint32_t alone = 0;               // heaviest other destinations dealt to a workgroup of their own
     // collective; the pre/post bitmaps and chunk groups are copied into
     // `pin_in` (pinned host memory: pre, then post, then the group ids)
     uint32_t C = 0, G = 0;
@@ -77,7 +82,7 @@ struct pccl_ctx {
     Layout ly{};
     Sizes sz{};
     int grid = 0, wpb = 0;  // matching kernel: workgroups, waves per workgroup
-    uint32_t alone = 0;     // heaviest destinations dealt to a workgroup of their own
+
     bool mirror = false;    // matching kernel keeps each destination's needs row in LDS
     // stage timing; ev[1] also marks that the setup's counts have reached `pin`
     // (events and the pinned block are made by pccl_create, so that a
@@ -157,6 +162,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     sz.WN = words(c->N);
     sz.max_sends = max_sends;
     sz.tmin = c->tmin;
+    sz.resident = c->resident ? 1u : 0u;
     const uint64_t hb = (uint64_t)sz.D * sz.Wp * sizeof(uint64_t);
     sz.hbytes = hb < (1ull << 31) ? (uint32_t)hb : 0u;
     const uint64_t nsort = std::max<uint64_t>(c->C, max_sends);
@@ -204,6 +210,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.dest_log = cv.take<unsigned long long>(D);
     ly.xslot = cv.take<uint64_t>(2ull * MAX_MATCH_GRID * XSLOT_WORDS);
     ly.wave_dest = cv.take<uint32_t>(D + (uint64_t)MATCH_WAVES * MAX_MATCH_GRID);
+    ly.wave_part = cv.take<uint32_t>(D + (uint64_t)MATCH_WAVES * MAX_MATCH_GRID);
     ly.out = cv.take<pccl_send>((c->op == PCCL_OP_ALLREDUCE ? 2 : 1) * max_sends);
     ly.sw = SwTab{};
     if (c->sw_active) {
@@ -424,30 +431,48 @@ pccl_status deal_switch_groups(pccl_ctx *c)
     return PCCL_OK;
 }
 
-// Destinations of the matching kernel's waves: heaviest first (most arrival
-// pairs, then most in-links), dealt across workgroups before filling any
-// workgroup's second wave, so that heavy destinations (switches) do not share
-// a compute unit and its memory pipeline.  Pass r of wave w handles entry
-// r * nwaves + w.
+// Destinations of the matching kernel's waves.  Split destinations first,
+// each taking a whole workgroup (wave p is part p; parts past the last are
+// empty and only take part in the part barriers).  The others heaviest first
+// (most arrival pairs, then most in-links), dealt across the remaining
+// workgroups before filling any workgroup's second wave, so that heavy
+// destinations do not share a compute unit and its memory pipeline.  Pass r
+// of wave w handles entry r * nwaves + w.
 void deal_destinations(pccl_ctx *c)
 {
     const uint32_t D = c->D, nb = (uint32_t)c->grid, wpb = (uint32_t)c->wpb, nw = nb * wpb;
-    std::vector<uint32_t> byweight(D);
-    for (uint32_t v = 0; v < D; v++) byweight[v] = v;
+    std::vector<uint8_t> is_split(D, 0);
+    for (uint32_t d : c->split) is_split[d] = 1;
+    std::vector<uint32_t> byweight;
+    byweight.reserve(D);
+    for (uint32_t v = 0; v < D; v++)
+        if (!is_split[v]) byweight.push_back(v);
     std::stable_sort(byweight.begin(), byweight.end(), [&](uint32_t a, uint32_t b) {
         if (c->dest_pairs[a] != c->dest_pairs[b]) return c->dest_pairs[a] > c->dest_pairs[b];
         return c->in_off[a + 1] - c->in_off[a] > c->in_off[b + 1] - c->in_off[b];
     });
-    const uint32_t passes = (D + nw - 1) / nw;
-    c->wave_dest.assign((size_t)std::max(passes, 1u) * nw, NONE32);
-    // the `alone` heaviest take wave 0 of the first workgroups (one pass,
-    // by construction of the grid), the others are dealt over the rest
-    const uint32_t h = c->alone, nb2 = nb - h;
-    for (uint32_t i = 0; i < h; i++) c->wave_dest[(size_t)i * wpb] = byweight[i];
-    for (uint32_t i = h; i < D; i++) {
-        const uint32_t q = i - h, n2 = nb2 * wpb;
+    // the `alone` heaviest unsplit destinations take wave 0 of the next
+    // workgroups (one pass, by construction of the grid)
+    const uint32_t hs = (uint32_t)c->split.size(), ha = c->alone, h = hs + ha;
+    const uint32_t nb2 = nb - h, rest = (uint32_t)byweight.size() - ha;
+    const uint32_t n2 = nb2 * wpb;
+    const uint32_t passes = n2 ? std::max(1u, (rest + n2 - 1) / n2) : 1u;
+    c->wave_dest.assign((size_t)passes * nw, NONE32);
+    c->wave_part.assign((size_t)passes * nw, 0u);
+    for (uint32_t i = 0; i < hs; i++) {
+        const uint32_t d = c->split[i];
+        const std::vector<uint32_t> &cut = c->split_cuts[i];  // cut[p] = first in-link of part p; cut.back() = in-degree
+        const uint32_t parts = (uint32_t)cut.size() - 1;
+        for (uint32_t p = 0; p < wpb; p++) {
+            const uint32_t first = p < parts ? cut[p] : cut.back(), cnt = p < parts ? cut[p + 1] - cut[p] : 0u;
+            c->wave_dest[(size_t)i * wpb + p] = d;
+            c->wave_part[(size_t)i * wpb + p] = (wpb << 24) | (p << 16) | (first << 8) | cnt;
+        }
+    }
+    for (uint32_t i = 0; i < ha; i++) c->wave_dest[(size_t)(hs + i) * wpb] = byweight[i];
+    for (uint32_t q = 0; q < rest; q++) {
         const uint32_t r = q / n2, j = q % n2, w = (h + j % nb2) * wpb + j / nb2;
-        c->wave_dest[(size_t)r * nw + w] = byweight[i];
+        c->wave_dest[(size_t)r * nw + w] = byweight[ha + q];
     }
 }
 
@@ -489,7 +514,30 @@ pccl_status ensure_pinned(pccl_ctx *c, char **buf, size_t *cap, size_t bytes)
     return PCCL_OK;
 }
 
-constexpr int IMG_PARTS = 13;
+constexpr int IMG_PARTS = 14;
+
+// Parts of destination d for a split over the waves of a workgroup:
+// consecutive in-links, at most `target` links and MAX_PAIRS arrival pairs
+// per part (MAX_IN_LINKS links at most).  Returns the first in-link of each
+// part followed by the in-degree.
+std::vector<uint32_t> cut_parts(const pccl_ctx *c, uint32_t d, uint32_t target)
+{
+    std::vector<uint32_t> cut = {0};
+    const uint32_t b = c->in_off[d], n = c->in_off[d + 1] - b;
+    target = std::min<uint32_t>(std::max<uint32_t>(target, 1), MAX_IN_LINKS);
+    uint32_t links = 0, pairs = 0;
+    for (uint32_t i = 0; i < n; i++) {
+        const uint32_t s = c->slot_src[b + i], p = c->in_off[s + 1] - c->in_off[s];
+        if (links == target || pairs + p > MAX_PAIRS) {
+            cut.push_back(i);
+            links = pairs = 0;
+        }
+        links++;
+        pairs += p;
+    }
+    cut.push_back(n);
+    return cut;
+}
 
 // Everything that depends on the topology, the collective and the switch
 // model but not on the workspace: the switch tables, the matching kernel's
@@ -507,49 +555,107 @@ pccl_status plan(pccl_ctx *c)
     const uint64_t Wp = row_words(c->C);
     const uint64_t hb = (uint64_t)c->D * Wp * sizeof(uint64_t);
     const bool desc_ok = hb < (1ull << 31);  // the LDS-row kernel reads holds through one buffer descriptor
+    // destinations one wave cannot take (more than MAX_IN_LINKS in-links or
+    // MAX_PAIRS arrival pairs) are split over the waves of one workgroup
+    std::vector<uint32_t> must;
+    uint32_t need_w = 1;
+    for (uint32_t d = 0; d < c->D; d++) {
+        const uint32_t parts = (uint32_t)cut_parts(c, d, MAX_IN_LINKS).size() - 1;
+        if (parts > 1) {
+            must.push_back(d);
+            need_w = std::max(need_w, parts);
+        }
+    }
+    if (need_w > MATCH_WAVES)
+        return fail(c, PCCL_EUNSUPPORTED, "a device needs %u waves for its in-links and arrival pairs (limit %u)", need_w,
+                    MATCH_WAVES);
+    // heavy destinations (at least four times the mean arrival pairs) get a
+    // workgroup, so a compute unit, of their own when the grid has room for
+    // it: their wave then has the unit's memory pipeline and LDS to itself
+    uint32_t n_heavy = 0;
+    {
+        uint64_t tot = 0;
+        for (uint32_t v = 0; v < c->D; v++) tot += c->dest_pairs[v];
+        std::vector<uint8_t> is_must(c->D, 0);
+        for (uint32_t d : must) is_must[d] = 1;
+        for (uint32_t v = 0; v < c->D; v++)
+            if (!is_must[v] && c->dest_pairs[v] > 0 && (uint64_t)c->dest_pairs[v] * c->D >= 4 * tot) n_heavy++;
+    }
+    const uint32_t D1 = std::max<uint32_t>(c->D, 1);
+    // the grid for w waves per workgroup with at most gmax workgroups:
+    // split destinations take a workgroup each, heavy ones too if it fits,
+    // the others a wave each
+    auto shape = [&](uint32_t w, int gmax, int &grid, bool &resident, uint32_t &alone) {
+        const uint64_t ns = must.size();
+        alone = 0;
+        const uint64_t g0 = ns + ((uint64_t)c->D - ns + w - 1) / w;
+        if (g0 > (uint64_t)gmax) {
+            if (ns) return false;
+            grid = std::min<int>(gmax, (int)((D1 + w - 1) / w));
+            resident = (uint64_t)grid * w >= c->D;
+            return grid > 0;
+        }
+        grid = (int)std::max<uint64_t>(g0, 1);
+        resident = true;
+        if (w > 1 && n_heavy) {
+            const uint64_t g1 = ns + n_heavy + ((uint64_t)c->D - ns - n_heavy + w - 1) / w;
+            if (g1 <= (uint64_t)gmax) {
+                alone = n_heavy;
+                grid = (int)g1;
+            }
+        }
+        return true;
+    };
     // waves per workgroup: as few as keep the grid near MATCH_TARGET_GRID
     // workgroups, so that few destinations still spread over many compute
     // units while many destinations do not make the window exchange poll
-    // too many slots
-    const uint32_t D1 = std::max<uint32_t>(c->D, 1);
+    // too many slots; at least as many as the largest split destination has
+    // parts
     int wpb = (int)std::min<uint32_t>(MATCH_WAVES, std::max<uint32_t>(1, (D1 + MATCH_TARGET_GRID - 1) / MATCH_TARGET_GRID));
+    wpb = std::max<int>(wpb, (int)need_w);
     // needs rows in LDS: with as many of those waves as leave room for one
-    // row per wave and still give every destination a wave of its own
+    // row per wave, when every wave then owns one destination (or part)
     c->mirror = false;
     int lds_cu = 0;
     HIP_OR_FAIL(c, hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, c->device));
     const size_t lds_static = match_static_lds(), row_bytes = (size_t)Wp * sizeof(uint64_t);
-    for (int w = wpb; w >= 1 && lds_static > 0 && desc_ok; w--) {
+    const bool spl = !must.empty();
+    int grid = 0;
+    bool resident = false;
+    uint32_t alone = 0;
+    for (int w = wpb; w >= (int)need_w && lds_static > 0 && desc_ok; w--) {
         const size_t dyn = (size_t)w * row_bytes;
         if (lds_static + dyn > (size_t)lds_cu) continue;
-        const int gmax = std::min<int>(match_max_grid(c->device, w, true, dyn), (int)MAX_MATCH_GRID);
-        if (gmax > 0 && (uint64_t)gmax * (uint64_t)w >= D1) {
+        const int gmax = std::min<int>(match_max_grid(c->device, w, true, dyn, spl), (int)MAX_MATCH_GRID);
+        if (gmax > 0 && shape((uint32_t)w, gmax, grid, resident, alone) && resident) {
             wpb = w;
             c->mirror = true;
             break;
         }
     }
+    if (!c->mirror) {
+        // destinations are split only by the kernel with needs rows in LDS
+        if (spl)
+            return fail(c, PCCL_EUNSUPPORTED, "device %u needs %u waves for its in-links and arrival pairs, which "
+                        "takes needs rows in LDS (%llu words per row do not fit, or the grid cannot be resident)",
+                        must[0], need_w, (unsigned long long)Wp);
+        const int gmax = std::min<int>(match_max_grid(c->device, wpb, false, 0, false), (int)MAX_MATCH_GRID);
+        if (gmax <= 0 || !shape((uint32_t)wpb, gmax, grid, resident, alone))
+            return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+    }
     c->wpb = wpb;
-    const size_t dyn = c->mirror ? (size_t)wpb * row_bytes : 0;
-    const int gmax = std::min<int>(match_max_grid(c->device, wpb, c->mirror, dyn), (int)MAX_MATCH_GRID);
-    c->grid = std::min<int>(gmax, (int)((D1 + wpb - 1) / wpb));
-    if (c->grid <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
-    // destinations with at least four times the mean arrival pairs get a
-    // workgroup (so a compute unit) of their own when the grid has room for
-    // it and every other destination still gets a wave: their wave then has
-    // the unit's memory pipeline and LDS to itself
-    c->alone = 0;
-    if (wpb > 1 && c->D > 0) {
-        uint64_t tot = 0;
-        for (uint32_t v = 0; v < c->D; v++) tot += c->dest_pairs[v];
-        uint32_t h = 0;
-        for (uint32_t v = 0; v < c->D; v++)
-            if ((uint64_t)c->dest_pairs[v] * c->D >= 4 * tot && c->dest_pairs[v] > 0) h++;
-        const uint64_t g = h + ((uint64_t)c->D - h + wpb - 1) / wpb;
-        if (h > 0 && g <= (uint64_t)gmax) {
-            c->alone = h;
-            c->grid = (int)g;
-        }
+    c->grid = grid;
+    c->resident = resident;
+    c->alone = alone;
+    c->split = must;
+    c->split_cuts.clear();
+    for (uint32_t d : c->split) {
+        // the in-links spread evenly over the workgroup's waves (as few
+        // parts as fit when the pairs do not allow that)
+        const uint32_t n = c->in_off[d + 1] - c->in_off[d];
+        std::vector<uint32_t> cut = cut_parts(c, d, (n + wpb - 1) / wpb);
+        if (cut.size() - 1 > (size_t)wpb) cut = cut_parts(c, d, MAX_IN_LINKS);
+        c->split_cuts.push_back(cut);
     }
     deal_destinations(c);
     if (c->sw_active) {
@@ -567,6 +673,7 @@ pccl_status plan(pccl_ctx *c)
         {c->slot_src.data(), 4ull * c->L},    {c->slot_time.data(), 4ull * c->L},
         {c->slot_cum.data(), 4ull * c->L},    {c->dest_pairs.data(), 4ull * c->D},
         {c->wave_dest.data(), 4ull * c->wave_dest.size()},
+        {c->wave_part.data(), 4ull * c->wave_part.size()},
         {c->gmask.data(), 8ull * c->gmask.size()},
         {c->swt.data(), c->sw_active ? 4ull * c->swt.size() : 0ull}};
     size_t total = 0;
@@ -726,17 +833,20 @@ pccl_status pccl_load_topology(pccl_ctx *c, uint32_t n_npus, uint32_t n_switches
     }
     for (uint32_t d = 0; d < D; d++) {
         const uint32_t indeg = in_off[d + 1] - in_off[d];
-        if (indeg > MAX_IN_LINKS)
-            return fail(c, PCCL_EUNSUPPORTED, "device %u has %u in-links (limit %u)", d, indeg, MAX_IN_LINKS);
+        if (indeg > MAX_SPLIT_LINKS)
+            return fail(c, PCCL_EUNSUPPORTED, "device %u has %u in-links (limit %u)", d, indeg, MAX_SPLIT_LINKS);
         uint64_t cum = 0;
         for (uint32_t sl = in_off[d]; sl < in_off[d + 1]; sl++) {
             slot_cum[sl] = (uint32_t)cum;
             const uint32_t s = slot_src[sl];
+            if (in_off[s + 1] - in_off[s] > MAX_PAIRS)
+                return fail(c, PCCL_EUNSUPPORTED, "device %u has %u in-links and feeds device %u (limit %u)", s,
+                            in_off[s + 1] - in_off[s], d, MAX_PAIRS);
             cum += in_off[s + 1] - in_off[s];
         }
-        if (cum > MAX_PAIRS)
+        if (cum > (uint64_t)MATCH_WAVES * MAX_PAIRS)
             return fail(c, PCCL_EUNSUPPORTED, "device %u: its in-links' sources have %llu in-links in total (limit %u)",
-                        d, (unsigned long long)cum, MAX_PAIRS);
+                        d, (unsigned long long)cum, MATCH_WAVES * MAX_PAIRS);
         dest_pairs[d] = (uint32_t)cum;
     }
     std::vector<uint32_t> rev(L, NONE32);
@@ -893,9 +1003,9 @@ static pccl_status upload(pccl_ctx *c)
 {
     const Layout &ly = c->ly;
     hipStream_t st = c->stream;
-    void *dst[IMG_PARTS] = {ly.lsrc,     ly.ldst,     ly.ltime,     ly.lrev,     ly.in_off,     ly.slot_link, ly.slot_src,
-                            ly.slot_time, ly.slot_cum, ly.dest_pairs, ly.wave_dest, ly.group_masks,
-                            const_cast<uint32_t *>(ly.sw.grp)};
+    void *dst[IMG_PARTS] = {ly.lsrc,      ly.ldst,     ly.ltime,      ly.lrev,      ly.in_off,
+                            ly.slot_link, ly.slot_src, ly.slot_time,  ly.slot_cum,  ly.dest_pairs,
+                            ly.wave_dest, ly.wave_part, ly.group_masks, const_cast<uint32_t *>(ly.sw.grp)};
     for (int k = 0; k < IMG_PARTS; k++)
         if (c->img_len[k])
             HIP_OR_FAIL(c, hipMemcpyAsync(dst[k], c->pin_img + c->img_off[k], c->img_len[k], hipMemcpyHostToDevice, st));
@@ -955,7 +1065,7 @@ static pccl_status synthesize_bound(pccl_ctx *c, uint64_t *n_sends, uint32_t *co
     if (c->sw_active)
         HIP_OR_FAIL(c, launch_match_sw(c->ly, c->sz, st, c->sw_grid));
     else
-        HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb, c->mirror));
+        HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb, c->mirror, !c->split.empty()));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
     HIP_OR_FAIL(c, hipEventSynchronize(c->ev[1]));
     const Control s0 = c->pin[0];

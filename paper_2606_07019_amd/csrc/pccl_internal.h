@@ -16,8 +16,11 @@ constexpr uint32_t ROW_ALIGN_WORDS = 128;
 // Matching kernel envelope (checked on the host when a topology is loaded).
 constexpr uint32_t MATCH_THREADS = 256;   // at most 4 wavefronts per workgroup (one per SIMD), one destination device each
 constexpr uint32_t MATCH_WAVES = MATCH_THREADS / 64;
-constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one device (one lane each)
-constexpr uint32_t MAX_PAIRS = 512;       // sum over a device's in-links of their sources' in-degree
+constexpr uint32_t MAX_IN_LINKS = 64;     // in-links of one wave's part of a device (one lane each)
+constexpr uint32_t MAX_PAIRS = 512;       // sum over a wave's in-links of their sources' in-degree
+// A device with more in-links or arrival pairs than one wave takes is split
+// over the waves of one workgroup (each wave one part of its in-links).
+constexpr uint32_t MAX_SPLIT_LINKS = MATCH_WAVES * MAX_IN_LINKS;
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
 constexpr uint32_t MAX_MATCH_GRID = 1024; // workgroups of the matching kernel (window exchange slots)
 constexpr uint32_t MATCH_TARGET_GRID = 128; // workgroups the matching kernel aims for (measured on MI355X)
@@ -146,6 +149,7 @@ struct Layout {
     unsigned long long *dest_log;  // [D] next send-log slot of each destination
     uint64_t *xslot;          // [2 * MAX_MATCH_GRID * XSLOT_WORDS] window exchange slots of the matching kernel
     uint32_t *wave_dest;      // [D + MATCH_WAVES * MAX_MATCH_GRID] destination of (pass, wave), NONE32 if none
+    uint32_t *wave_part;      // [same] for a split destination: parts << 24 | part << 16 | first link << 8 | links; 0 = whole
     SwTab sw;                 // switch-model tables (null pointers without a switch model)
     // output
     void *out;                // pccl_send [2 * max_sends]
@@ -161,6 +165,7 @@ struct Sizes {
     uint32_t tmin; // smallest link time (window length)
     uint32_t max_tiles;
     uint32_t hbytes;  // bytes of the holds bitmap (D rows of Wp words) when below 2 GiB, else 0
+    uint32_t resident; // every wave of the matching kernel owns one destination (or part) for the whole run
 };
 
 // ---- launchers (each defined in the translation unit that holds its kernels)
@@ -168,8 +173,11 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
                         const uint16_t *chunk_group, uint64_t seed, hipStream_t st);
 // mirror: every wave keeps its destination's needs row in LDS (waves_per_block
 // rows of Wp words of dynamic shared memory); requires one destination per wave.
-hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror);
-int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds);
+// split: some destinations are split over the waves of a workgroup (the
+// kernel variant with part synchronisation; requires mirror)
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror,
+                        bool split);
+int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds, bool split);
 size_t match_static_lds();  // static LDS bytes of the matching kernel
 hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
 int match_sw_max_grid(int device);

@@ -82,17 +82,41 @@ struct alignas(16) WaveShared {
     // per pick round: the lowest listed candidate of each link (arrivals
     // not yet in the source's row) and how many listed candidates it has
     uint32_t xpick[MAXIN], xcnt[MAXIN];
+    // split destinations: per part, its winners of the round (table order)
+    // that also win across parts; this part's first send-log slot of the round
+    uint64_t fin[NWAVES];
+    unsigned long long logq;
     uint32_t arr_end[PAIRS], arr_c[PAIRS];
     uint32_t unf_c[PAIRS];
     uint8_t arr_j[PAIRS], unf_j[PAIRS], arr_need[PAIRS], unf_need[PAIRS];
     uint32_t seg_j[MAXIN], seg_p[MAXIN], seg_pos[MAXIN];  // probe groups: link, result, continuation word
-    // clash detection: lane that last wrote a hashed pick, and slots written twice
-    uint8_t clash_lane[CLASH_SLOTS], clash_hit[CLASH_SLOTS];
+    // clash detection: lane that last wrote a hashed pick, and slots written
+    // twice.  For a part of a split destination, clash_lane also holds the
+    // part's winners of a pick round once its own clashes are resolved
+    alignas(16) uint8_t clash_lane[CLASH_SLOTS];
+    uint8_t clash_hit[CLASH_SLOTS];
     // round (low 16 bits) in which a chunk of each hash slot was last delivered
     uint16_t dlv_round[CLASH_SLOTS];
 };
 
 
+
+// Winners of one pick round of a part of a split destination (chunk, link
+// time, link id), read by the other parts of the destination.
+struct WinTable {
+    uint32_t chunk[MAXIN], tim[MAXIN], lid[MAXIN];
+};
+static_assert(sizeof(WinTable) <= CLASH_SLOTS, "the winners' table lives in the clash table's space");
+__device__ __forceinline__ WinTable &win_table(WaveShared &w) { return *reinterpret_cast<WinTable *>(w.clash_lane); }
+
+// What the parts of a split destination exchange (one per workgroup: a split
+// destination has a workgroup to itself, one part per wave).
+struct GroupShared {
+    unsigned long long log_next;  // next free slot of the destination's send-log segment
+    uint32_t tmin[NWAVES];        // per part: its next event time
+    uint32_t wcnt[NWAVES];        // per part: its winners of the round (in its table)
+    uint32_t flag[NWAVES];        // per part: bit 0 a link picked, bit 1 a link lost a clash inside the part
+};
 
 __device__ inline void wave_sync()
 {
@@ -306,6 +330,7 @@ struct Exchange {
 
 struct BlockShared {
     WaveShared w[NWAVES];
+    GroupShared g;
     uint32_t red_tmin[NWAVES], red_err[NWAVES];
     unsigned long long red_sent[NWAVES];
     Exchange ex;
@@ -410,6 +435,7 @@ struct Acc {
 // One wavefront's destination: uniform values and this lane's in-link.
 struct Dest {
     uint32_t d, base, n, pairs;
+    uint32_t part, nparts;      // split destination: this wave's part and the number of parts (else 0, 0)
     uint32_t src, tim, lid;     // this lane's in-link (lane < n): source, time, link id
     uint32_t busy, infl, idle;  // its state
     uint32_t ready;             // the cursor points at a candidate found ahead of time
@@ -423,13 +449,22 @@ struct Dest {
     uint32_t pair[PAIRS_PER_LANE];
 };
 
-__device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds)
+// `wp`: the wave's part of a split destination (parts << 24 | part << 16 |
+// first in-link << 8 | in-links), 0 for a whole destination.
+__device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, uint32_t wp, Dest &ds)
 {
     const uint32_t lane = threadIdx.x & 63;
     ds.d = d;
-    ds.base = ly.in_off[d];
-    ds.n = ly.in_off[d + 1] - ds.base;
-    ds.pairs = ly.dest_pairs[d];
+    const uint32_t b0 = ly.in_off[d], nall = ly.in_off[d + 1] - b0;
+    const uint32_t first = wp ? (wp >> 8) & 0xFFu : 0u;
+    ds.nparts = wp >> 24;
+    ds.part = (wp >> 16) & 0xFFu;
+    ds.base = b0 + first;
+    ds.n = wp ? (wp & 0xFFu) : nall;
+    // arrival pairs of this part's in-links (the prefix is per destination)
+    const uint32_t cum0 = first < nall ? ly.slot_cum[ds.base] : ly.dest_pairs[d];
+    const uint32_t cum1 = first + ds.n < nall ? ly.slot_cum[ds.base + ds.n] : ly.dest_pairs[d];
+    ds.pairs = cum1 - cum0;
     ds.log = ly.dest_log[d];
     ds.src = 0;
     ds.tim = 0;
@@ -455,7 +490,7 @@ __device__ void load_dest(const Layout &ly, WaveShared &ws, uint32_t d, Dest &ds
         ws.tim[lane] = ds.tim;
         ds.lid = ly.slot_link[sl];
         ws.cur[lane] = ly.cur[sl];
-        ws.cum[lane] = ly.slot_cum[sl];
+        ws.cum[lane] = ly.slot_cum[sl] - cum0;
         ws.known[lane] = ly.lcnt[sl];
     }
     if (lane == 0) ws.cum[ds.n] = ds.pairs;
@@ -609,19 +644,31 @@ __device__ __forceinline__ uint64_t snap_load(const uint64_t *p)
 }
 
 // All events of window [t0, t1) for one destination, by one wavefront.
-template <bool MIRROR>
+// `grp`: the WaveShared of part 0 of a split destination (its parts are
+// consecutive waves), `gs` what the parts exchange; unused otherwise.  The
+// parts of a split destination run the same event times and pick rounds in
+// step: a workgroup barrier gives every part the next event time, another
+// follows the publication of each part's winners of a round (every part then
+// resolves the clashes between parts the same way: fastest link, then lowest
+// id), a third the commits of the round (so the next round's picks see the
+// shared needs row as all parts left it).
+template <bool MIRROR, bool SPLIT>
 __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws, Dest &ds, uint32_t k,
-                               uint32_t t0, uint64_t t1, bool resident, Acc &acc, LookAhead &la)
+                               uint32_t t0, uint64_t t1, bool resident, Acc &acc, LookAhead &la, WaveShared *grp,
+                               GroupShared &gs)
 {
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t n = ds.n, d = ds.d;
-    if (n == 0) return;
+    // (only the kernel variant built for split destinations, which keeps
+    // needs rows in LDS, takes parts; the host deals parts to no other)
+    const bool split = SPLIT && MIRROR && ds.nparts > 1;
+    if (n == 0 && !split) return;
     // Wp: row stride; Ws: where scans end (bits past the last chunk are zero
     // in both rows, so no candidate lies beyond the row's own words)
     const uint64_t Wp = sz.Wp, Ws = (sz.W + 1) & ~1ull, L = sz.L;
     const uint32_t END = (uint32_t)(Ws * 64);
     uint64_t *nd;
-    if constexpr (MIRROR) nd = needs_lds + (uint64_t)(threadIdx.x >> 6) * Wp;
+    if constexpr (MIRROR) nd = needs_lds + (uint64_t)((threadIdx.x >> 6) - ds.part) * Wp;  // part 0's row
     else nd = ly.needs + (uint64_t)d * Wp;
     uint64_t *hd = ly.holds + (uint64_t)d * Wp;
     const uint64_t *snap1 = ly.snap + (uint64_t)((k + 2) % 3) * L;  // in flight at the end of window k-1
@@ -754,7 +801,13 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             for (uint32_t q = lane; q < n_arr; q += 64)
                 if (ws.arr_need[q] && (int64_t)ws.arr_end[q] > t_prev) m = min(m, ws.arr_end[q]);
         }
-        const uint32_t t = wave_min(m);
+        uint32_t t = wave_min(m);
+        if (split) {
+            // the destination's next event: the earliest over its parts
+            if (lane == 0) gs.tmin[ds.part] = t;
+            __syncthreads();
+            for (uint32_t q = 0; q < ds.nparts; q++) t = min(t, gs.tmin[q]);
+        }
         if (t == NONE32) break;
 
         // links whose transfer ends now are free and need a full scan
@@ -994,7 +1047,8 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                 ws.mode[lane] = md;
             }
             const bool act = mine && md != M_IDLE;
-            if (!__ballot(act)) break;
+            // (the parts of a split destination decide together, below)
+            if (!split && !__ballot(act)) break;
             // clash resolution among d's in-links: fastest link, then lowest id.
             // With few picking links every pick is compared with every other
             // one, read from its lane.  Otherwise picks are hashed into a
@@ -1037,9 +1091,70 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     }
                 }
             }
+            // a split destination's parts publish their winners; every part
+            // then finds, for every part's winners, which lose to a winner of
+            // another part (same chunk, smaller (time, link id))
+            bool group_losers = false;
+            if (split) {
+                WinTable &tb = win_table(ws);
+                const uint64_t wm = __ballot(win);
+                if (win) {
+                    const uint32_t i = lane_prefix(wm, lane);
+                    tb.chunk[i] = pk;
+                    tb.tim[i] = ds.tim;
+                    tb.lid[i] = ds.lid;
+                }
+                if (lane == 0) {
+                    gs.wcnt[ds.part] = (uint32_t)__popcll(wm);
+                    gs.flag[ds.part] = (actm ? 1u : 0u) | (__ballot(act && !win) ? 2u : 0u);
+                }
+                __syncthreads();
+                bool any_act = false;
+                for (uint32_t q = 0; q < ds.nparts; q++) {
+                    any_act |= (gs.flag[q] & 1u) != 0;
+                    group_losers |= (gs.flag[q] & 2u) != 0;
+                }
+                if (!any_act) {
+                    // nobody picked: the round ends for every part (a
+                    // barrier first, so that no part writes its table of the
+                    // next round while others read this one's flags)
+                    __syncthreads();
+                    break;
+                }
+                uint64_t myfin = 0;
+#pragma unroll
+                for (uint32_t q = 0; q < NWAVES; q++) {
+                    if (q >= ds.nparts) break;
+                    const uint32_t nq = gs.wcnt[q];
+                    bool ok = lane < nq;
+                    if (ok) {
+                        const WinTable &a = win_table(grp[q]);
+                        const uint32_t c = a.chunk[lane];
+                        const uint64_t kq = ((uint64_t)a.tim[lane] << 32) | a.lid[lane];
+                        for (uint32_t r = 0; r < ds.nparts && ok; r++) {
+                            if (r == q) continue;
+                            const WinTable &b = win_table(grp[r]);
+                            for (uint32_t i = 0; i < gs.wcnt[r]; i++)
+                                if (b.chunk[i] == c && (((uint64_t)b.tim[i] << 32) | b.lid[i]) < kq) ok = false;
+                        }
+                    }
+                    const uint64_t fq = __ballot(ok);
+                    if (lane == 0) ws.fin[q] = fq;
+                    if (q == ds.part) myfin = fq;
+                    group_losers |= fq != (nq >= 64 ? ~0ull : ((1ull << nq) - 1ull));
+                }
+                if (win) win = (myfin >> lane_prefix(wm, lane)) & 1ull;
+            }
             const uint64_t wins = __ballot(win);
             const uint64_t losers = __ballot(act && !win);
             uint32_t ce = 0;
+            unsigned long long logq = 0;
+            if (split) {
+                // this round's slots of the shared send-log segment
+                if (lane == 0) ws.logq = wins ? atomicAdd(&gs.log_next, (unsigned long long)__popcll(wins)) : 0ull;
+                wave_sync();
+                logq = ws.logq;
+            }
             bool overflow = false;
             if (act) {
                 if (win) {
@@ -1058,7 +1173,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     ce = e32;
                     __hip_atomic_store(&snap0[sl], ((uint64_t)pk << 32) | e32, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
-                    const unsigned long long q = ds.log + n_send + lane_prefix(wins, lane);
+                    const unsigned long long q = (split ? logq : ds.log + n_send) + lane_prefix(wins, lane);
                     ly.skey[0][q] = ((uint64_t)t << 32) | ds.lid;
                     ly.sval[0][q] = pk;
                     const uint32_t kn = ws.known[lane];
@@ -1085,7 +1200,32 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             // picks; otherwise winners stamp their chunk's hash slot with the
             // round, and a stamped slot drops the candidate (a hash collision
             // only drops one that is still valid, which costs a scan)
-            if (few) {
+            if (split) {
+                // every part's winners, from their tables
+#pragma unroll
+                for (uint32_t q = 0; q < NWAVES; q++) {
+                    if (q >= ds.nparts) break;
+                    const WinTable &a = win_table(grp[q]);
+                    for (uint64_t m = ws.fin[q]; m; m &= m - 1) {
+                        const uint32_t c = a.chunk[__builtin_ffsll((long long)m) - 1];
+                        if (c == ds.ready_c) ds.ready_c = NONE32;
+                    }
+                }
+                if (n_arr | n_unf) {
+#pragma unroll
+                    for (uint32_t q0 = 0; q0 < NWAVES; q0++) {
+                        if (q0 >= ds.nparts) break;
+                        const WinTable &a = win_table(grp[q0]);
+                        for (uint64_t m = ws.fin[q0]; m; m &= m - 1) {
+                            const uint32_t c = a.chunk[__builtin_ffsll((long long)m) - 1];
+                            for (uint32_t q = lane; q < n_arr; q += 64)
+                                if (ws.arr_c[q] == c) ws.arr_need[q] = 0;
+                            for (uint32_t q = lane; q < n_unf; q += 64)
+                                if (ws.unf_c[q] == c) ws.unf_need[q] = 0;
+                        }
+                    }
+                }
+            } else if (few) {
                 bool gone = false;
                 for (uint64_t m = wins; m; m &= m - 1)
                     gone |= readlane32(pk, (uint32_t)__builtin_ffsll((long long)m) - 1u) == ds.ready_c;
@@ -1099,7 +1239,7 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             // the delivered chunks are no longer needed: clear their flags
             // (each entry is compared with the winners' picks, read from
             // their lanes)
-            if ((n_arr | n_unf) && wins) {
+            if (!split && (n_arr | n_unf) && wins) {
                 for (uint32_t q = lane; q < n_arr; q += 64) {
                     const uint32_t c = ws.arr_c[q];
                     bool hit = false;
@@ -1129,11 +1269,19 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     ws.mode[lane] = md;
                 }
             }
-            acc.rounds++;
+            if (!split || ds.part == 0) acc.rounds++;
             wave_sync();
-            // no loser: every link that picked has committed, and a further
-            // round would find no link left to pick
-            if (!losers) break;
+            if (split) {
+                // the round's commits (needs row) are seen by every part's
+                // next picks, and nobody writes a table still being read
+                if constexpr (!MIRROR) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): needs row in device memory
+                __syncthreads();
+                if (!group_losers) break;
+            } else if (!losers) {
+                // no loser: every link that picked has committed, and a
+                // further round would find no link left to pick
+                break;
+            }
         }
         t_prev = t;
     }
@@ -1164,14 +1312,16 @@ __device__ __forceinline__ void look_ahead_late(const Layout &ly, const Sizes &s
     const uint32_t lane = threadIdx.x & 63;
     const uint64_t Wp = sz.Wp, Ws = (sz.W + 1) & ~1ull;
     const uint64_t *nd;
-    if constexpr (MIRROR) nd = needs_lds + (uint64_t)(threadIdx.x >> 6) * Wp;
+    if constexpr (MIRROR) nd = needs_lds + (uint64_t)((threadIdx.x >> 6) - ds.part) * Wp;  // part 0's row
     else nd = ly.needs + (uint64_t)ds.d * Wp;
     look_ahead_issue<MIRROR>(ly, sz.hbytes, Wp, Ws, ws, ds, nd, lane < ds.n, ds.n_arr_prev, ds.n_unf_prev, la);
 }
 
 // MIRROR: every wave owns one destination for the whole run and keeps its
-// needs row in LDS (the host checks both).
-template <bool MIRROR>
+// needs row in LDS (the host checks both).  SPLIT: some destinations are
+// split over the waves of a workgroup (only with MIRROR; a separate build of
+// the kernel, so that the others carry none of the part synchronisation).
+template <bool MIRROR, bool SPLIT>
 __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 {
     __shared__ BlockShared sh;
@@ -1185,8 +1335,9 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         return;
     }
     const unsigned long long max_windows = ctl->needs_total + 2ull;
-    // every wave owns at most one destination: its state stays on chip
-    const bool resident = sz.D <= nwaves;
+    // every wave owns at most one destination (or part of one): its state
+    // stays on chip
+    const bool resident = sz.resident != 0;
     // (the host picks that kernel only with one destination per wave and a
     // holds bitmap the buffer descriptor spans)
     if (MIRROR && (!resident || sz.hbytes == 0)) {
@@ -1201,9 +1352,11 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     }
     const uint32_t passes = (sz.D + nwaves - 1) / nwaves;
     const uint32_t mine_d = resident ? ly.wave_dest[gwave] : NONE32;
-    if (mine_d != NONE32) load_dest(ly, ws, mine_d, ds);
+    if (mine_d != NONE32) load_dest(ly, ws, mine_d, ly.wave_part[gwave], ds);
+    // a split destination's send-log segment is shared by its parts
+    if (SPLIT && mine_d != NONE32 && ds.nparts > 1 && ds.part == 0 && lane == 0) sh.g.log_next = ds.log;
     if constexpr (MIRROR) {
-        if (mine_d != NONE32) {
+        if (mine_d != NONE32 && ds.part == 0) {
             uint64_t *row = needs_lds + (uint64_t)wave * sz.Wp;
             const uint64_t *g = ly.needs + (uint64_t)mine_d * sz.Wp;
             for (uint64_t i = 2 * lane; i < sz.Wp; i += 128)
@@ -1211,6 +1364,8 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         }
         wave_sync();
     }
+    // the parts of a split destination see part 0's row and log slot
+    if constexpr (SPLIT) __syncthreads();
     Acc acc = {NONE32, 0u, 0u, 0ull, 0ull, 0ull, 0ull, 0ull, 0u};
     LookAhead la;
     la.cur = NONE32;
@@ -1224,13 +1379,15 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
         acc.tmin = NONE32;
         const unsigned long long sent0 = acc.sent;
         if (resident) {
-            if (mine_d != NONE32) process_window<MIRROR>(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc, la);
+            if (mine_d != NONE32)
+                process_window<MIRROR, SPLIT>(ly, sz, ws, ds, (uint32_t)k, t0, t1, true, acc, la, sh.w + (wave - ds.part),
+                                              sh.g);
         } else if constexpr (!MIRROR) {
             for (uint32_t r = 0; r < passes; r++) {
                 const uint32_t d = ly.wave_dest[(uint64_t)r * nwaves + gwave];
                 if (d == NONE32) continue;
-                load_dest(ly, ws, d, ds);
-                process_window<false>(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc, la);
+                load_dest(ly, ws, d, 0u, ds);
+                process_window<false, false>(ly, sz, ws, ds, (uint32_t)k, t0, t1, false, acc, la, sh.w, sh.g);
                 store_dest(ly, ws, ds);
             }
         }
@@ -1259,7 +1416,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
             // window's start then finds nothing left to do
             if (wave != 0 && ds.n > 0) {
                 const uint64_t *nd;
-                if constexpr (MIRROR) nd = needs_lds + (uint64_t)wave * sz.Wp;
+                if constexpr (MIRROR) nd = needs_lds + (uint64_t)(wave - ds.part) * sz.Wp;  // part 0's row
                 else nd = ly.needs + (uint64_t)ds.d * sz.Wp;
                 look_ahead_finish<MIRROR>((sz.W + 1) & ~1ull, ws, ds, nd, lane < ds.n, la);
             }
@@ -1295,23 +1452,24 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 }  // namespace
 
 namespace {
-const void *match_kernel(bool mirror)
+const void *match_kernel(bool mirror, bool split)
 {
-    return mirror ? reinterpret_cast<const void *>(k_match<true>) : reinterpret_cast<const void *>(k_match<false>);
+    if (split) return reinterpret_cast<const void *>(k_match<true, true>);
+    return mirror ? reinterpret_cast<const void *>(k_match<true, false>) : reinterpret_cast<const void *>(k_match<false, false>);
 }
 }  // namespace
 
 size_t match_static_lds()
 {
     hipFuncAttributes a{};
-    if (hipFuncGetAttributes(&a, match_kernel(true)) != hipSuccess) return 0;
+    if (hipFuncGetAttributes(&a, match_kernel(true, false)) != hipSuccess) return 0;
     return a.sharedSizeBytes;
 }
 
-int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds)
+int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds, bool split)
 {
     int per_cu = 0, cus = 0;
-    const void *kern = match_kernel(mirror);
+    const void *kern = match_kernel(mirror, split);
     if (dyn_lds && hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn_lds) != hipSuccess)
         return 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * waves_per_block, dyn_lds) != hipSuccess)
@@ -1320,11 +1478,13 @@ int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds)
     return per_cu * cus;
 }
 
-hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror)
+hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror,
+                        bool split)
 {
     if (waves_per_block < 1 || waves_per_block > (int)NWAVES) return hipErrorInvalidValue;
+    if (split && !mirror) return hipErrorInvalidValue;
     const size_t dyn = mirror ? (size_t)waves_per_block * sz.Wp * sizeof(uint64_t) : 0;
-    const void *kern = match_kernel(mirror);
+    const void *kern = match_kernel(mirror, split);
     if (dyn) {
         const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
         if (e != hipSuccess) return e;

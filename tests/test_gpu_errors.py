@@ -77,11 +77,20 @@ def test_status_matches_the_oracle(label, wl):
     assert msg
 
 
-def test_more_in_links_than_lanes_is_outside_the_envelope():
-    # a hub with 65 in-links: one wavefront lane per in-link
+def test_in_link_envelope():
+    # a hub with 65 in-links is split over two waves (one lane per in-link)
+    # and matches the oracle; 257 in-links exceed the four waves of a
+    # workgroup
     pairs = [(v, 0) for v in range(1, 66)] + [(0, v) for v in range(1, 66)]
-    tp = W.make_topology(66, 0, pairs, 1, 1)
-    st, msg, _ = _gpu(_wl(tp, W.all_gather(66, [0, 1], 1, 8)))
+    wl = _wl(W.make_topology(66, 0, pairs, 1, 1), W.all_gather(66, [0, 1], 1, 8))
+    ref = O.run_workload(wl)
+    st, msg, res = _gpu(wl)
+    assert st == "OK", msg
+    assert res[0] == len(ref.sends) and res[1] == ref.collective_time
+    np.testing.assert_array_equal(res[2], ref.sends)
+    pairs = [(v, 0) for v in range(1, 258)] + [(0, v) for v in range(1, 258)]
+    tp = W.make_topology(258, 0, pairs, 1, 1)
+    st, msg, _ = _gpu(_wl(tp, W.all_gather(258, [0, 1], 1, 8)))
     assert st == "EUNSUPPORTED" and "in-links" in msg
 
 
