@@ -271,6 +271,15 @@ def main():
     prof = syn.profile()
     st = syn.stats()
     n = syn.n_sends
+    busy, bins, bin_ns = syn.link_usage(20)
+    ct = max(syn.collective_time, 1)
+    frac = busy / ct
+    schedule_metrics = {
+        "link_busy_fraction": {"mean": round(float(frac.mean()), 4), "max": round(float(frac.max()), 4),
+                               "min": round(float(frac.min()), 4), "links_unused": int((busy == 0).sum())},
+        "utilization_over_time": {"bins": 20, "bin_ns": bin_ns,
+                                  "fraction_of_links_busy": [round(float(b) / (len(busy) * bin_ns), 4) for b in bins]},
+    }
     log(f"[bench] {args.steps} steps in {dt:.3f} s; stages (ms, last step) {prof}")
 
     avg_match_s = sum(match_ms) / len(match_ms) / 1e3
@@ -303,6 +312,7 @@ def main():
         "stage_ms": {"setup": sum(setup_ms) / len(setup_ms), "match": sum(match_ms) / len(match_ms),
                      "output": sum(output_ms) / len(output_ms)},
         "roofline": roofline,
+        "schedule_metrics": schedule_metrics,
         "context": {"paper_512npu_a2a_synthesis_s": 700.8, "paper_hardware": "not stated",
                     "paper_topology": "2D Mesh / 3D Hypercube family (not this topology)"},
     }

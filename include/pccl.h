@@ -305,6 +305,24 @@ pccl_status pccl_export_program(pccl_ctx *ctx, pccl_step *steps, uint64_t step_c
                                 uint64_t dep_capacity, uint64_t *n_steps, uint64_t *n_deps);
 
 /*
+ * Link usage of the schedule (the quantities behind the paper's link
+ * utilization heat map and bandwidth-over-time figures, Sec. 6.4), computed
+ * on the host from the last synthesize call's schedule (all of it: both
+ * halves of an All-Reduce):
+ *   busy_ns[L]: time link l carries transfers, the sum of T[l] over its
+ *     sends (its busy fraction is busy_ns[l] / collective time);
+ *   bin_busy_ns[n_bins]: the collective time cut into n_bins bins of
+ *     *bin_ns = ceil(collective time / n_bins) ns; entry b is the link-time
+ *     of all transfers inside bin b (utilization over time = bin_busy_ns[b]
+ *     / (L * bin_ns)).
+ * Output arrays are HOST memory; either may be NULL (n_bins is then
+ * ignored).  PCCL_ESTATE without a schedule, PCCL_EINVAL for n_bins == 0
+ * with bin_busy_ns given.
+ */
+pccl_status pccl_get_link_usage(pccl_ctx *ctx, uint64_t *busy_ns, uint32_t n_bins, uint64_t *bin_busy_ns,
+                                uint32_t *bin_ns);
+
+/*
  * Statistics of the last synthesize call:
  *   events  -- distinct event times visited by the event loop (time 0 plus
  *              every transfer end up to the last transfer start),

@@ -1376,6 +1376,37 @@ pccl_status pccl_get_stats(pccl_ctx *c, uint64_t *events, uint64_t *rounds, uint
     GUARD_END(c)
 }
 
+pccl_status pccl_get_link_usage(pccl_ctx *c, uint64_t *busy_ns, uint32_t n_bins, uint64_t *bin_busy_ns,
+                                uint32_t *bin_ns)
+{
+    if (!c) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!result_alive(c)) return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this schedule was reused" : "no schedule");
+    if (bin_busy_ns && n_bins == 0) return fail(c, PCCL_EINVAL, "no bins");
+    std::vector<pccl_send> s(c->n_sends);
+    if (c->n_sends) {
+        HIP_OR_FAIL(c, hipMemcpyAsync(s.data(), c->ly.out, sizeof(pccl_send) * c->n_sends, hipMemcpyDeviceToHost,
+                                      c->stream));
+        HIP_OR_FAIL(c, hipStreamSynchronize(c->stream));
+    }
+    if (busy_ns) {
+        std::fill(busy_ns, busy_ns + c->L, 0ull);
+        for (const pccl_send &x : s) busy_ns[x.link] += c->T[x.link];
+    }
+    if (bin_busy_ns) {
+        const uint64_t ct = c->coll_time, w = std::max<uint64_t>(1, (ct + n_bins - 1) / n_bins);
+        std::fill(bin_busy_ns, bin_busy_ns + n_bins, 0ull);
+        for (const pccl_send &x : s) {
+            const uint64_t a = x.t_start_ns, e = a + c->T[x.link];
+            for (uint64_t b = a / w; b < n_bins && b * w < e; b++)
+                bin_busy_ns[b] += std::min(e, (b + 1) * w) - std::max(a, b * w);
+        }
+        if (bin_ns) *bin_ns = (uint32_t)w;
+    }
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
 pccl_status pccl_get_profile(pccl_ctx *c, double *setup_ms, double *match_ms, double *output_ms,
                              uint64_t *scan_words)
 {

@@ -306,7 +306,7 @@ __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restr
 // barrier: every workgroup publishes its results in one 64-bit slot of its
 // own cache line (so the pollers' loads spread over the memory channels):
 // gen+1 (12 bits) | error flag | transfers committed (19 bits) | earliest
-// transfer end (32 bits).  Wave 0 of every workgroup then polls all slots,
+// transfer end (32 bits).  The last wave of every workgroup then polls all slots,
 // one per lane, until each carries the tag, and reduces them itself.  Slots
 // alternate with the window parity: a workgroup can run at most one window
 // ahead of the slowest poller, so it never overwrites a slot that is still
@@ -359,7 +359,10 @@ __device__ bool window_wait(Control *ctl, uint64_t *xslot, BlockShared &sh, uint
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
     const uint64_t tag = (uint64_t)((gen + 1u) & 0xFFFu) << 52;
     uint64_t *slot = xslot + (uint64_t)((gen + 1u) & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
-    if (threadIdx.x < 64) {
+    // the last wave polls: in a workgroup that holds one heavy destination on
+    // wave 0 and idle waves after it, the destination's wave is then free to
+    // finish its look-ahead during the wait
+    if ((threadIdx.x >> 6) == (blockDim.x >> 6) - 1u) {
         uint32_t spins = 0, ok = 1;
         uint32_t tn = NONE32, e = 0;
         unsigned long long s = 0;
@@ -1414,7 +1417,7 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
             // waves that do not poll the exchange finish it while they wait
             // (it reads nothing the exchange changes); the call at the next
             // window's start then finds nothing left to do
-            if (wave != 0 && ds.n > 0) {
+            if (wave != wpb - 1u && ds.n > 0) {
                 const uint64_t *nd;
                 if constexpr (MIRROR) nd = needs_lds + (uint64_t)(wave - ds.part) * sz.Wp;  // part 0's row
                 else nd = ly.needs + (uint64_t)ds.d * sz.Wp;

@@ -67,6 +67,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "pccl_get_stats": ([P, ctypes.POINTER(U64), ctypes.POINTER(U64), ctypes.POINTER(U64),
                             ctypes.POINTER(U64)], I),
         "pccl_get_setup": ([P, P, P, P, P], I),
+        "pccl_get_link_usage": ([P, P, U32, P, ctypes.POINTER(U32)], I),
         "pccl_get_profile": ([P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(U64)], I),
         "pccl_last_error": ([P], ctypes.c_char_p),
@@ -212,6 +213,15 @@ def pccl_get_stats(h) -> dict:
     return dict(zip(["events", "rounds", "clashes", "windows"], [int(x.value) for x in v]))
 
 
+def pccl_get_link_usage(h, n_links: int, n_bins: int = 20):
+    """(busy_ns per link, busy link-time per time bin, bin width in ns)."""
+    busy = np.zeros(max(n_links, 1), np.uint64)
+    bins = np.zeros(max(n_bins, 1), np.uint64)
+    w = ctypes.c_uint32()
+    _check(h, load_library().pccl_get_link_usage(h, _np_ptr(busy), n_bins, _np_ptr(bins), ctypes.byref(w)))
+    return busy[:n_links], bins[:n_bins], int(w.value)
+
+
 def pccl_get_profile(h) -> dict:
     d = [ctypes.c_double() for _ in range(3)]
     w = ctypes.c_uint64()
@@ -289,6 +299,9 @@ class Synthesizer:
 
     def profile(self) -> dict:
         return pccl_get_profile(self.h)
+
+    def link_usage(self, n_bins: int = 20):
+        return pccl_get_link_usage(self.h, self.topo.n_links, n_bins)
 
     def setup(self):
         return pccl_get_setup(self.h, self.topo.n_links, self.coll.n_chunks)

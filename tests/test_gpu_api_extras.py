@@ -159,3 +159,31 @@ def test_inputs_may_be_freed_on_return():
                 np.testing.assert_array_equal(out, ref.sends)
         finally:
             P.pccl_destroy(h)
+
+
+@pytest.mark.parametrize("make", [W.config1, W.config2, lambda: W.random_small(4)])
+def test_link_usage_from_the_schedule(make):
+    # per-link busy time and busy link-time per time bin (Sec. 6.4
+    # utilization), recomputed here from the schedule the library returned
+    from paper_2606_07019_amd.pccl import Synthesizer
+    wl = make()
+    print(f"[api] link usage: {wl.name}", flush=True)
+    s = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed)
+    try:
+        n, ct = s.synthesize()
+        sched = s.schedule()
+        busy, bins, w = s.link_usage(7)
+    finally:
+        s.close()
+    bw = wl.topo.bw_GBps.astype(np.int64)
+    T = wl.topo.alpha_ns.astype(np.int64) + (wl.coll.chunk_bytes + bw - 1) // bw
+    want = np.zeros(wl.topo.n_links, np.int64)
+    np.add.at(want, sched[:, 0].astype(np.int64), T[sched[:, 0]])
+    np.testing.assert_array_equal(busy.astype(np.int64), want)
+    assert w == max(1, -(-ct // 7))
+    got = np.zeros(7, np.int64)
+    for l, c, t, f in sched.astype(np.int64):
+        for b in range(7):
+            got[b] += max(0, min(t + T[l], (b + 1) * w) - max(t, b * w))
+    np.testing.assert_array_equal(bins.astype(np.int64), got)
+    assert int(bins.sum()) == int(want.sum())
