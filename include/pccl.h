@@ -117,9 +117,12 @@ void pccl_destroy(pccl_ctx *ctx);
  * sources have more than 2048 in-links in total.  (The matching kernel gives
  * a device one wavefront, one lane per in-link and lists of up to 512
  * arrival pairs in LDS; a device beyond 64 in-links or 512 pairs is split
- * over the wavefronts of a workgroup of its own, at most four, which needs
- * the needs rows in LDS: pccl_set_collective returns PCCL_EUNSUPPORTED when
- * a row of the collective's chunks does not fit there.)
+ * over the wavefronts of a workgroup of its own, at most four.
+ * pccl_set_collective returns PCCL_EUNSUPPORTED when the matching kernel
+ * cannot keep a workgroup per split device and a wavefront per other device
+ * resident at once: with needs rows too wide for LDS that is 512 workgroups
+ * of four wavefronts on MI355X (128 nodes of 8 NPUs behind 128-port switches
+ * take 8 + 256 of them).)
  */
 pccl_status pccl_load_topology(pccl_ctx *ctx, uint32_t n_npus, uint32_t n_switches,
                                uint32_t n_links, const uint32_t *link_src,

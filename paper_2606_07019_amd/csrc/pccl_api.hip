@@ -634,14 +634,12 @@ pccl_status plan(pccl_ctx *c)
         }
     }
     if (!c->mirror) {
-        // destinations are split only by the kernel with needs rows in LDS
-        if (spl)
-            return fail(c, PCCL_EUNSUPPORTED, "device %u needs %u waves for its in-links and arrival pairs, which "
-                        "takes needs rows in LDS (%llu words per row do not fit, or the grid cannot be resident)",
-                        must[0], need_w, (unsigned long long)Wp);
-        const int gmax = std::min<int>(match_max_grid(c->device, wpb, false, 0, false), (int)MAX_MATCH_GRID);
-        if (gmax <= 0 || !shape((uint32_t)wpb, gmax, grid, resident, alone))
-            return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+        const int gmax = std::min<int>(match_max_grid(c->device, wpb, false, 0, spl), (int)MAX_MATCH_GRID);
+        if (gmax <= 0) return fail(c, PCCL_EDEVICE, "matching kernel cannot be resident");
+        if (!shape((uint32_t)wpb, gmax, grid, resident, alone))
+            return fail(c, PCCL_EUNSUPPORTED, "device %u needs %u waves for its in-links and arrival pairs; the "
+                        "matching kernel cannot keep a workgroup per such device and a wave per other device "
+                        "resident (%d workgroups of %d waves at most)", must[0], need_w, gmax, wpb);
     }
     c->wpb = wpb;
     c->grid = grid;

@@ -174,7 +174,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
 // mirror: every wave keeps its destination's needs row in LDS (waves_per_block
 // rows of Wp words of dynamic shared memory); requires one destination per wave.
 // split: some destinations are split over the waves of a workgroup (the
-// kernel variant with part synchronisation; requires mirror)
+// kernel variants with part synchronisation)
 hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int grid, int waves_per_block, bool mirror,
                         bool split);
 int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds, bool split);

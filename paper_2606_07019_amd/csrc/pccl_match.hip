@@ -662,9 +662,9 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
 {
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t n = ds.n, d = ds.d;
-    // (only the kernel variant built for split destinations, which keeps
-    // needs rows in LDS, takes parts; the host deals parts to no other)
-    const bool split = SPLIT && MIRROR && ds.nparts > 1;
+    // (only the kernel variants built for split destinations take parts;
+    // the host deals parts to no other)
+    const bool split = SPLIT && ds.nparts > 1;
     if (n == 0 && !split) return;
     // Wp: row stride; Ws: where scans end (bits past the last chunk are zero
     // in both rows, so no candidate lies beyond the row's own words)
@@ -1107,9 +1107,12 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
                     tb.tim[i] = ds.tim;
                     tb.lid[i] = ds.lid;
                 }
+                // (the ballot is taken by the whole wave, not inside the
+                // lane-0 branch, where it would see lane 0 alone)
+                const uint64_t lost = __ballot(act && !win);
                 if (lane == 0) {
                     gs.wcnt[ds.part] = (uint32_t)__popcll(wm);
-                    gs.flag[ds.part] = (actm ? 1u : 0u) | (__ballot(act && !win) ? 2u : 0u);
+                    gs.flag[ds.part] = (actm ? 1u : 0u) | (lost ? 2u : 0u);
                 }
                 __syncthreads();
                 bool any_act = false;
@@ -1242,16 +1245,19 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             // the delivered chunks are no longer needed: clear their flags
             // (each entry is compared with the winners' picks, read from
             // their lanes)
+            // (wave-uniform loops: the winners' picks are read lane by lane)
             if (!split && (n_arr | n_unf) && wins) {
-                for (uint32_t q = lane; q < n_arr; q += 64) {
-                    const uint32_t c = ws.arr_c[q];
+                for (uint32_t q0 = 0; q0 < n_arr; q0 += 64) {
+                    const uint32_t q = q0 + lane;
+                    const uint32_t c = q < n_arr ? ws.arr_c[q] : NONE32;
                     bool hit = false;
                     for (uint64_t wm = wins; wm; wm &= wm - 1)
                         hit |= readlane32(pk, (uint32_t)__builtin_ffsll((long long)wm) - 1u) == c;
                     if (hit) ws.arr_need[q] = 0;
                 }
-                for (uint32_t q = lane; q < n_unf; q += 64) {
-                    const uint32_t c = ws.unf_c[q];
+                for (uint32_t q0 = 0; q0 < n_unf; q0 += 64) {
+                    const uint32_t q = q0 + lane;
+                    const uint32_t c = q < n_unf ? ws.unf_c[q] : NONE32;
                     bool hit = false;
                     for (uint64_t wm = wins; wm; wm &= wm - 1)
                         hit |= readlane32(pk, (uint32_t)__builtin_ffsll((long long)wm) - 1u) == c;
@@ -1322,10 +1328,13 @@ __device__ __forceinline__ void look_ahead_late(const Layout &ly, const Sizes &s
 
 // MIRROR: every wave owns one destination for the whole run and keeps its
 // needs row in LDS (the host checks both).  SPLIT: some destinations are
-// split over the waves of a workgroup (only with MIRROR; a separate build of
-// the kernel, so that the others carry none of the part synchronisation).
+// split over the waves of a workgroup (a separate build of the kernel, so
+// that the others carry none of the part synchronisation; it needs every
+// wave resident, so the build that keeps needs rows in device memory is
+// held to two workgroups per compute unit, spilling registers, to keep one
+// wave per destination on the largest topologies).
 template <bool MIRROR, bool SPLIT>
-__global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
+__global__ void __launch_bounds__(NT, (!MIRROR && SPLIT) ? 2 : 1) k_match(Layout ly, Sizes sz)
 {
     __shared__ BlockShared sh;
     Control *ctl = ly.ctl;
@@ -1341,9 +1350,10 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
     // every wave owns at most one destination (or part of one): its state
     // stays on chip
     const bool resident = sz.resident != 0;
-    // (the host picks that kernel only with one destination per wave and a
-    // holds bitmap the buffer descriptor spans)
-    if (MIRROR && (!resident || sz.hbytes == 0)) {
+    // (the host picks the kernels with needs rows in LDS or with split
+    // destinations only with one destination per wave, and the first only
+    // with a holds bitmap the buffer descriptor spans)
+    if ((MIRROR && (!resident || sz.hbytes == 0)) || (SPLIT && !resident)) {
         if (blockIdx.x == 0 && tid == 0) record_error(ctl, ST_EINTERNAL, 2, 0, 0);
         return;
     }
@@ -1457,7 +1467,9 @@ __global__ void __launch_bounds__(NT) k_match(Layout ly, Sizes sz)
 namespace {
 const void *match_kernel(bool mirror, bool split)
 {
-    if (split) return reinterpret_cast<const void *>(k_match<true, true>);
+    if (split)
+        return mirror ? reinterpret_cast<const void *>(k_match<true, true>)
+                      : reinterpret_cast<const void *>(k_match<false, true>);
     return mirror ? reinterpret_cast<const void *>(k_match<true, false>) : reinterpret_cast<const void *>(k_match<false, false>);
 }
 }  // namespace
@@ -1485,7 +1497,6 @@ hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int g
                         bool split)
 {
     if (waves_per_block < 1 || waves_per_block > (int)NWAVES) return hipErrorInvalidValue;
-    if (split && !mirror) return hipErrorInvalidValue;
     const size_t dyn = mirror ? (size_t)waves_per_block * sz.Wp * sizeof(uint64_t) : 0;
     const void *kern = match_kernel(mirror, split);
     if (dyn) {

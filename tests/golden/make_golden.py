@@ -6,7 +6,7 @@ canonical schedule (uint32 little-endian rows: link, chunk, t_start, flags)
 and 512 evenly spaced schedule rows, so GPU tests at full size can compare
 element by element on the samples and bit-exactly through the digest.
 
-    python tests/golden/make_golden.py [k ...]
+    python tests/golden/make_golden.py [k ...]     # k = 1..5 or a name in EXTRA
 """
 
 import hashlib
@@ -31,8 +31,18 @@ def digest(sends: np.ndarray) -> str:
     return hashlib.sha256(np.ascontiguousarray(sends, dtype="<u4").tobytes()).hexdigest()
 
 
-def make(k: int) -> dict:
-    wl = W.CONFIGS[k]()
+# Workloads beyond the five benchmark shapes, digested the same way
+# (file tests/golden/<name>.json).
+EXTRA = {
+    # 128 nodes x 8 NPUs, rail switches with 128 ports each (Sec. 4.7; the
+    # 2D Switch family of Sec. 6.2), All-to-All of 128 KiB chunks
+    "rail1024": lambda: W.Workload("switch2level_1024_a2a_128KiB", W.switch2level(128, 8),
+                                   W.a2a_bitmaps(1024, 128 << 10), 0),
+}
+
+
+def make(k) -> dict:
+    wl = EXTRA[k]() if k in EXTRA else W.CONFIGS[k]()
     t0 = time.time()
     r = O.run_workload(wl)
     dt = time.time() - t0
@@ -53,9 +63,10 @@ def make(k: int) -> dict:
 
 
 if __name__ == "__main__":
-    ks = [int(a) for a in sys.argv[1:]] or [1, 2, 3, 4, 5]
+    ks = [a if a in EXTRA else int(a) for a in sys.argv[1:]] or [1, 2, 3, 4, 5]
     for k in ks:
         g = make(k)
-        with open(os.path.join(HERE, f"config{k}.json"), "w") as f:
+        name = k if k in EXTRA else f"config{k}"
+        with open(os.path.join(HERE, f"{name}.json"), "w") as f:
             json.dump(g, f, indent=1)
         print(k, g["workload"], g["n_sends"], g["collective_time_ns"], g["oracle_seconds"], "s", flush=True)

@@ -77,3 +77,85 @@ def _hub_graph(seed, n_hub_in):
 @pytest.mark.parametrize("seed,n_hub_in", [(0, 70), (1, 100), (2, 130), (3, 190), (4, 250), (5, 64), (6, 66)])
 def test_hub_in_links(seed, n_hub_in):
     _compare(_hub_graph(seed, n_hub_in), "hub")
+
+
+def _sparse_wide(topo, n_npus, n_chunks, n_used, seed, name, max_dests=6):
+    # n_chunks columns (rows too wide for LDS next to a second wave's), of
+    # which n_used random ones are held by one random NPU and needed by 1 to
+    # max_dests others; the rest are held and needed by nobody
+    rng = np.random.default_rng(seed)
+    used = np.sort(rng.choice(n_chunks, size=n_used, replace=False))
+    src_of = [None] * n_chunks
+    dests_of = [()] * n_chunks
+    for c in used:
+        s = int(rng.integers(n_npus))
+        ds = set(int(x) for x in rng.integers(n_npus, size=int(rng.integers(1, max_dests + 1)))) - {s}
+        src_of[int(c)] = s
+        dests_of[int(c)] = sorted(ds)
+    coll = W.collective_from_lists(n_npus, n_chunks, 32 << 10, src_of, dests_of, [list(range(n_npus))])
+    return W.Workload(name, topo, coll, seed)
+
+
+def _cluster_hub(n_clusters, size):
+    # clusters of `size` NPUs, fully meshed by fast links, every NPU also
+    # linked to one hub NPU and back by slow ones: a chunk spreads through its
+    # cluster first, then several of the hub's in-links offer it at once, so
+    # the parts of the split hub pick the same chunks and clash
+    n = n_clusters * size
+    hub = n
+    pairs, alpha, bw = [], [], []
+    for c in range(n_clusters):
+        m = range(c * size, (c + 1) * size)
+        for i in m:
+            for j in m:
+                if i != j:
+                    pairs.append((i, j)); alpha.append(100); bw.append(400)
+    for i in range(n):
+        pairs += [(i, hub), (hub, i)]
+        alpha += [700, 700]
+        bw += [50, 50]
+    return W.make_topology(n + 1, 0, pairs, alpha, bw)
+
+
+def _cluster_hub_collective(n_clusters, size, n_chunks, n_used, seed):
+    # each used chunk starts on one NPU and is needed by its whole cluster
+    # and by the hub
+    rng = np.random.default_rng(seed)
+    n = n_clusters * size
+    used = np.sort(rng.choice(n_chunks, size=n_used, replace=False))
+    src_of = [None] * n_chunks
+    dests_of = [()] * n_chunks
+    for c in used:
+        s = int(rng.integers(n))
+        k = s // size
+        src_of[int(c)] = s
+        dests_of[int(c)] = [v for v in range(k * size, (k + 1) * size) if v != s] + [n]
+    return W.collective_from_lists(n + 1, n_chunks, 32 << 10, src_of, dests_of, [list(range(n + 1))])
+
+
+@pytest.mark.parametrize("n_clusters,size,C,seed", [(6, 10, 30, 0), (6, 10, 200, 0), (13, 10, 4000, 0), (16, 8, 5000, 1), (13, 10, 600_000, 2)])
+def test_cluster_hub_clashes(n_clusters, size, C, seed):
+    # clashes between the links of a split device, inside a part and across
+    # parts (the 6 x 10 hub has 60 in-links but 600 arrival pairs, so two
+    # parts; a part whose lane 0 is not among its losers must still run
+    # another pick round for them); the last case with rows too wide for LDS
+    wl = W.Workload(f"clusterhub{n_clusters}x{size}_c{C}", _cluster_hub(n_clusters, size),
+                    _cluster_hub_collective(n_clusters, size, C, min(C, 3000), seed), seed)
+    _compare(wl, "cluster hub")
+
+
+@pytest.mark.parametrize("kind,seed", [("star128", 0), ("rails96x2", 1), ("hub130", 2), ("star256", 3)])
+def test_split_with_rows_in_device_memory(kind, seed):
+    # 600,000 chunks: a needs row is 75 KB, so the waves of a split device
+    # cannot keep it in LDS and the kernel reads it from device memory
+    C = 600_000
+    if kind == "star128":
+        topo, n = W.star(128), 128
+    elif kind == "star256":
+        topo, n = W.star(256), 256
+    elif kind == "rails96x2":
+        topo, n = W.switch2level(96, 2), 192
+    else:
+        hub = _hub_graph(seed, 130)
+        topo, n = hub.topo, hub.topo.n_npus
+    _compare(_sparse_wide(topo, n, C, 3000, seed, f"{kind}_wide{C}"), "rows in device memory")
