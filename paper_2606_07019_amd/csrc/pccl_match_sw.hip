@@ -36,12 +36,14 @@ constexpr uint32_t SCAN_STEP = 4;  // row words one link's scan loads at once
 constexpr uint32_t PEND = 4;       // needed chunks below a link's cursor it keeps as explicit candidates
 static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
+constexpr uint32_t SW_FILTER_WORDS = 512;  // 16,384 filter bits, shared by the group's unicast switches
+
+static_assert(SW_MAX_LINKS <= SW_THREADS, "the pick stage gives link i to thread i");
 
 struct SwShared {
     // per group link: state, static description and per-round scratch
     uint32_t busy[SW_MAX_LINKS], infl[SW_MAX_LINKS], cur[SW_MAX_LINKS], pick[SW_MAX_LINKS];
     uint32_t lsrc[SW_MAX_LINKS], ldst[SW_MAX_LINKS], ltim[SW_MAX_LINKS], llink[SW_MAX_LINKS];
-    uint32_t lslot[SW_MAX_LINKS];
     uint16_t ldl[SW_MAX_LINKS], lsrcj[SW_MAX_LINKS];
     uint8_t luni[SW_MAX_LINKS], ldbuf[SW_MAX_LINKS], lsbuf[SW_MAX_LINKS];
     uint8_t win1[SW_MAX_LINKS], win2[SW_MAX_LINKS], win3[SW_MAX_LINKS];
@@ -57,6 +59,15 @@ struct SwShared {
     uint16_t bpoff[SW_MAX_SW + 1], booff[SW_MAX_SW + 1];
     uint32_t bout[SW_MAX_LINKS];
     uint32_t pc[SW_MAX_POOL], pn[SW_MAX_POOL], occ[SW_MAX_SW];
+    // chunks each unicast switch of the group may have in flight (a hashed
+    // bit set per switch, a superset: a hit is checked against the links)
+    uint32_t filt[SW_FILTER_WORDS];
+    // per wave: its links that scan their row in this pick round, in lane order
+    uint8_t wsl[SWAVES][64];
+    // per unicast switch: its out-links that won their destination's clash
+    // in this pick round ([uoff[u], uoff[u] + ucnt[u]) of uwin)
+    uint16_t uwin[SW_MAX_LINKS];
+    uint32_t ucnt[SW_MAX_SW];
     uint32_t red[SWAVES];
     uint32_t x_tmin, x_err, x_ok;
     unsigned long long x_sent;
@@ -194,7 +205,7 @@ __device__ void fold_and_publish(const Layout &ly, const Sizes &sz, const SwGrou
                                  const SwShared &sh, bool in_lds)
 {
     for (uint32_t i = threadIdx.x; i < gp.nL; i += ST) {
-        const uint32_t sl = in_lds ? sh.lslot[i] : ly.sw.lk_slot[gp.lbase + i];
+        const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
         const uint32_t d = in_lds ? sh.ldst[i] : ly.ldst[ly.slot_link[sl]];
         const uint64_t e = ly.snap[sl];
         if (e != NONE64 && (uint32_t)e < t0) {
@@ -214,7 +225,6 @@ __device__ void load_group_state(const Layout &ly, const Sizes &sz, const SwGrou
     const uint32_t tid = threadIdx.x;
     for (uint32_t i = tid; i < gp.nL; i += ST) {
         const uint32_t x = gp.lbase + i, sl = sw.lk_slot[x], l = ly.slot_link[sl];
-        sh.lslot[i] = sl;
         sh.llink[i] = l;
         sh.lsrc[i] = ly.lsrc[l];
         sh.ldst[i] = ly.ldst[l];
@@ -266,6 +276,46 @@ __device__ inline bool sending(const SwShared &sh, uint32_t u, uint32_t c, uint3
     return false;
 }
 
+__device__ inline void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The sending filter: SW_FILTER_WORDS * 32 bits split evenly over the
+// group's unicast switches (a power of two each, at least 256 with the
+// group limit of 64 switches); chunk c of switch u sets one hashed bit.
+__device__ inline uint32_t filter_log2(uint32_t n_uni)
+{
+    const uint32_t per = (SW_FILTER_WORDS * 32u) / max(n_uni, 1u);
+    return 31u - (uint32_t)__builtin_clz(per);
+}
+
+__device__ inline uint32_t filter_bit(uint32_t u, uint32_t c, uint32_t fl)
+{
+    return (u << fl) + ((c * 2654435761u) >> (32u - fl));
+}
+
+// Is chunk c in flight on an out-link of unicast switch u at time t?  The
+// filter answers "no" for most chunks without walking the links.
+__device__ inline bool sent_by(const SwShared &sh, uint32_t u, uint32_t c, uint32_t t, uint32_t fl)
+{
+    const uint32_t b = filter_bit(u, c, fl);
+    return ((sh.filt[b >> 5] >> (b & 31u)) & 1u) && sending(sh, u, c, t);
+}
+
+// Bits of word w (chunks 64 w .. 64 w + 63) that lie in [lo, hi).
+__device__ inline uint64_t range_bits(uint64_t w, uint32_t lo, uint32_t hi)
+{
+    const uint64_t b0 = w * 64;
+    uint64_t m = ~0ull;
+    if (b0 + 64 <= lo || b0 >= hi) return 0ull;
+    if (b0 < lo) m &= ~0ull << (lo - b0);
+    if (b0 + 64 > hi) m &= ~0ull >> (b0 + 64 - hi);
+    return m;
+}
+
 // The pick of free link i at event t (the BFS step: the first chunk in
 // priority order that the source holds and the destination still needs),
 // skipping chunks its unicast source switch is already sending.  Candidates
@@ -276,7 +326,9 @@ __device__ inline bool sending(const SwShared &sh, uint32_t u, uint32_t c, uint3
 // this workgroup clears bits of its destinations' rows and nothing sets them
 // while matching, so a cached word can only show a chunk as still needed.
 // The lowest candidate is confirmed with one coherent load; a stale one is
-// dropped where it came from and the pick repeats.
+// dropped where it came from and the pick repeats.  (One thread per link,
+// serial: the pick stage below shares the row scans out among the lanes of
+// a wave and calls this only when its candidate turns out stale.)
 __device__ uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, uint32_t i, uint32_t t,
                               unsigned long long &words)
 {
@@ -438,6 +490,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     }
     __syncthreads();
     int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
+    const uint32_t fl = filter_log2(gp.nU);
     for (;;) {
         // next event of the group: a transfer into it ends, or a chunk
         // arrives at one of its sources (time 0 opens the first window)
@@ -452,15 +505,147 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         }
         const uint32_t t = block_min(sh, m);
         if (t == NONE32) break;
-        for (;;) {
-            // picks of the free links; a full buffer admits nothing
+        if (gp.nU) {
+            // the chunks in flight on the unicast switches' out-links at t
+            // (commits at t add theirs as they happen)
+            const uint32_t nfw = (gp.nU << fl) >> 5;
+            for (uint32_t x = tid; x < nfw; x += ST) sh.filt[x] = 0u;
+            __syncthreads();
             for (uint32_t i = tid; i < gp.nL; i += ST) {
-                uint32_t pk = NONE32;
-                if (sh.busy[i] <= t) {
-                    const uint32_t b = sh.ldbuf[i];
-                    if (b == SW_NONE8 || sh.occ[b] < sh.bcap[b]) pk = pick_link(ly, sz, sh, i, t, acc.words);
+                const uint32_t u = sh.luni[i];
+                if (u != SW_NONE8 && sh.infl[i] != NONE32 && sh.busy[i] > t) {
+                    const uint32_t b = filter_bit(u, sh.infl[i], fl);
+                    atomicOr(&sh.filt[b >> 5], 1u << (b & 31u));
                 }
-                sh.pick[i] = pk;
+            }
+            __syncthreads();
+        }
+        for (;;) {
+            // picks of the free links (a full buffer admits nothing), in three
+            // steps inside each wave: every free link's lowest explicit
+            // candidate (pending or arrived); the row scans below it, shared
+            // out among the wave's lanes; the lower of the two, confirmed
+            // with one coherent load (thread tid owns link tid)
+            {
+                const uint32_t i = tid, lane = tid & 63u, wave = tid >> 6;
+                bool free = false;
+                uint32_t u = NONE32, bxv = NONE32, cu = 0, lim = 0;
+                const uint64_t *nd = ly.needs;
+                if (i < gp.nL && sh.busy[i] <= t) {
+                    const uint32_t b = sh.ldbuf[i];
+                    free = b == SW_NONE8 || sh.occ[b] < sh.bcap[b];
+                }
+                if (free) {
+                    nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
+                    u = sh.luni[i] == SW_NONE8 ? NONE32 : sh.luni[i];
+                    // earlier arrivals kept below the cursor (needs words
+                    // loaded together, word 0 for an empty entry)
+                    uint64_t pw[PEND];
+#pragma unroll
+                    for (uint32_t e = 0; e < PEND; e++) {
+                        const uint32_t c = sh.pend[i][e];
+                        pw[e] = nd[(c == NONE32 ? 0u : c) >> 6];
+                    }
+#pragma unroll
+                    for (uint32_t e = 0; e < PEND; e++) {
+                        const uint32_t c = sh.pend[i][e];
+                        if (c == NONE32 || c >= bxv) continue;
+                        if (!((pw[e] >> (c & 63u)) & 1ull)) {
+                            sh.pend[i][e] = NONE32;
+                            continue;
+                        }
+                        if (u != NONE32 && sent_by(sh, u, c, t, fl)) continue;
+                        bxv = c;
+                    }
+                    // arrivals up to t that the destination may still need
+                    const uint32_t base = sh.poff[sh.lsrcj[i]];
+                    for (uint64_t y = sh.amask[i]; y; y &= y - 1) {
+                        const uint32_t p = base + (uint32_t)__builtin_ctzll(y), c = sh.arr_c[p];
+                        if (sh.arr_t[p] > t || c >= bxv) continue;
+                        if (u != NONE32 && sent_by(sh, u, c, t, fl)) continue;
+                        bxv = c;
+                    }
+                    // the row matters below the explicit candidate only
+                    cu = sh.cur[i];
+                    lim = min(sh.hi[i], bxv);
+                }
+                const bool scan = free && cu < lim;
+                const uint64_t smask = __ballot(scan);
+                if (smask) {
+                    // G = 64 / next_pow2(k) lanes per scanning link, two
+                    // words per lane per step; a min over each lane group
+                    // gives the first hit (the new cursor) and the first hit
+                    // the source switch is not sending (the row candidate)
+                    if (scan) sh.wsl[wave][__popcll(smask & ((1ull << lane) - 1ull))] = (uint8_t)lane;
+                    wave_sync();
+                    const uint32_t ks = (uint32_t)__popcll(smask);
+                    const uint32_t lg = ks <= 1u ? 0u : 32u - (uint32_t)__builtin_clz(ks - 1u);
+                    const uint32_t G = 64u >> lg, g = lane >> (6u - lg), sub = lane & (G - 1u);
+                    const bool act = g < ks;
+                    const uint32_t jl = sh.wsl[wave][act ? g : 0u];
+                    const uint32_t cj = (uint32_t)__shfl((int)cu, (int)jl);
+                    const uint32_t lj = (uint32_t)__shfl((int)lim, (int)jl);
+                    const uint32_t uj = (uint32_t)__shfl((int)u, (int)jl);
+                    const uint32_t ij = (wave << 6) | jl;
+                    const uint64_t *hrow = ly.holds + (uint64_t)sh.lsrc[ij] * sz.Wp;
+                    const uint64_t *nrow = ly.needs + (uint64_t)sh.ldst[ij] * sz.Wp;
+                    const uint64_t wl = ((uint64_t)lj + 63u) >> 6;
+                    uint64_t pos = (cj >> 6) & ~1ull;
+                    bool live = act && cj < lj;
+                    uint32_t fh = NONE32, rc = NONE32;
+                    while (__ballot(live)) {
+                        // loads at a clamped, always valid word pair (rows
+                        // have an even number of words), masked after
+                        const uint64_t w = pos + 2ull * sub;
+                        const uint64_t wc = min<uint64_t>(w, sz.Wp - 2);
+                        const uint4 hv = *reinterpret_cast<const uint4 *>(hrow + wc);
+                        const uint4 nv = *reinterpret_cast<const uint4 *>(nrow + wc);
+                        uint32_t lfh = NONE32, lrc = NONE32;
+                        if (live && w < wl) {
+                            uint64_t a[2];
+                            a[0] = ((((uint64_t)hv.y << 32) | hv.x) & (((uint64_t)nv.y << 32) | nv.x)) &
+                                   range_bits(w, cj, lj);
+                            a[1] = ((((uint64_t)hv.w << 32) | hv.z) & (((uint64_t)nv.w << 32) | nv.z)) &
+                                   range_bits(w + 1, cj, lj);
+                            acc.words += 2;
+#pragma unroll
+                            for (uint32_t k = 0; k < 2; k++) {
+                                for (uint64_t y = lrc == NONE32 ? a[k] : 0ull; y; y &= y - 1) {
+                                    const uint32_t c = (uint32_t)((w + k) * 64 + (uint64_t)__builtin_ctzll(y));
+                                    if (lfh == NONE32) lfh = c;
+                                    if (uj == NONE32 || !sent_by(sh, uj, c, t, fl)) {
+                                        lrc = c;
+                                        break;
+                                    }
+                                }
+                            }
+                        }
+                        for (uint32_t off = 1; off < G; off <<= 1) {
+                            lfh = min(lfh, (uint32_t)__shfl_xor((int)lfh, (int)off));
+                            lrc = min(lrc, (uint32_t)__shfl_xor((int)lrc, (int)off));
+                        }
+                        if (live) {
+                            fh = min(fh, lfh);
+                            rc = lrc;
+                            pos += 2ull * G;
+                            if (lrc != NONE32 || pos >= wl) live = false;
+                        }
+                    }
+                    if (act && sub == 0) {
+                        sh.pick[ij] = rc;
+                        sh.cur[ij] = fh != NONE32 ? fh : max(cj, lj);
+                    }
+                    wave_sync();
+                }
+                uint32_t pk = NONE32;
+                if (free) {
+                    pk = min(scan ? sh.pick[i] : NONE32, bxv);
+                    // a candidate delivered since its needs word was cached:
+                    // the serial pick drops it and finds the next one
+                    if (pk != NONE32 && !need_bit(nd, pk)) pk = pick_link(ly, sz, sh, i, t, acc.words);
+                }
+                if (i < gp.nU) sh.ucnt[i] = 0u;
+                if (i < gp.nL) sh.pick[i] = pk;
             }
             __syncthreads();
             // clash on (destination, chunk): fastest link, then lowest id
@@ -476,6 +661,8 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         if (j != i && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
                     }
                     if (first) acc.rounds++;
+                    const uint32_t u = sh.luni[i];
+                    if (w && u != SW_NONE8) sh.uwin[sh.uoff[u] + atomicAdd(&sh.ucnt[u], 1u)] = (uint16_t)i;
                 }
                 sh.win1[i] = w;
             }
@@ -487,9 +674,9 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 if (w && u != SW_NONE8) {
                     const uint32_t pk = sh.pick[i];
                     const uint64_t key = link_key(sh, i);
-                    for (uint32_t q = sh.uoff[u]; q < sh.uoff[u + 1]; q++) {
-                        const uint32_t j = sh.ulist[q];
-                        if (j != i && sh.win1[j] && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
+                    for (uint32_t q = sh.uoff[u], qe = q + sh.ucnt[u]; q < qe; q++) {
+                        const uint32_t j = sh.uwin[q];
+                        if (j != i && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
                     }
                 }
                 sh.win2[i] = w;
@@ -541,6 +728,11 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 const uint32_t e32 = end > 0xFFFFFFFFull ? NONE32 - 1u : (uint32_t)end;
                 sh.busy[i] = e32;
                 sh.infl[i] = pk;
+                const uint32_t u = sh.luni[i];
+                if (u != SW_NONE8) {
+                    const uint32_t fb = filter_bit(u, pk, fl);
+                    atomicOr(&sh.filt[fb >> 5], 1u << (fb & 31u));
+                }
                 acc.cstar = max(acc.cstar, e32);
                 const unsigned long long q = atomicAdd(&ly.dest_log[d], 1ull);
                 ly.skey[0][q] = ((uint64_t)t << 32) | sh.llink[i];
@@ -607,7 +799,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         sh.hi[i] = h;
         if (sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1) tm = min(tm, sh.busy[i]);
         if (!resident) {
-            const uint32_t sl = sh.lslot[i];
+            const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
             ly.cur[sl] = c;
             ly.lflags[sl] = (uint32_t)(sz.W * 64) - h;
             ly.busy[sl] = sh.busy[i];
