@@ -185,9 +185,10 @@ pccl_status pccl_set_collective(pccl_ctx *ctx, uint32_t n_chunks, uint64_t chunk
  * out-neighbours, and a limited switch together with its out-neighbours,
  * form one group.  PCCL_EUNSUPPORTED (from pccl_workspace_bytes /
  * pccl_set_workspace) when a group has more than 1024 in-links, 1024
- * distinct sources of those links, 8192 in-links of those sources, 64 limited
- * or unicast switches, or more than 1024 buffer places (capacities at or
- * above the chunk count count as unlimited).  Buffers can deadlock: then
+ * distinct sources of those links, 8192 in-links of those sources, a source
+ * with more than 64 in-links, 64 limited or unicast switches, or more than
+ * 1024 buffer places (capacities at or above the chunk count count as
+ * unlimited).  Buffers can deadlock: then
  * pccl_synthesize returns PCCL_EDEADLOCK.  PCCL_EINVAL on a count mismatch.
  */
 pccl_status pccl_set_switch_model(pccl_ctx *ctx, uint32_t n_switches, const uint32_t *buffer_chunks,

@@ -375,6 +375,10 @@ pccl_status build_switch_tables(pccl_ctx *c)
         if (np > SW_MAX_PAIRS)
             return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u: its sources have %u in-links (limit %u)",
                         mem[0], np, SW_MAX_PAIRS);
+        for (uint32_t sv : srcs)
+            if (c->in_off[sv + 1] - c->in_off[sv] > SW_MAX_SRC_IN)
+                return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u: source %u has %u in-links (limit %u)",
+                            mem[0], sv, c->in_off[sv + 1] - c->in_off[sv], SW_MAX_SRC_IN);
         if (nu > SW_MAX_SW || nb > SW_MAX_SW)
             return fail(c, PCCL_EUNSUPPORTED, "switch group of device %u has %u unicast and %u limited switches "
                         "(limit %u each)", mem[0], nu, nb, SW_MAX_SW);

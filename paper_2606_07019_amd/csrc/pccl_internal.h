@@ -33,6 +33,7 @@ constexpr uint32_t SW_MAX_LINKS = 1024;  // in-links of the destinations of one 
 constexpr uint32_t SW_MAX_SRC = 1024;    // distinct sources of those links
 constexpr uint32_t SW_MAX_PAIRS = 8192;  // in-links of those sources (arrival slots)
 constexpr uint32_t SW_MAX_SW = 64;       // unicast or limited switches in one group
+constexpr uint32_t SW_MAX_SRC_IN = 64;   // in-links of one source of a group link (one bit each in a link's arrival mask)
 constexpr uint32_t SW_MAX_POOL = 1024;   // buffer places of a group's limited switches
 constexpr uint8_t SW_NONE8 = 0xFF;
 

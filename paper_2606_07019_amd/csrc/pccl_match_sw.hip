@@ -33,10 +33,11 @@ constexpr uint32_t ST = SW_THREADS;
 constexpr uint32_t SWAVES = ST / 64;
 constexpr uint32_t SW_SPIN_LIMIT = 1u << 24;
 constexpr uint32_t SCAN_STEP = 4;  // row words one link's scan loads at once
-constexpr uint32_t PEND = 4;       // needed chunks below a link's cursor it keeps as explicit candidates
+constexpr uint32_t PEND = 2;       // needed chunks below a link's cursor it keeps as explicit candidates
 static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
 constexpr uint32_t SW_FILTER_WORDS = 512;  // 16,384 filter bits, shared by the group's unicast switches
+constexpr uint32_t SW_HASH_WORDS = 256;    // 4,096 two-bit slots per clash table
 
 static_assert(SW_MAX_LINKS <= SW_THREADS, "the pick stage gives link i to thread i");
 
@@ -46,7 +47,9 @@ struct SwShared {
     uint32_t lsrc[SW_MAX_LINKS], ldst[SW_MAX_LINKS], ltim[SW_MAX_LINKS], llink[SW_MAX_LINKS];
     uint16_t ldl[SW_MAX_LINKS], lsrcj[SW_MAX_LINKS];
     uint8_t luni[SW_MAX_LINKS], ldbuf[SW_MAX_LINKS], lsbuf[SW_MAX_LINKS];
-    uint8_t win1[SW_MAX_LINKS], win2[SW_MAX_LINKS], win3[SW_MAX_LINKS];
+    // a link's pick in this round won: bit 0 its destination's clash, bit 1
+    // also its unicast source switch's, bit 2 also a buffer place
+    uint8_t winf[SW_MAX_LINKS];
     uint16_t doff[SW_MAX_LINKS + 1];  // links of destination dl: [doff[dl], doff[dl + 1])
     uint16_t poff[SW_MAX_SRC + 1];    // arrival pairs of source j
     uint32_t arr_t[SW_MAX_PAIRS];     // arrival time inside the window, NONE32 if none
@@ -68,6 +71,13 @@ struct SwShared {
     // in this pick round ([uoff[u], uoff[u] + ucnt[u]) of uwin)
     uint16_t uwin[SW_MAX_LINKS];
     uint32_t ucnt[SW_MAX_SW];
+    // per pick round: hashed (destination, chunk) and (unicast switch,
+    // chunk) tables of two-bit "seen once / seen again" marks, so that a pick
+    // alone in its slot skips the comparison with its rivals; and one bit per
+    // destination that picked (rounds are counted per such destination)
+    uint32_t hd[SW_HASH_WORDS], hu[SW_HASH_WORDS], dpk[SW_MAX_LINKS / 32];
+    // next send-log slot of each destination of the group (its segment)
+    unsigned long long lcur[SW_MAX_LINKS];
     uint32_t red[SWAVES];
     uint32_t x_tmin, x_err, x_ok;
     unsigned long long x_sent;
@@ -263,6 +273,8 @@ __device__ void load_group_state(const Layout &ly, const Sizes &sz, const SwGrou
     for (uint32_t x = tid; x < nul; x += ST) sh.ulist[x] = (uint16_t)sw.u_list[gp.ulbase + x];
     const uint32_t nbo = gp.nB ? sh.booff[gp.nB] : 0u;
     for (uint32_t x = tid; x < nbo; x += ST) sh.bout[x] = sw.b_out[gp.bobase + x];
+    for (uint32_t x = tid; x < gp.nD; x += ST)
+        if (sh.doff[x] < sh.doff[x + 1]) sh.lcur[x] = ly.dest_log[sh.ldst[sh.doff[x]]];
 }
 
 // A unicast switch keeps one copy of a chunk in flight: is chunk c in flight
@@ -303,6 +315,25 @@ __device__ inline bool sent_by(const SwShared &sh, uint32_t u, uint32_t c, uint3
 {
     const uint32_t b = filter_bit(u, c, fl);
     return ((sh.filt[b >> 5] >> (b & 31u)) & 1u) && sending(sh, u, c, t);
+}
+
+// Slot of (owner, chunk) in a clash table, and its marks: the first insert
+// sets bit 0 of the slot, any later one bit 1.  A slot whose bit 1 is clear
+// after all inserts holds one pick only.
+__device__ inline uint32_t clash_slot(uint32_t owner, uint32_t c)
+{
+    return ((c ^ (owner * 0x9E3779B9u)) * 2654435761u) >> 20;  // 12 bits
+}
+
+__device__ inline void clash_mark(uint32_t *tab, uint32_t slot)
+{
+    const uint32_t b = 1u << ((slot & 15u) * 2u);
+    if (atomicOr(&tab[slot >> 4], b) & b) atomicOr(&tab[slot >> 4], b << 1);
+}
+
+__device__ inline bool clash_alone(const uint32_t *tab, uint32_t slot)
+{
+    return !((tab[slot >> 4] >> ((slot & 15u) * 2u + 1u)) & 1u);
 }
 
 // Bits of word w (chunks 64 w .. 64 w + 63) that lie in [lo, hi).
@@ -456,38 +487,53 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             sh.arr_c[p] = (uint32_t)(e[k] >> 32);
         }
     }
+    __syncthreads();
+    // which arrivals each link's destination may still need: each link walks
+    // its source's pairs (at most 64) in LDS and loads the needs words of the
+    // live ones eight at a time, all in flight together (through the caches,
+    // a superset: picks confirm each candidate)
+    const uint32_t share = gp.nL && gp.nL <= ST / 2 ? 2u : 1u;
     for (uint32_t i = tid; i < gp.nL; i += ST) sh.amask[i] = 0ull;
     __syncthreads();
-    // which arrivals each link's destination may still need: (link, pair)
-    // items spread over the workgroup, need words loaded four at a time
-    // through the caches (a superset: picks confirm each candidate)
-    const uint32_t nx = gp.nL * 64u;
-    for (uint32_t x0 = tid; x0 < nx; x0 += 4u * ST) {
-        bool v[4];
-        uint32_t c[4];
-        const uint64_t *row[4];
+    for (uint32_t x = tid; x < gp.nL * share; x += ST) {
+        const uint32_t i = x % gp.nL, half = x / gp.nL;
+        const uint32_t j = sh.lsrcj[i], p0 = sh.poff[j], np = sh.poff[j + 1] - p0;
+        const uint64_t *nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
+        // the pairs with an arrival (this thread's half of them when shared)
+        uint64_t live = 0;
+        for (uint32_t q0 = 0; q0 < np; q0 += 8) {
+            uint32_t a[8];
 #pragma unroll
-        for (uint32_t k = 0; k < 4; k++) {
-            const uint32_t x = x0 + k * ST, i = x >> 6, j = i < gp.nL ? sh.lsrcj[i] : 0u;
-            const uint32_t p = i < gp.nL ? sh.poff[j] + (x & 63u) : 0u;
-            v[k] = x < nx && p < sh.poff[j + 1] && sh.arr_t[p] != NONE32;
-            c[k] = v[k] ? sh.arr_c[p] : 0u;
-            row[k] = ly.needs + (uint64_t)(v[k] ? sh.ldst[i] : 0u) * sz.Wp;
+            for (uint32_t k = 0; k < 8; k++) a[k] = sh.arr_t[p0 + min(q0 + k, np - 1u)];
+#pragma unroll
+            for (uint32_t k = 0; k < 8; k++)
+                if (q0 + k < np && a[k] != NONE32 && ((q0 + k) % share) == half) live |= 1ull << (q0 + k);
         }
-        // unconditional loads (row 0, word 0 for an empty item), so that all
-        // four are in flight together
-        uint64_t nw[4];
+        uint64_t m = 0;
+        while (live) {
+            uint32_t q[8], c[8];
 #pragma unroll
-        for (uint32_t k = 0; k < 4; k++) nw[k] = row[k][c[k] >> 6];
-#pragma unroll
-        for (uint32_t k = 0; k < 4; k++) v[k] = v[k] && ((nw[k] >> (c[k] & 63u)) & 1ull);
-#pragma unroll
-        for (uint32_t k = 0; k < 4; k++)
-            if (v[k]) {
-                const uint32_t x = x0 + k * ST;
-                atomicOr((unsigned long long *)&sh.amask[x >> 6], 1ull << (x & 63u));
+            for (uint32_t k = 0; k < 8; k++) {
+                q[k] = live ? (uint32_t)__builtin_ctzll(live) : 64u;
+                live &= live - 1;
+                c[k] = q[k] < 64u ? sh.arr_c[p0 + q[k]] : 0u;
             }
+            // all eight loads in flight together (word 0 for an empty entry)
+            uint64_t nw[8];
+#pragma unroll
+            for (uint32_t k = 0; k < 8; k++) nw[k] = nd[c[k] >> 6];
+#pragma unroll
+            for (uint32_t k = 0; k < 8; k++)
+                if (q[k] < 64u && ((nw[k] >> (c[k] & 63u)) & 1ull)) m |= 1ull << q[k];
+        }
+        if (m) atomicOr((unsigned long long *)&sh.amask[i], m);
     }
+    __syncthreads();
+    for (uint32_t x = tid; x < SW_HASH_WORDS; x += ST) {
+        sh.hd[x] = 0u;
+        sh.hu[x] = 0u;
+    }
+    for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
     __syncthreads();
     int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
     const uint32_t fl = filter_log2(gp.nU);
@@ -646,6 +692,11 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 }
                 if (i < gp.nU) sh.ucnt[i] = 0u;
                 if (i < gp.nL) sh.pick[i] = pk;
+                if (pk != NONE32) {
+                    const uint32_t dl = sh.ldl[i];
+                    clash_mark(sh.hd, clash_slot(dl, pk));
+                    if (!(atomicOr(&sh.dpk[dl >> 5], 1u << (dl & 31u)) & (1u << (dl & 31u)))) acc.rounds++;
+                }
             }
             __syncthreads();
             // clash on (destination, chunk): fastest link, then lowest id
@@ -653,25 +704,34 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 const uint32_t pk = sh.pick[i];
                 uint8_t w = pk != NONE32;
                 if (w) {
-                    const uint64_t key = link_key(sh, i);
                     const uint32_t dl = sh.ldl[i];
-                    bool first = true;  // rounds are counted per destination that picked
-                    for (uint32_t j = sh.doff[dl]; j < sh.doff[dl + 1]; j++) {
-                        if (j < i && sh.pick[j] != NONE32) first = false;
-                        if (j != i && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
+                    if (!clash_alone(sh.hd, clash_slot(dl, pk))) {
+                        const uint64_t key = link_key(sh, i);
+                        for (uint32_t j0 = sh.doff[dl], je = sh.doff[dl + 1]; j0 < je; j0 += 4) {
+                            uint32_t pj[4];
+#pragma unroll
+                            for (uint32_t k = 0; k < 4; k++) pj[k] = sh.pick[min(j0 + k, je - 1u)];
+#pragma unroll
+                            for (uint32_t k = 0; k < 4; k++) {
+                                const uint32_t j = j0 + k;
+                                if (j < je && j != i && pj[k] == pk && link_key(sh, j) < key) w = 0;
+                            }
+                        }
                     }
-                    if (first) acc.rounds++;
                     const uint32_t u = sh.luni[i];
-                    if (w && u != SW_NONE8) sh.uwin[sh.uoff[u] + atomicAdd(&sh.ucnt[u], 1u)] = (uint16_t)i;
+                    if (w && u != SW_NONE8) {
+                        sh.uwin[sh.uoff[u] + atomicAdd(&sh.ucnt[u], 1u)] = (uint16_t)i;
+                        clash_mark(sh.hu, clash_slot(u, pk));
+                    }
                 }
-                sh.win1[i] = w;
+                sh.winf[i] = w;
             }
             __syncthreads();
             // clash on (unicast switch, chunk) among the destination winners
             for (uint32_t i = tid; i < gp.nL; i += ST) {
-                uint8_t w = sh.win1[i];
+                uint8_t w = sh.winf[i];
                 const uint32_t u = sh.luni[i];
-                if (w && u != SW_NONE8) {
+                if (w && u != SW_NONE8 && !clash_alone(sh.hu, clash_slot(u, sh.pick[i]))) {
                     const uint32_t pk = sh.pick[i];
                     const uint64_t key = link_key(sh, i);
                     for (uint32_t q = sh.uoff[u], qe = q + sh.ucnt[u]; q < qe; q++) {
@@ -679,31 +739,44 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         if (j != i && sh.pick[j] == pk && link_key(sh, j) < key) w = 0;
                     }
                 }
-                sh.win2[i] = w;
+                sh.winf[i] = w ? 3u : 0u;
             }
             __syncthreads();
             // free places of a limited switch, in (link time, link id) order
             for (uint32_t i = tid; i < gp.nL; i += ST) {
-                uint8_t w = sh.win2[i];
+                uint8_t w = (sh.winf[i] >> 1) & 1u;
                 const uint32_t b = sh.ldbuf[i];
                 if (w && b != SW_NONE8) {
                     const uint64_t key = link_key(sh, i);
                     const uint32_t dl = sh.ldl[i];
                     uint32_t ahead = 0;
-                    for (uint32_t j = sh.doff[dl]; j < sh.doff[dl + 1]; j++)
-                        if (j != i && sh.win2[j] && link_key(sh, j) < key) ahead++;
+                    for (uint32_t j0 = sh.doff[dl], je = sh.doff[dl + 1]; j0 < je; j0 += 4) {
+                        uint8_t fj[4];
+#pragma unroll
+                        for (uint32_t k = 0; k < 4; k++) fj[k] = j0 + k < je ? sh.winf[min(j0 + k, je - 1u)] : 0u;
+#pragma unroll
+                        for (uint32_t k = 0; k < 4; k++)
+                            if (j0 + k != i && ((fj[k] >> 1) & 1u) && link_key(sh, j0 + k) < key) ahead++;
+                    }
                     if (ahead >= sh.bcap[b] - sh.occ[b]) w = 0;
                 }
-                sh.win3[i] = w;
+                // (bits 0 and 1, which other links read in this stage, keep their values)
+                sh.winf[i] = (uint8_t)((sh.winf[i] & 3u) | (w << 2));
             }
             __syncthreads();
             // commit: the destination no longer needs the chunk, so neither
-            // do the limited switches feeding it on its behalf
+            // do the limited switches feeding it on its behalf (and the
+            // round's clash tables are cleared for the next round)
+            for (uint32_t x = tid; x < SW_HASH_WORDS; x += ST) {
+                sh.hd[x] = 0u;
+                sh.hu[x] = 0u;
+            }
+            for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
             uint32_t mine = 0;
             for (uint32_t i = tid; i < gp.nL; i += ST) {
                 const uint32_t pk = sh.pick[i];
                 if (pk == NONE32) continue;
-                if (!sh.win3[i]) {
+                if (!((sh.winf[i] >> 2) & 1u)) {
                     acc.clashes++;
                     continue;
                 }
@@ -711,14 +784,31 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 __hip_atomic_fetch_and(&ly.needs[(uint64_t)d * sz.Wp + (pk >> 6)], ~(1ull << (pk & 63u)),
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 const uint32_t dl = sh.ldl[i];
-                for (uint32_t j = sh.doff[dl]; j < sh.doff[dl + 1]; j++) {
-                    const uint32_t b = sh.lsbuf[j];
-                    if (b == SW_NONE8) continue;
-                    for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
-                        if (sh.pc[s] == pk && sh.pn[s] != 0u) {
-                            if (atomicSub(&sh.pn[s], 1u) == 1u) atomicSub(&sh.occ[b], 1u);
-                            break;
+                if (gp.nB) {
+                    for (uint32_t j0 = sh.doff[dl], je = sh.doff[dl + 1]; j0 < je; j0 += 8) {
+                        uint8_t bj[8];
+#pragma unroll
+                        for (uint32_t k = 0; k < 8; k++) bj[k] = j0 + k < je ? sh.lsbuf[min(j0 + k, je - 1u)] : SW_NONE8;
+#pragma unroll
+                        for (uint32_t k = 0; k < 8; k++) {
+                            const uint32_t b = bj[k];
+                            if (b == SW_NONE8) continue;
+                            // the place holding pk, four places compared at a time
+                            bool done = false;
+                            for (uint32_t s0 = sh.bpoff[b], se = sh.bpoff[b + 1]; s0 < se && !done; s0 += 4) {
+                                uint32_t cs[4];
+#pragma unroll
+                                for (uint32_t m = 0; m < 4; m++) cs[m] = sh.pc[min(s0 + m, se - 1u)];
+#pragma unroll
+                                for (uint32_t m = 0; m < 4; m++) {
+                                    const uint32_t s = s0 + m;
+                                    if (done || s >= se || cs[m] != pk || sh.pn[s] == 0u) continue;
+                                    if (atomicSub(&sh.pn[s], 1u) == 1u) atomicSub(&sh.occ[b], 1u);
+                                    done = true;
+                                }
+                            }
                         }
+                    }
                 }
                 const uint64_t end = (uint64_t)t + sh.ltim[i];
                 if (end > 0xFFFFFFFFull) {
@@ -734,27 +824,32 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     atomicOr(&sh.filt[fb >> 5], 1u << (fb & 31u));
                 }
                 acc.cstar = max(acc.cstar, e32);
-                const unsigned long long q = atomicAdd(&ly.dest_log[d], 1ull);
+                const unsigned long long q = atomicAdd(&sh.lcur[dl], 1ull);
                 ly.skey[0][q] = ((uint64_t)t << 32) | sh.llink[i];
                 ly.sval[0][q] = pk;
                 mine++;
             }
-            __builtin_amdgcn_s_waitcnt(0x0F70);  // the needs updates are done before the next stage reads them
+            // the needs updates are done before admissions and the next
+            // round's picks read them
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             __syncthreads();
             // a limited switch that took a chunk buffers it while an
             // out-neighbour still needs it
             for (uint32_t i = tid; i < gp.nL; i += ST) {
                 const uint32_t b = sh.ldbuf[i];
-                if (!sh.win3[i] || b == SW_NONE8) continue;
+                if (!((sh.winf[i] >> 2) & 1u) || b == SW_NONE8) continue;
                 const uint32_t pk = sh.pick[i];
                 uint32_t cnt = 0;
-                for (uint32_t q0 = sh.booff[b]; q0 < sh.booff[b + 1]; q0 += 4) {
-                    bool nb[4];
+                for (uint32_t q0 = sh.booff[b], qe = sh.booff[b + 1]; q0 < qe; q0 += 16) {
+                    // unconditional loads (the last out-neighbour again past
+                    // the end, not counted)
+                    uint64_t nw[16];
 #pragma unroll
-                    for (uint32_t k = 0; k < 4; k++)
-                        nb[k] = q0 + k < sh.booff[b + 1] && need_bit(ly.needs + (uint64_t)sh.bout[q0 + k] * sz.Wp, pk);
+                    for (uint32_t k = 0; k < 16; k++)
+                        nw[k] = __hip_atomic_load(&ly.needs[(uint64_t)sh.bout[min(q0 + k, qe - 1u)] * sz.Wp + (pk >> 6)],
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
-                    for (uint32_t k = 0; k < 4; k++) cnt += nb[k] ? 1u : 0u;
+                    for (uint32_t k = 0; k < 16; k++) cnt += (q0 + k < qe && ((nw[k] >> (pk & 63u)) & 1ull)) ? 1u : 0u;
                 }
                 if (!cnt) continue;
                 for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
@@ -780,9 +875,32 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         const uint64_t *nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
         const uint32_t base = sh.poff[sh.lsrcj[i]];
         uint32_t c = sh.cur[i], h = sh.hi[i];
+        // the region only grows below, so the arrivals outside it now are
+        // the only ones whose need is asked: their words are loaded first
+        uint64_t out = 0, needed = 0;
         for (uint64_t y = sh.amask[i]; y; y &= y - 1) {
-            const uint32_t ac = sh.arr_c[base + (uint32_t)__builtin_ctzll(y)];
-            if ((c <= ac && ac < h) || !need_bit(nd, ac)) continue;
+            const uint32_t q = (uint32_t)__builtin_ctzll(y), ac = sh.arr_c[base + q];
+            if (!(c <= ac && ac < h)) out |= 1ull << q;
+        }
+        while (out) {
+            uint32_t q[8], ac[8];
+#pragma unroll
+            for (uint32_t k = 0; k < 8; k++) {
+                q[k] = out ? (uint32_t)__builtin_ctzll(out) : 64u;
+                out &= out - 1;
+                ac[k] = q[k] < 64u ? sh.arr_c[base + q[k]] : 0u;
+            }
+            uint64_t nw[8];
+#pragma unroll
+            for (uint32_t k = 0; k < 8; k++)
+                nw[k] = __hip_atomic_load(&nd[ac[k] >> 6], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+            for (uint32_t k = 0; k < 8; k++)
+                if (q[k] < 64u && ((nw[k] >> (ac[k] & 63u)) & 1ull)) needed |= 1ull << q[k];
+        }
+        for (uint64_t y = sh.amask[i]; y; y &= y - 1) {
+            const uint32_t q = (uint32_t)__builtin_ctzll(y), ac = sh.arr_c[base + q];
+            if ((c <= ac && ac < h) || !((needed >> q) & 1ull)) continue;
             uint32_t e = 0;
             while (e < PEND && sh.pend[i][e] != NONE32 && sh.pend[i][e] != ac) e++;
             if (e < PEND) {
@@ -811,6 +929,8 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     }
     acc.tmin = min(acc.tmin, tm);
     if (!resident) {
+        for (uint32_t x = tid; x < gp.nD; x += ST)
+            if (sh.doff[x] < sh.doff[x + 1]) ly.dest_log[sh.ldst[sh.doff[x]]] = sh.lcur[x];
         for (uint32_t x = tid; x < gp.pool_n; x += ST) {
             ly.sw.pool_c[gp.pool_base + x] = sh.pc[x];
             ly.sw.pool_n[gp.pool_base + x] = sh.pn[x];

@@ -75,6 +75,27 @@ def test_switch_group_envelope():
     assert e.value.name == "PCCL_EUNSUPPORTED" and "in-links" in str(e.value)
 
 
+def test_switch_group_source_in_link_envelope():
+    # with a switch model, a group link's source may have at most 64 in-links
+    # (one bit per arrival pair in a link's arrival mask): a unicast switch
+    # with 80 ports feeds every NPU of its group
+    from paper_2606_07019_amd.pccl import PcclError, Synthesizer
+    print("[api] switch group source envelope", flush=True)
+    wl = W.star_all_gather(80, unicast=True)
+    with pytest.raises(PcclError) as e:
+        Synthesizer(wl.topo, wl.coll)
+    assert e.value.name == "PCCL_EUNSUPPORTED" and "source" in str(e.value) and "limit 64" in str(e.value)
+    ok = W.star_all_gather(64, unicast=True)
+    s = Synthesizer(ok.topo, ok.coll)
+    try:
+        n, ct = s.synthesize()
+        ref = O.run_workload(ok)
+        assert (n, ct) == (len(ref.sends), ref.collective_time)
+        np.testing.assert_array_equal(s.schedule(), ref.sends)
+    finally:
+        s.close()
+
+
 def test_buffer_places_envelope_and_oversized_capacity():
     from paper_2606_07019_amd.pccl import PcclError, Synthesizer
     print("[api] buffer places", flush=True)
