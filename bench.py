@@ -179,12 +179,16 @@ def switch_model(args, W, Synthesizer, torch):
         torch.cuda.synchronize()
         step_s = (time.perf_counter() - t0) / steps
         st, pr = syn.stats(), syn.profile()
+        # the switch-group kernel, or the plain one when the device found
+        # that the no-multicast rule cannot act (and no buffer limit binds)
+        kern = "k_match_sw" if syn.matcher() == "switch" else "k_match"
         kms = sum(match_ms) / len(match_ms)
         alg = BYTES_PER_SCANNED_WORD * pr["scan_words"] + BYTES_PER_MATCH * syn.n_sends
         pt = {"workload": wl.name, "npus": nn * pn, "buffer_chunks": buf, "unicast": bool(uni),
               "sends": syn.n_sends, "collective_time_ns": syn.collective_time, "windows": st["windows"],
               "synthesis_ms": step_s * 1e3, "match_ms": kms, "matches_per_s": syn.n_sends / step_s,
-              "roofline": {"bound": "hbm", "kernel": "k_match_sw", "achieved": round(alg / (kms * 1e-3) / 1e9, 3),
+              "matcher": kern,
+              "roofline": {"bound": "hbm", "kernel": kern, "achieved": round(alg / (kms * 1e-3) / 1e9, 3),
                            "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                            "frac": round(alg / (kms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 6),
                            "alg_bytes_per_launch": alg, "scan_words": pr["scan_words"]}}

@@ -342,6 +342,17 @@ pccl_status pccl_get_stats(pccl_ctx *ctx, uint64_t *events, uint64_t *rounds,
                            uint64_t *clashes, uint64_t *windows);
 
 /*
+ * Which matching kernel produced the last schedule: *kernel = 0 for the
+ * event-stepped kernel with one wavefront per destination, 1 for the
+ * switch-group kernel of the switch model (Sec. 4.7).  With a switch model
+ * that has no binding buffer limit, the second runs only when two
+ * out-neighbours of one unicast switch need the same chunk (checked on the
+ * device after the setup); otherwise the no-multicast rule can never act and
+ * the first gives the same schedule.  PCCL_ESTATE before a schedule exists.
+ */
+pccl_status pccl_get_matcher(pccl_ctx *ctx, uint32_t *kernel);
+
+/*
  * Setup products of the last synthesize call, copied to host arrays (any may
  * be NULL): link_time_ns[L] = alpha + ceil(m / bw); chunk_src[C] (source NPU
  * or 0xFFFFFFFF when the chunk is unused); chunk_dist[C] (max shortest-path

@@ -59,7 +59,10 @@ struct pccl_ctx {
     bool sw_active = false;        // the switch-model matching kernel runs
     std::vector<uint32_t> swt;     // switch-model tables, uploaded as one region
     std::vector<uint32_t> sw_links;  // links of each switch group
-    uint64_t swo[18] = {};         // offsets of the tables inside swt (order of SwTab)
+    uint64_t swo[20] = {};         // offsets of the tables inside swt (order of SwTab)
+    bool sw_gate = false;          // only the no-multicast rule may bind: the plain kernel runs when it cannot
+    uint32_t sw_nuni = 0;          // unicast switches with out-links
+    bool ran_sw = false;           // the last synthesis ran the switch-group kernel
     uint32_t sw_groups = 0, sw_pool = 0, sw_nbt = 0;
     int sw_grid = 0;
     // plan (made once per collective and switch model, before any workspace)
@@ -163,6 +166,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     sz.max_sends = max_sends;
     sz.tmin = c->tmin;
     sz.resident = c->resident ? 1u : 0u;
+    sz.sw_gate = c->sw_active && c->sw_gate ? 1u : 0u;
     const uint64_t hb = (uint64_t)sz.D * sz.Wp * sizeof(uint64_t);
     sz.hbytes = hb < (1ull << 31) ? (uint32_t)hb : 0u;
     const uint64_t nsort = std::max<uint64_t>(c->C, max_sends);
@@ -215,11 +219,11 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.sw = SwTab{};
     if (c->sw_active) {
         uint32_t *t = cv.take<uint32_t>(c->swt.size());
-        const uint32_t **p[18] = {&ly.sw.grp,    &ly.sw.blk,     &ly.sw.blk_list, &ly.sw.lk_slot, &ly.sw.lk_dl,
+        const uint32_t **p[20] = {&ly.sw.grp,    &ly.sw.blk,     &ly.sw.blk_list, &ly.sw.lk_slot, &ly.sw.lk_dl,
                                   &ly.sw.lk_srcj, &ly.sw.lk_uni,  &ly.sw.lk_dbuf,  &ly.sw.lk_sbuf, &ly.sw.d_off,
                                   &ly.sw.s_poff, &ly.sw.p_slot,  &ly.sw.u_off,    &ly.sw.u_list,  &ly.sw.b_cap,
-                                  &ly.sw.b_poff, &ly.sw.b_ooff,  &ly.sw.b_out};
-        for (int i = 0; i < 18; i++) *p[i] = t ? t + c->swo[i] : nullptr;
+                                  &ly.sw.b_poff, &ly.sw.b_ooff,  &ly.sw.b_out,    &ly.sw.uc_off,  &ly.sw.uc_dst};
+        for (int i = 0; i < 20; i++) *p[i] = t ? t + c->swo[i] : nullptr;
         ly.sw.pool_c = cv.take<uint32_t>(c->sw_pool);
         ly.sw.pool_n = cv.take<uint32_t>(c->sw_pool);
         ly.sw.occ = cv.take<uint32_t>(c->sw_nbt);
@@ -240,6 +244,8 @@ pccl_status build_switch_tables(pccl_ctx *c)
 {
     c->sw_built = true;
     c->sw_active = false;
+    c->sw_gate = false;
+    c->sw_nuni = 0;
     c->swt.clear();
     c->sw_links.clear();
     if (!c->sw_model) return PCCL_OK;
@@ -391,17 +397,34 @@ pccl_status build_switch_tables(pccl_ctx *c)
         pool += pl;
         c->sw_links.push_back(nl);
     }
+    // with no binding buffer limit only the no-multicast rule can change the
+    // schedule, and only if two out-neighbours of one unicast switch need the
+    // same chunk: the device checks that after the setup (the needs rows
+    // include the relay marks) and runs the plain kernel when they never do
+    std::vector<uint32_t> uc_off, uc_dst;
+    bool any_cap = false;
+    for (uint32_t i = 0; i < S; i++) any_cap = any_cap || cap[i];
+    for (uint32_t i = 0; i < S; i++) {
+        const uint32_t v = N + i;
+        if (!uni[i] || out_off[v + 1] - out_off[v] < 2) continue;
+        uc_off.push_back((uint32_t)uc_dst.size());
+        for (uint32_t k = out_off[v]; k < out_off[v + 1]; k++) uc_dst.push_back(c->dst[out_l[k]]);
+    }
+    c->sw_nuni = (uint32_t)uc_off.size();
+    uc_off.push_back((uint32_t)uc_dst.size());
+    c->sw_gate = !any_cap;
     std::vector<const std::vector<uint32_t> *> parts = {&grp,    nullptr, nullptr, &lk_slot, &lk_dl,  &lk_srcj,
                                                         &lk_uni, &lk_dbuf, &lk_sbuf, &d_off,  &s_poff, &p_slot,
-                                                        &u_off,  &u_list,  &b_cap,   &b_poff, &b_ooff, &b_out};
+                                                        &u_off,  &u_list,  &b_cap,   &b_poff, &b_ooff, &b_out,
+                                                        &uc_off, &uc_dst};
     uint64_t off = 0;
-    for (int i = 0; i < 18; i++) {
+    for (int i = 0; i < 20; i++) {
         c->swo[i] = off;
         off += i == 1 ? MAX_MATCH_GRID + 1ull : i == 2 ? (uint64_t)G : parts[i]->size();
         off = (off + 63) & ~63ull;
     }
     c->swt.assign(off, 0u);
-    for (int i = 0; i < 18; i++)
+    for (int i = 0; i < 20; i++)
         if (parts[i]) std::copy(parts[i]->begin(), parts[i]->end(), c->swt.begin() + c->swo[i]);
     c->sw_groups = G;
     c->sw_pool = pool;
@@ -1064,10 +1087,18 @@ static pccl_status synthesize_bound(pccl_ctx *c, uint64_t *n_sends, uint32_t *co
     // while the matching kernel runs and queues the output kernels behind it
     HIP_OR_FAIL(c, hipMemcpyAsync(&c->pin[0], c->ly.ctl, sizeof(Control), hipMemcpyDeviceToHost, st));
     HIP_OR_FAIL(c, hipEventRecord(c->ev[1], st));
-    if (c->sw_active)
+    const bool gate = c->sw_active && c->sw_gate;
+    if (gate) {
+        // both kernels are queued; the check picks the one that runs and the
+        // other returns at once
+        if (c->sw_nuni) HIP_OR_FAIL(c, launch_unicast_check(c->ly, c->sz, st, c->sw_nuni));
         HIP_OR_FAIL(c, launch_match_sw(c->ly, c->sz, st, c->sw_grid));
-    else
         HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb, c->mirror, !c->split.empty()));
+    } else if (c->sw_active) {
+        HIP_OR_FAIL(c, launch_match_sw(c->ly, c->sz, st, c->sw_grid));
+    } else {
+        HIP_OR_FAIL(c, launch_match(c->ly, c->sz, st, c->grid, c->wpb, c->mirror, !c->split.empty()));
+    }
     HIP_OR_FAIL(c, hipEventRecord(c->ev[2], st));
     HIP_OR_FAIL(c, hipEventSynchronize(c->ev[1]));
     const Control s0 = c->pin[0];
@@ -1078,6 +1109,7 @@ static pccl_status synthesize_bound(pccl_ctx *c, uint64_t *n_sends, uint32_t *co
     HIP_OR_FAIL(c, hipStreamSynchronize(st));
     c->ctl_host = c->pin[1];
     const Control &h = c->ctl_host;
+    c->ran_sw = c->sw_active && (!gate || h.sw_binds);
     if (h.abort) return fail(c, PCCL_EINTERNAL, "matching kernel barrier timed out");
     if (h.error) return device_error(c, h);
     if (h.n_log != h.needs_total || !out_queued || h.needs_total != s0.needs_total)
@@ -1330,6 +1362,16 @@ pccl_status pccl_export_program(pccl_ctx *c, pccl_step *steps, uint64_t step_cap
     for (uint32_t i = 0; i < st.size(); i++)
         steps[i] = {st[i].rank, st[i].tb, st[i].op, st[i].peer, st[i].chunk, st[i].t, dep_first[i], dep_count[i]};
     if (!dl.empty()) std::memcpy(deps, dl.data(), sizeof(uint32_t) * dl.size());
+    return PCCL_OK;
+    GUARD_END(c)
+}
+
+pccl_status pccl_get_matcher(pccl_ctx *c, uint32_t *kernel)
+{
+    if (!c || !kernel) return PCCL_EINVAL;
+    GUARD_BEGIN
+    if (!result_alive(c)) return fail(c, PCCL_ESTATE, c->have_result ? "the static scratch holding this schedule was reused" : "no schedule");
+    *kernel = c->ran_sw ? 1u : 0u;
     return PCCL_OK;
     GUARD_END(c)
 }

@@ -59,7 +59,7 @@ struct Control {
     uint32_t sort_cur;       // radix sort: buffer holding the current order
     uint32_t sort_buf[9];    // radix sort: buffer holding the order before pass i of a sort
     uint32_t sort_skip;      // radix sort (scan kernel): the pending pass is a no-op
-    uint32_t pad[1];
+    uint32_t sw_binds;       // switch model: the no-multicast rule can change the schedule
 };
 
 __device__ inline void record_error(Control *ctl, uint32_t code, uint32_t a = 0, uint32_t b = 0,
@@ -109,6 +109,8 @@ struct SwTab {
     const uint32_t *b_poff;   // [nB + 1] per group: its places in the group's pool
     const uint32_t *b_ooff;   // [nB + 1] per group: its out-neighbours
     const uint32_t *b_out;    // out-neighbour device ids
+    const uint32_t *uc_off;   // [n_uni + 1] every unicast switch of the model: its out-neighbours in uc_dst
+    const uint32_t *uc_dst;   // out-neighbour device ids
     uint32_t *pool_c, *pool_n;  // buffer places: chunk, out-neighbours still needing it (0 = free)
     uint32_t *occ;              // [nB + 1] per group: occupied places
 };
@@ -167,6 +169,7 @@ struct Sizes {
     uint32_t max_tiles;
     uint32_t hbytes;  // bytes of the holds bitmap (D rows of Wp words) when below 2 GiB, else 0
     uint32_t resident; // every wave of the matching kernel owns one destination (or part) for the whole run
+    uint32_t sw_gate;  // both matching kernels are queued; Control::sw_binds picks the one that runs
 };
 
 // ---- launchers (each defined in the translation unit that holds its kernels)
@@ -181,6 +184,9 @@ hipError_t launch_match(const Layout &ly, const Sizes &sz, hipStream_t st, int g
 int match_max_grid(int device, int waves_per_block, bool mirror, size_t dyn_lds, bool split);
 size_t match_static_lds();  // static LDS bytes of the matching kernel
 hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid);
+// sets Control::sw_binds when two out-neighbours of one of the n_uni unicast
+// switches need the same chunk
+hipError_t launch_unicast_check(const Layout &ly, const Sizes &sz, hipStream_t st, uint32_t n_uni);
 int match_sw_max_grid(int device);
 hipError_t launch_output(const Layout &ly, const Sizes &sz, int op, uint64_t n, hipStream_t st);
 // LSD radix sort of (key, value) pairs by key bytes [byte_lo, byte_hi), stable;

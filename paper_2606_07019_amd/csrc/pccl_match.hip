@@ -1339,6 +1339,9 @@ __global__ void __launch_bounds__(NT, (!MIRROR && SPLIT) ? 2 : 1) k_match(Layout
     __shared__ BlockShared sh;
     Control *ctl = ly.ctl;
     if (__hip_atomic_load(&ctl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+    // queued next to the switch-group kernel: runs only when the check found
+    // that the no-multicast rule cannot act
+    if (sz.sw_gate && __hip_atomic_load(&ctl->sw_binds, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
     const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t wpb = blockDim.x >> 6;  // waves in this workgroup (1..NWAVES)
     const uint32_t gwave = blockIdx.x * wpb + wave, nwaves = gridDim.x * wpb;

@@ -940,11 +940,42 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     __syncthreads();
 }
 
+// Can the no-multicast rule change the schedule?  Only when two
+// out-neighbours of one unicast switch need the same chunk (the needs rows as
+// set up, relay marks included, over the whole run: needs only shrink).
+// Otherwise no two out-links of a unicast switch ever pick the same chunk, so
+// the rule never acts and, with no binding buffer limit, the plain matching
+// gives the same schedule.  One thread per (unicast switch, row word).
+__global__ void __launch_bounds__(256) k_unicast_check(Layout ly, Sizes sz)
+{
+    if (__hip_atomic_load(&ly.ctl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+    const uint32_t u = blockIdx.y;
+    const uint64_t x = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (x >= sz.W) return;
+    const uint32_t q0 = ly.sw.uc_off[u], q1 = ly.sw.uc_off[u + 1];
+    uint64_t acc = 0, twice = 0;
+    for (uint32_t q = q0; q < q1; q += 8) {
+        uint64_t w[8];
+#pragma unroll
+        for (uint32_t k = 0; k < 8; k++) w[k] = ly.needs[(uint64_t)ly.sw.uc_dst[min(q + k, q1 - 1u)] * sz.Wp + x];
+#pragma unroll
+        for (uint32_t k = 0; k < 8; k++)
+            if (q + k < q1) {
+                twice |= acc & w[k];
+                acc |= w[k];
+            }
+    }
+    if (twice) atomicOr(&ly.ctl->sw_binds, 1u);
+}
+
 __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
 {
     __shared__ SwShared sh;
     Control *ctl = ly.ctl;
     if (__hip_atomic_load(&ctl->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+    // queued next to the plain kernel: runs only when the check found that
+    // the no-multicast rule can act
+    if (sz.sw_gate && !__hip_atomic_load(&ctl->sw_binds, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
     const uint32_t tid = threadIdx.x;
     if (ctl->needs_total == 0) {
         if (blockIdx.x == 0 && tid == 0) ctl->windows = 0;
@@ -1021,6 +1052,16 @@ int match_sw_max_grid(int device)
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_match_sw, ST, 0) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return 0;
     return per_cu * cus;
+}
+
+hipError_t launch_unicast_check(const Layout &ly, const Sizes &sz, hipStream_t st, uint32_t n_uni)
+{
+    if (n_uni == 0 || sz.W == 0) return hipSuccess;
+    if (n_uni > 65535u) return hipErrorInvalidValue;
+    const uint64_t bx = (sz.W + 255) / 256;
+    if (bx > 0x7FFFFFFFull) return hipErrorInvalidValue;
+    k_unicast_check<<<dim3((uint32_t)bx, n_uni), 256, 0, st>>>(ly, sz);
+    return hipGetLastError();
 }
 
 hipError_t launch_match_sw(const Layout &ly, const Sizes &sz, hipStream_t st, int grid)

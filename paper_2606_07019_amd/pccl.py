@@ -64,6 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "pccl_get_schedule": ([P, P, U64], I),
         "pccl_get_path": ([P, U32, U32, P, P, U32, ctypes.POINTER(U32)], I),
         "pccl_export_program": ([P, P, U64, P, U64, ctypes.POINTER(U64), ctypes.POINTER(U64)], I),
+        "pccl_get_matcher": ([P, ctypes.POINTER(U32)], I),
         "pccl_get_stats": ([P, ctypes.POINTER(U64), ctypes.POINTER(U64), ctypes.POINTER(U64),
                             ctypes.POINTER(U64)], I),
         "pccl_get_setup": ([P, P, P, P, P], I),
@@ -213,6 +214,13 @@ def pccl_get_stats(h) -> dict:
     return dict(zip(["events", "rounds", "clashes", "windows"], [int(x.value) for x in v]))
 
 
+def pccl_get_matcher(h) -> str:
+    """Which matching kernel made the last schedule: "plain" or "switch"."""
+    v = ctypes.c_uint32()
+    _check(h, load_library().pccl_get_matcher(h, ctypes.byref(v)))
+    return "switch" if v.value else "plain"
+
+
 def pccl_get_link_usage(h, n_links: int, n_bins: int = 20):
     """(busy_ns per link, busy link-time per time bin, bin width in ns)."""
     busy = np.zeros(max(n_links, 1), np.uint64)
@@ -299,6 +307,9 @@ class Synthesizer:
 
     def profile(self) -> dict:
         return pccl_get_profile(self.h)
+
+    def matcher(self) -> str:
+        return pccl_get_matcher(self.h)
 
     def link_usage(self, n_bins: int = 20):
         return pccl_get_link_usage(self.h, self.topo.n_links, n_bins)

@@ -192,3 +192,62 @@ def test_repeat_runs_identical(make):
             np.testing.assert_array_equal(s.schedule(), a)
     finally:
         s.close()
+
+
+def _matcher_and_compare(wl, want):
+    from paper_2606_07019_amd.pccl import Synthesizer
+    ref = O.run_workload(wl)
+    assert ref.status == 0, ref.message
+    s = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed)
+    try:
+        n, ct = s.synthesize()
+        assert s.matcher() == want
+        assert (n, ct) == (len(ref.sends), ref.collective_time)
+        np.testing.assert_array_equal(s.schedule(), ref.sends)
+        st = s.stats()
+        for key in ("events", "rounds", "clashes"):
+            assert st[key] == ref.stats[key], key
+    finally:
+        s.close()
+
+
+@pytest.mark.parametrize("make,want", [
+    # All-to-All behind unicast rail switches with unlimited buffers: no two
+    # out-neighbours of a switch need one chunk, the rule cannot act
+    (lambda: W.switch2level_model(8, 4, 0, True), "plain"),
+    (lambda: W.switch2level_model(16, 8, 0, True), "plain"),
+    # All-Gather through a unicast switch: every NPU needs every chunk
+    (lambda: W.star_all_gather(9, chunks_per_npu=5, unicast=True), "switch"),
+    (lambda: W.star_all_gather(33, chunks_per_npu=2, unicast=True), "switch"),
+    # a finite buffer always takes the switch-group kernel
+    (lambda: W.switch2level_model(8, 4, 2, True), "switch"),
+])
+def test_unicast_rule_check_picks_the_kernel(make, want):
+    # the device checks after the setup whether the no-multicast rule can
+    # act; either kernel's schedule equals the oracle's
+    wl = make()
+    print(f"[switch gate] {wl.name}: {want}", flush=True)
+    _matcher_and_compare(wl, want)
+
+
+def test_full_size_unicast_unlimited_is_the_plain_schedule():
+    # 512-NPU rail All-to-All with unicast rail switches and unlimited
+    # buffers: the plain kernel runs and its schedule is the plain model's
+    # (the oracle's digest of the same workload without a switch model)
+    import hashlib
+    import json
+    import os
+    from paper_2606_07019_amd.pccl import Synthesizer
+    print("[switch gate] 512-NPU unicast, unlimited buffers", flush=True)
+    with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "config4.json")) as f:
+        g = json.load(f)
+    wl = W.switch2level_model(64, 8, 0, True)
+    s = Synthesizer(wl.topo, wl.coll, tie_seed=wl.tie_seed)
+    try:
+        s.synthesize()
+        assert s.matcher() == "plain"
+        assert s.n_sends == g["n_sends"] and s.collective_time == g["collective_time_ns"]
+        sched = s.schedule()
+        assert hashlib.sha256(np.ascontiguousarray(sched, dtype="<u4").tobytes()).hexdigest() == g["sha256"]
+    finally:
+        s.close()
