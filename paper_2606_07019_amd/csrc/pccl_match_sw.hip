@@ -76,6 +76,9 @@ struct SwShared {
     // alone in its slot skips the comparison with its rivals; and one bit per
     // destination that picked (rounds are counted per such destination)
     uint32_t hd[SW_HASH_WORDS], hu[SW_HASH_WORDS], dpk[SW_MAX_LINKS / 32];
+    // per pick round (two, alternating): bit 0 a pick lost a clash, bit 1 a
+    // free link was held back by a full buffer, bit 2 a buffer place was freed
+    uint32_t rflag[2];
     // next send-log slot of each destination of the group (its segment)
     unsigned long long lcur[SW_MAX_LINKS];
     uint32_t red[SWAVES];
@@ -534,7 +537,9 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         sh.hu[x] = 0u;
     }
     for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
+    if (tid < 2) sh.rflag[tid] = 0u;
     __syncthreads();
+    uint32_t par = 0;  // this round's rflag word
     int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
     const uint32_t fl = filter_log2(gp.nU);
     for (;;) {
@@ -580,6 +585,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 if (i < gp.nL && sh.busy[i] <= t) {
                     const uint32_t b = sh.ldbuf[i];
                     free = b == SW_NONE8 || sh.occ[b] < sh.bcap[b];
+                    if (!free) atomicOr(&sh.rflag[par], 2u);
                 }
                 if (free) {
                     nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
@@ -772,12 +778,16 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 sh.hu[x] = 0u;
             }
             for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
+            // the next round's flags (last read right after the previous
+            // round's final barrier, first set after this round's)
+            if (tid == 0) sh.rflag[par ^ 1u] = 0u;
             uint32_t mine = 0;
             for (uint32_t i = tid; i < gp.nL; i += ST) {
                 const uint32_t pk = sh.pick[i];
                 if (pk == NONE32) continue;
                 if (!((sh.winf[i] >> 2) & 1u)) {
                     acc.clashes++;
+                    atomicOr(&sh.rflag[par], 1u);
                     continue;
                 }
                 const uint32_t d = sh.ldst[i];
@@ -803,7 +813,10 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                                 for (uint32_t m = 0; m < 4; m++) {
                                     const uint32_t s = s0 + m;
                                     if (done || s >= se || cs[m] != pk || sh.pn[s] == 0u) continue;
-                                    if (atomicSub(&sh.pn[s], 1u) == 1u) atomicSub(&sh.occ[b], 1u);
+                                    if (atomicSub(&sh.pn[s], 1u) == 1u) {
+                                        atomicSub(&sh.occ[b], 1u);
+                                        atomicOr(&sh.rflag[par], 4u);
+                                    }
                                     done = true;
                                 }
                             }
@@ -860,8 +873,14 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     }
             }
             acc.sent += mine;
-            const int any = __syncthreads_or(mine != 0);
-            if (!any) break;
+            // another round picks something only for a link that lost a
+            // clash, or one a full buffer held back when a place was freed:
+            // holds do not change inside an event, needs and free places only
+            // shrink otherwise, and chunks in flight only add up
+            __syncthreads();
+            const uint32_t f = sh.rflag[par];
+            par ^= 1u;
+            if (!(f & 1u) && (f & 6u) != 6u) break;
         }
         t_prev = t;
     }
