@@ -79,6 +79,11 @@ struct SwShared {
     // per pick round (two, alternating): bit 0 a pick lost a clash, bit 1 a
     // free link was held back by a full buffer, bit 2 a buffer place was freed
     uint32_t rflag[2];
+    // destinations whose links lie in one wave in (link time, link id) order
+    // (the buffer-place order is then a ballot and a bit count)
+    uint32_t dord[SW_MAX_LINKS / 32];
+    // admissions of a round (their list and counts reuse wsl and uwin)
+    uint32_t acount;
     // next send-log slot of each destination of the group (its segment)
     unsigned long long lcur[SW_MAX_LINKS];
     uint32_t red[SWAVES];
@@ -278,6 +283,21 @@ __device__ void load_group_state(const Layout &ly, const Sizes &sz, const SwGrou
     for (uint32_t x = tid; x < nbo; x += ST) sh.bout[x] = sw.b_out[gp.bobase + x];
     for (uint32_t x = tid; x < gp.nD; x += ST)
         if (sh.doff[x] < sh.doff[x + 1]) sh.lcur[x] = ly.dest_log[sh.ldst[sh.doff[x]]];
+    // (a wave per 64 destinations, one flag word per 32)
+    for (uint32_t x0 = 0; x0 < gp.nD; x0 += ST) {
+        const uint32_t x = x0 + tid;
+        bool ok = false;
+        if (x < gp.nD) {
+            const uint32_t a = sh.doff[x], e = sh.doff[x + 1];
+            ok = e > a && (a >> 6) == ((e - 1u) >> 6);
+            for (uint32_t j = a; ok && j + 1 < e; j++) ok = link_key(sh, j) < link_key(sh, j + 1);
+        }
+        const uint64_t m = __ballot(ok);
+        if ((tid & 63u) == 0 && x < gp.nD) {
+            sh.dord[x >> 5] = (uint32_t)m;
+            if (x + 32 < gp.nD) sh.dord[(x >> 5) + 1] = (uint32_t)(m >> 32);
+        }
+    }
 }
 
 // A unicast switch keeps one copy of a chunk in flight: is chunk c in flight
@@ -749,25 +769,36 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             }
             __syncthreads();
             // free places of a limited switch, in (link time, link id) order
-            for (uint32_t i = tid; i < gp.nL; i += ST) {
-                uint8_t w = (sh.winf[i] >> 1) & 1u;
-                const uint32_t b = sh.ldbuf[i];
+            {
+                const uint32_t i = tid;
+                const uint8_t wf = i < gp.nL ? sh.winf[i] : 0u;
+                uint32_t w = (wf >> 1) & 1u;
+                const uint32_t b = i < gp.nL ? sh.ldbuf[i] : SW_NONE8;
+                const uint64_t w2m = __ballot(w != 0u);
                 if (w && b != SW_NONE8) {
-                    const uint64_t key = link_key(sh, i);
                     const uint32_t dl = sh.ldl[i];
                     uint32_t ahead = 0;
-                    for (uint32_t j0 = sh.doff[dl], je = sh.doff[dl + 1]; j0 < je; j0 += 4) {
-                        uint8_t fj[4];
+                    if ((sh.dord[dl >> 5] >> (dl & 31u)) & 1u) {
+                        // the destination's winners with a smaller key are its
+                        // winners on lower lanes of this wave
+                        const uint32_t lo = sh.doff[dl] & 63u, me = i & 63u;
+                        ahead = (uint32_t)__popcll(w2m & ((1ull << me) - 1ull) & ~((1ull << lo) - 1ull));
+                    } else {
+                        const uint64_t key = link_key(sh, i);
+                        for (uint32_t j0 = sh.doff[dl], je = sh.doff[dl + 1]; j0 < je; j0 += 4) {
+                            uint8_t fj[4];
 #pragma unroll
-                        for (uint32_t k = 0; k < 4; k++) fj[k] = j0 + k < je ? sh.winf[min(j0 + k, je - 1u)] : 0u;
+                            for (uint32_t k = 0; k < 4; k++) fj[k] = j0 + k < je ? sh.winf[min(j0 + k, je - 1u)] : 0u;
 #pragma unroll
-                        for (uint32_t k = 0; k < 4; k++)
-                            if (j0 + k != i && ((fj[k] >> 1) & 1u) && link_key(sh, j0 + k) < key) ahead++;
+                            for (uint32_t k = 0; k < 4; k++)
+                                if (j0 + k != i && ((fj[k] >> 1) & 1u) && link_key(sh, j0 + k) < key) ahead++;
+                        }
                     }
                     if (ahead >= sh.bcap[b] - sh.occ[b]) w = 0;
                 }
                 // (bits 0 and 1, which other links read in this stage, keep their values)
-                sh.winf[i] = (uint8_t)((sh.winf[i] & 3u) | (w << 2));
+                if (i < gp.nL) sh.winf[i] = (uint8_t)((wf & 3u) | (w << 2));
+                if (i == 0) sh.acount = 0u;
             }
             __syncthreads();
             // commit: the destination no longer needs the chunk, so neither
@@ -781,7 +812,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             // the next round's flags (last read right after the previous
             // round's final barrier, first set after this round's)
             if (tid == 0) sh.rflag[par ^ 1u] = 0u;
-            uint32_t mine = 0;
+            uint32_t mine = 0, myadm = NONE32;
             for (uint32_t i = tid; i < gp.nL; i += ST) {
                 const uint32_t pk = sh.pick[i];
                 if (pk == NONE32) continue;
@@ -838,6 +869,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 }
                 acc.cstar = max(acc.cstar, e32);
                 const unsigned long long q = atomicAdd(&sh.lcur[dl], 1ull);
+                if (sh.ldbuf[i] != SW_NONE8) myadm = atomicAdd(&sh.acount, 1u);
                 ly.skey[0][q] = ((uint64_t)t << 32) | sh.llink[i];
                 ly.sval[0][q] = pk;
                 mine++;
@@ -847,8 +879,40 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             __syncthreads();
             // a limited switch that took a chunk buffers it while an
-            // out-neighbour still needs it
-            for (uint32_t i = tid; i < gp.nL; i += ST) {
+            // out-neighbour still needs it.  The out-neighbours' need bits
+            // are counted by whole waves (admission k on wave k mod 16, a
+            // lane per out-neighbour, one round trip for up to 16
+            // admissions), then the admitting link takes a free place
+            const uint32_t nadm = sh.acount;
+            uint16_t *alist = reinterpret_cast<uint16_t *>(&sh.wsl[0][0]);
+            if (nadm && nadm <= SWAVES * 64u / 2u) {
+                if (myadm != NONE32) alist[myadm] = (uint16_t)tid;
+                __syncthreads();
+                const uint32_t lane = tid & 63u, wave = tid >> 6;
+                for (uint32_t k = wave; k < nadm; k += SWAVES) {
+                    const uint32_t i = alist[k], b = sh.ldbuf[i], pk = sh.pick[i];
+                    const uint32_t q0 = sh.booff[b], qe = sh.booff[b + 1];
+                    uint32_t cnt = 0;
+                    for (uint32_t q = q0; q < qe; q += 64) {
+                        const uint32_t qq = min(q + lane, qe - 1u);
+                        const uint64_t nw = __hip_atomic_load(&ly.needs[(uint64_t)sh.bout[qq] * sz.Wp + (pk >> 6)],
+                                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        cnt += (uint32_t)__popcll(__ballot(q + lane < qe && ((nw >> (pk & 63u)) & 1ull)));
+                    }
+                    if (lane == 0) sh.uwin[k] = (uint16_t)cnt;
+                }
+                __syncthreads();
+                if (myadm != NONE32) {
+                    const uint32_t i = tid, b = sh.ldbuf[i], pk = sh.pick[i], cnt = sh.uwin[myadm];
+                    if (cnt)
+                        for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
+                            if (atomicCAS(&sh.pn[s], 0u, cnt) == 0u) {
+                                sh.pc[s] = pk;
+                                atomicAdd(&sh.occ[b], 1u);
+                                break;
+                            }
+                }
+            } else if (nadm) for (uint32_t i = tid; i < gp.nL; i += ST) {
                 const uint32_t b = sh.ldbuf[i];
                 if (!((sh.winf[i] >> 2) & 1u) || b == SW_NONE8) continue;
                 const uint32_t pk = sh.pick[i];
