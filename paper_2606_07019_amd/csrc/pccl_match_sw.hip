@@ -515,43 +515,77 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     // its source's pairs (at most 64) in LDS and loads the needs words of the
     // live ones eight at a time, all in flight together (through the caches,
     // a superset: picks confirm each candidate)
-    const uint32_t share = gp.nL && gp.nL <= ST / 2 ? 2u : 1u;
-    for (uint32_t i = tid; i < gp.nL; i += ST) sh.amask[i] = 0ull;
-    __syncthreads();
-    for (uint32_t x = tid; x < gp.nL * share; x += ST) {
-        const uint32_t i = x % gp.nL, half = x / gp.nL;
-        const uint32_t j = sh.lsrcj[i], p0 = sh.poff[j], np = sh.poff[j + 1] - p0;
-        const uint64_t *nd = ly.needs + (uint64_t)sh.ldst[i] * sz.Wp;
-        // the pairs with an arrival (this thread's half of them when shared)
-        uint64_t live = 0;
-        for (uint32_t q0 = 0; q0 < np; q0 += 8) {
-            uint32_t a[8];
-#pragma unroll
-            for (uint32_t k = 0; k < 8; k++) a[k] = sh.arr_t[p0 + min(q0 + k, np - 1u)];
-#pragma unroll
-            for (uint32_t k = 0; k < 8; k++)
-                if (q0 + k < np && a[k] != NONE32 && ((q0 + k) % share) == half) live |= 1ull << (q0 + k);
+    // which arrivals each link's destination may still need: the (link,
+    // pair) items of all links, spread evenly over the workgroup's threads
+    // (a block prefix over the links' pair counts, kept in `pick`, which
+    // the rounds overwrite later); each thread loads the needs words of its
+    // items eight at a time, all in flight together, through the caches (a
+    // superset: picks confirm each candidate)
+    {
+        const uint32_t lane = tid & 63u, wave = tid >> 6;
+        const uint32_t np_me =
+            tid < gp.nL ? (uint32_t)(sh.poff[sh.lsrcj[tid] + 1] - sh.poff[sh.lsrcj[tid]]) : 0u;
+        uint32_t inc = np_me;
+        for (uint32_t o = 1; o < 64; o <<= 1) {
+            const uint32_t y = (uint32_t)__shfl_up((int)inc, (int)o);
+            if (lane >= o) inc += y;
         }
-        uint64_t m = 0;
-        while (live) {
-            uint32_t q[8], c[8];
-#pragma unroll
-            for (uint32_t k = 0; k < 8; k++) {
-                q[k] = live ? (uint32_t)__builtin_ctzll(live) : 64u;
-                live &= live - 1;
-                c[k] = q[k] < 64u ? sh.arr_c[p0 + q[k]] : 0u;
+        if (lane == 63) sh.red[wave] = inc;
+        if (tid < gp.nL) sh.amask[tid] = 0ull;
+        __syncthreads();
+        uint32_t below = 0, tot = 0;
+        for (uint32_t w = 0; w < SWAVES; w++) {
+            const uint32_t r = sh.red[w];
+            if (w < wave) below += r;
+            tot += r;
+        }
+        if (tid < gp.nL) sh.pick[tid] = below + inc - np_me;
+        __syncthreads();
+        const uint32_t per = (tot + ST - 1) / ST;
+        uint32_t x = tid * per;
+        const uint32_t xe = min(x + per, tot);
+        if (x < xe) {
+            // the link holding item x: the last link whose first item is at
+            // or below x, then past the links without pairs
+            uint32_t lo = 0, hi2 = gp.nL;
+            while (hi2 - lo > 1) {
+                const uint32_t m = (lo + hi2) >> 1;
+                if (sh.pick[m] <= x) lo = m;
+                else hi2 = m;
             }
-            // all eight loads in flight together (word 0 for an empty entry)
-            uint64_t nw[8];
+            uint32_t i = lo, q = x - sh.pick[i];
+            uint32_t p0 = sh.poff[sh.lsrcj[i]], np = sh.poff[sh.lsrcj[i] + 1] - p0;
+            while (x < xe) {
+                uint32_t li[8], qb[8], c[8];
+                bool v[8];
 #pragma unroll
-            for (uint32_t k = 0; k < 8; k++) nw[k] = nd[c[k] >> 6];
+                for (uint32_t k = 0; k < 8; k++) {
+                    while (q >= np && i + 1 < gp.nL) {
+                        q -= np;
+                        i++;
+                        p0 = sh.poff[sh.lsrcj[i]];
+                        np = sh.poff[sh.lsrcj[i] + 1] - p0;
+                    }
+                    v[k] = x < xe && q < np && sh.arr_t[p0 + min(q, np - 1u)] != NONE32;
+                    li[k] = i;
+                    qb[k] = q;
+                    c[k] = v[k] ? sh.arr_c[p0 + q] : 0u;
+                    x++;
+                    q++;
+                }
+                // unconditional loads (row 0, word 0 for an item without an arrival)
+                uint64_t nw[8];
 #pragma unroll
-            for (uint32_t k = 0; k < 8; k++)
-                if (q[k] < 64u && ((nw[k] >> (c[k] & 63u)) & 1ull)) m |= 1ull << q[k];
+                for (uint32_t k = 0; k < 8; k++)
+                    nw[k] = ly.needs[(uint64_t)(v[k] ? sh.ldst[li[k]] : 0u) * sz.Wp + (c[k] >> 6)];
+#pragma unroll
+                for (uint32_t k = 0; k < 8; k++)
+                    if (v[k] && ((nw[k] >> (c[k] & 63u)) & 1ull))
+                        atomicOr((unsigned long long *)&sh.amask[li[k]], 1ull << qb[k]);
+            }
         }
-        if (m) atomicOr((unsigned long long *)&sh.amask[i], m);
+        __syncthreads();
     }
-    __syncthreads();
     for (uint32_t x = tid; x < SW_HASH_WORDS; x += ST) {
         sh.hd[x] = 0u;
         sh.hu[x] = 0u;
