@@ -383,7 +383,7 @@ __device__ inline uint64_t range_bits(uint64_t w, uint32_t lo, uint32_t hi)
 // dropped where it came from and the pick repeats.  (One thread per link,
 // serial: the pick stage below shares the row scans out among the lanes of
 // a wave and calls this only when its candidate turns out stale.)
-__device__ uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, uint32_t i, uint32_t t,
+__device__ __attribute__((noinline)) uint32_t pick_link(const Layout &ly, const Sizes &sz, SwShared &sh, uint32_t i, uint32_t t,
                               unsigned long long &words)
 {
     const uint64_t *hs = ly.holds + (uint64_t)sh.lsrc[i] * sz.Wp;
@@ -492,18 +492,20 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     // a workgroup with one group keeps its tables and state in LDS
     if (!resident || first_window) load_group_state(ly, sz, gp, sh);
     // arrivals at the group's sources inside the window, from the entries
-    // published at t0 (the source's in-links, pair p of source j)
-    // (four pairs per thread in flight: slot indices, then the entries)
-    for (uint32_t p0 = tid; p0 < gp.nP; p0 += 4u * ST) {
-        uint32_t sl[4];
-        uint64_t e[4];
+    // published at t0 (the source's in-links, pair p of source j): eight
+    // pairs per thread, so one pass covers a group's 8,192 pairs with two
+    // dependent round trips (slot indices, then the entries)
+    static_assert(SW_MAX_PAIRS <= 8u * ST, "one pass of eight pairs per thread");
+    if (gp.nP) {
+        uint32_t sl[8];
+        uint64_t e[8];
 #pragma unroll
-        for (uint32_t k = 0; k < 4; k++) sl[k] = ly.sw.p_slot[gp.pbase + min(p0 + k * ST, gp.nP - 1u)];
+        for (uint32_t k = 0; k < 8; k++) sl[k] = ly.sw.p_slot[gp.pbase + min(tid + k * ST, gp.nP - 1u)];
 #pragma unroll
-        for (uint32_t k = 0; k < 4; k++) e[k] = ly.snap[sl[k]];
+        for (uint32_t k = 0; k < 8; k++) e[k] = ly.snap[sl[k]];
 #pragma unroll
-        for (uint32_t k = 0; k < 4; k++) {
-            const uint32_t p = p0 + k * ST, b = (uint32_t)e[k];
+        for (uint32_t k = 0; k < 8; k++) {
+            const uint32_t p = tid + k * ST, b = (uint32_t)e[k];
             if (p >= gp.nP) continue;
             const bool in = e[k] != NONE64 && b >= t0 && (uint64_t)b < t1;
             sh.arr_t[p] = in ? b : NONE32;
@@ -511,10 +513,6 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         }
     }
     __syncthreads();
-    // which arrivals each link's destination may still need: each link walks
-    // its source's pairs (at most 64) in LDS and loads the needs words of the
-    // live ones eight at a time, all in flight together (through the caches,
-    // a superset: picks confirm each candidate)
     // which arrivals each link's destination may still need: the (link,
     // pair) items of all links, spread evenly over the workgroup's threads
     // (a block prefix over the links' pair counts, kept in `pick`, which
