@@ -159,3 +159,65 @@ def test_split_with_rows_in_device_memory(kind, seed):
         hub = _hub_graph(seed, 130)
         topo, n = hub.topo, hub.topo.n_npus
     _compare(_sparse_wide(topo, n, C, 3000, seed, f"{kind}_wide{C}"), "rows in device memory")
+
+
+def _random_hubs(seed, n_chunks):
+    # seeded random topology: a bidirectional ring of 100-200 NPUs cut into
+    # clusters of 3-6 that are fully meshed by fast links; 1-3 hub NPUs that
+    # 65-200 random ring NPUs link to by slow links, and that link back to a
+    # few; chunks start on one NPU and go to its cluster, often a hub and a
+    # few random NPUs, so that several of a hub's in-neighbours hold a chunk
+    # at once and the hub's parts clash
+    rng = np.random.default_rng(9000 + seed)
+    n_ring = int(rng.integers(100, 201))
+    n_hub = int(rng.integers(1, 4))
+    n = n_ring + n_hub
+    pairs = {}
+    for i in range(n_ring):
+        for j in ((i + 1) % n_ring, (i - 1) % n_ring):
+            pairs[(i, j)] = (int(rng.integers(300, 900)), 100)
+    cl, start = [], 0
+    while start < n_ring:
+        size = int(rng.integers(3, 7))
+        cl.append(list(range(start, min(start + size, n_ring))))
+        start += size
+    cluster_of = {v: k for k, m in enumerate(cl) for v in m}
+    for m in cl:
+        for i in m:
+            for j in m:
+                if i != j:
+                    pairs[(i, j)] = (100, 400)
+    for h in range(n_ring, n):
+        k = int(rng.integers(65, min(200, n_ring) + 1))
+        for v in rng.choice(n_ring, size=k, replace=False):
+            pairs[(int(v), h)] = (int(rng.integers(500, 1500)), int(rng.choice([25, 50])))
+        for v in rng.choice(n_ring, size=int(rng.integers(2, 9)), replace=False):
+            pairs[(h, int(v))] = (700, 50)
+    keys = sorted(pairs)
+    topo = W.make_topology(n, 0, keys, [pairs[k][0] for k in keys], [pairs[k][1] for k in keys])
+    used = min(n_chunks, 600)
+    cols = np.sort(rng.choice(n_chunks, size=used, replace=False))
+    src_of = [None] * n_chunks
+    dests_of = [()] * n_chunks
+    for c in cols:
+        s = int(rng.integers(n_ring))
+        ds = set(cl[cluster_of[s]])
+        if rng.random() < 0.8:
+            ds.add(int(rng.integers(n_ring, n)))
+        ds.update(int(x) for x in rng.integers(n, size=int(rng.integers(0, 4))))
+        ds.discard(s)
+        src_of[int(c)] = s
+        dests_of[int(c)] = sorted(ds)
+    coll = W.collective_from_lists(n, n_chunks, 32 << 10, src_of, dests_of, [list(range(n))])
+    return W.Workload(f"randhubs{seed}_c{n_chunks}", topo, coll, seed)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_hubs_rows_in_lds(seed):
+    _compare(_random_hubs(seed, 2000), "random hubs")
+
+
+@pytest.mark.parametrize("seed", range(12, 18))
+def test_random_hubs_rows_in_device_memory(seed):
+    # 600,000 columns: needs rows too wide for LDS
+    _compare(_random_hubs(seed, 600_000), "random hubs, wide rows")
