@@ -32,9 +32,24 @@
 // candidate set was found empty stays empty until its source receives a
 // chunk its destination needs (needs only shrink), so it is not rescanned;
 // a busy link keeps a cursor below which it has no candidate (lowered when
-// its source receives a needed chunk), so its next scan starts there.  Each
-// lane first probes the next few words of its own link's two rows; only the
-// scans that run past the probe are continued by the whole wavefront.
+// its source receives a needed chunk), so its next scan starts there, and
+// an upper bound on its number of candidates (counted in the setup, raised
+// by such arrivals, lowered by its own commits), so a freed link whose bound
+// is zero, or whose candidates are all listed arrivals, is not scanned.
+// Each lane first probes the next few words of its own link's two rows; only
+// the scans that run past the probe are continued by the whole wavefront.
+//
+// A device with more than 64 in-links or more than 512 arrival pairs (a
+// switch with many ports) is split over the wavefronts of a workgroup of its
+// own, one part of its in-links each.  The parts share the device's needs
+// row and send-log segment, run the same event times and pick rounds, and
+// settle clashes between parts through winner tables in LDS, with workgroup
+// barriers per event and per round (a separate build of the kernel, so that
+// the other devices carry none of it).
+//
+// With a switch model (Sec. 4.7) whose only binding rule is the
+// no-multicast one, this kernel is queued next to the switch-group kernel
+// and runs only when the device found that the rule cannot act.
 #include "pccl_internal.h"
 
 namespace pccl {

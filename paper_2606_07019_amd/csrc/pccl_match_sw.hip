@@ -15,7 +15,14 @@
 // destinations' event times are merged and each event runs the round loop of
 // the event-stepped matching (pick, clash on (destination, chunk), clash on
 // (unicast switch, chunk), free buffer places, commit) with workgroup barriers
-// between the stages.
+// between the stages.  Thread i owns group link i; the picks themselves stay
+// inside each wavefront (row scans shared out among its lanes), and hashed
+// marks let a pick alone in its clash slot win without comparisons.
+//
+// When no buffer limit binds, the no-multicast rule can act only if two
+// out-neighbours of one unicast switch need the same chunk; k_unicast_check
+// finds out after the setup, and this kernel then runs only if they do (the
+// plain kernel, queued next to it, runs otherwise).
 //
 // Groups interact only through chunk arrivals, which take at least the
 // smallest link time, so the windows [t0, t0 + Tmin) of the plain matcher
