@@ -57,8 +57,12 @@ def test_static_entry_point_matches_workspace_path():
     stream = torch.cuda.current_stream(0).cuda_stream
     # each call smaller than the one before; the 512-NPU All-to-All is the
     # largest collective here and fits the scratch with its exact bound
-    cases = [W.config4(), W.config3(), W.mesh3x3_two_groups(), W.star_all_gather(6, 3, buffer=2, unicast=True),
-             W.config1()]
+    # (the 32-NPU rail All-to-All behind unicast switches with unlimited
+    # buffers runs the plain kernel after the device's check; the star with
+    # two buffer places runs the switch-group kernel)
+    cases = [W.config4(), W.config3(), W.switch2level_model(8, 4, 0, True), W.mesh3x3_two_groups(),
+             W.star_all_gather(6, 3, buffer=2, unicast=True), W.config1()]
+    kernels = {"switch2level_32_a2a_b0_u1": "plain", "star6_allgather_b2_u1": "switch"}
     refs, handles = [], []
     try:
         for wl in cases:
@@ -70,6 +74,8 @@ def test_static_entry_point_matches_workspace_path():
             assert P.pccl_synthesize_static(h, n, stream) == (n, ct)
             np.testing.assert_array_equal(_schedule(h, n), want)
             assert P.pccl_get_stats(h) == stats
+            if wl.name in kernels:
+                assert P.pccl_get_matcher(h) == kernels[wl.name]
         # every earlier context's schedule sat in the scratch a later call reused
         for h in handles[:-1]:
             assert _status(P.pccl_get_schedule, h, 0, 0) == "ESTATE"
