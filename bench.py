@@ -289,10 +289,14 @@ def main():
     avg_match_s = sum(match_ms) / len(match_ms) / 1e3
     alg_bytes = BYTES_PER_SCANNED_WORD * prof["scan_words"] + BYTES_PER_MATCH * n
     achieved = alg_bytes / avg_match_s / 1e9
+    traffic = measured_traffic(args.config)
     roofline = {"bound": "hbm", "achieved": round(achieved, 3), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBPS, 6), "traffic": measured_traffic(args.config),
+                "frac": round(achieved / PEAK_HBM_GBPS, 6), "traffic": traffic,
                 "kernel": "k_match", "kernel_ms": round(avg_match_s * 1e3, 4),
-                "alg_bytes_per_launch": alg_bytes, "scan_words": prof["scan_words"], "matches": n}
+                "alg_bytes_per_launch": alg_bytes, "scan_words": prof["scan_words"], "matches": n,
+                # the counter bytes (FETCH_SIZE + WRITE_SIZE, calibrated) over the same
+                # kernel time: HBM GB/s as the hardware counts it, MALL hits included
+                "traffic_GBps": None if traffic is None else round(traffic / avg_match_s / 1e9, 3)}
 
     out = {
         "metric": "synthesis wall time (s) + link-chunk matches/s, 512-NPU All-to-All; HBM GB/s",
