@@ -498,6 +498,13 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     const uint32_t tid = threadIdx.x;
     // a workgroup with one group keeps its tables and state in LDS
     if (!resident || first_window) load_group_state(ly, sz, gp, sh);
+    const uint32_t fl = filter_log2(gp.nU);
+    // the sending filter is built once per window, from the transfers in
+    // flight on the unicast switches' out-links at t0 (a superset at every
+    // later event of the window: a set bit only costs the exact check), and
+    // commits add theirs as they happen; cleared here, filled below
+    const uint32_t nfw = gp.nU ? (gp.nU << fl) >> 5 : 0u;
+    for (uint32_t x = tid; x < nfw; x += ST) sh.filt[x] = 0u;
     // arrivals at the group's sources inside the window, from the entries
     // published at t0 (the source's in-links, pair p of source j): eight
     // pairs per thread, so one pass covers a group's 8,192 pairs with two
@@ -589,6 +596,14 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         atomicOr((unsigned long long *)&sh.amask[li[k]], 1ull << qb[k]);
             }
         }
+        if (gp.nU)
+            for (uint32_t i = tid; i < gp.nL; i += ST) {
+                const uint32_t u = sh.luni[i];
+                if (u != SW_NONE8 && sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] > (uint64_t)t0) {
+                    const uint32_t b = filter_bit(u, sh.infl[i], fl);
+                    atomicOr(&sh.filt[b >> 5], 1u << (b & 31u));
+                }
+            }
         __syncthreads();
     }
     for (uint32_t x = tid; x < SW_HASH_WORDS; x += ST) {
@@ -600,7 +615,6 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     __syncthreads();
     uint32_t par = 0;  // this round's rflag word
     int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
-    const uint32_t fl = filter_log2(gp.nU);
     for (;;) {
         // next event of the group: a transfer into it ends, or a chunk
         // arrives at one of its sources (time 0 opens the first window)
@@ -615,21 +629,6 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         }
         const uint32_t t = block_min(sh, m);
         if (t == NONE32) break;
-        if (gp.nU) {
-            // the chunks in flight on the unicast switches' out-links at t
-            // (commits at t add theirs as they happen)
-            const uint32_t nfw = (gp.nU << fl) >> 5;
-            for (uint32_t x = tid; x < nfw; x += ST) sh.filt[x] = 0u;
-            __syncthreads();
-            for (uint32_t i = tid; i < gp.nL; i += ST) {
-                const uint32_t u = sh.luni[i];
-                if (u != SW_NONE8 && sh.infl[i] != NONE32 && sh.busy[i] > t) {
-                    const uint32_t b = filter_bit(u, sh.infl[i], fl);
-                    atomicOr(&sh.filt[b >> 5], 1u << (b & 31u));
-                }
-            }
-            __syncthreads();
-        }
         for (;;) {
             // picks of the free links (a full buffer admits nothing), in three
             // steps inside each wave: every free link's lowest explicit
