@@ -94,6 +94,9 @@ struct SwShared {
     // next send-log slot of each destination of the group (its segment)
     unsigned long long lcur[SW_MAX_LINKS];
     uint32_t red[SWAVES];
+    // per wave, at the window barrier: earliest transfer end, transfers
+    // committed, error flag (reduced by the thread that publishes the slot)
+    uint32_t xr_t[SWAVES], xr_s[SWAVES], xr_e[SWAVES];
     uint32_t x_tmin, x_err, x_ok;
     unsigned long long x_sent;
 };
@@ -160,18 +163,38 @@ __device__ uint32_t block_min(SwShared &sh, uint32_t v)
 // transfers committed, earliest transfer end in flight) in its own 128-byte
 // slot; wave 0 polls all slots.  Two slot sets alternate, so a workgroup
 // that is already one barrier ahead does not overwrite a slot still read.
+// tmin, sent and err are each thread's own: every wave reduces its threads'
+// values into an LDS slot before the workgroup barrier, and the thread that
+// publishes combines the waves' slots after it.
 __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tmin, uint32_t sent, uint32_t err,
                         SwShared &sh)
 {
-    const uint32_t nb = gridDim.x, lane = threadIdx.x & 63;
+    const uint32_t nb = gridDim.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint64_t tag = (uint64_t)(gen & 0xFFFu) << 52;
     uint64_t *slot = xslot + (uint64_t)(gen & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
+    for (int off = 32; off; off >>= 1) {
+        tmin = min(tmin, (uint32_t)__shfl_xor((int)tmin, off));
+        sent += (uint32_t)__shfl_xor((int)sent, off);
+        err |= (uint32_t)__shfl_xor((int)err, off);
+    }
+    if (lane == 0) {
+        sh.xr_t[wave] = tmin;
+        sh.xr_s[wave] = sent;
+        sh.xr_e[wave] = err;
+    }
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores and atomics are done
     __syncthreads();
-    if (threadIdx.x == 0)
+    if (threadIdx.x == 0) {
+        uint32_t bt = NONE32, bs = 0, be = 0;
+        for (uint32_t w = 0; w < SWAVES; w++) {
+            bt = min(bt, sh.xr_t[w]);
+            bs += sh.xr_s[w];
+            be |= sh.xr_e[w];
+        }
         __hip_atomic_store(&slot[(uint64_t)blockIdx.x * XSLOT_WORDS],
-                           tag | ((uint64_t)(err ? 1u : 0u) << 51) | ((uint64_t)(sent & 0x7FFFFu) << 32) | tmin,
+                           tag | ((uint64_t)(be ? 1u : 0u) << 51) | ((uint64_t)(bs & 0x7FFFFu) << 32) | bt,
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     if (threadIdx.x < 64) {
         uint32_t spins = 0, ok = 1, tn = NONE32, e = 0;
         unsigned long long s = 0;
@@ -604,15 +627,15 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     atomicOr(&sh.filt[b >> 5], 1u << (b & 31u));
                 }
             }
+        // the round tables start empty
+        for (uint32_t x = tid; x < SW_HASH_WORDS; x += ST) {
+            sh.hd[x] = 0u;
+            sh.hu[x] = 0u;
+        }
+        for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
+        if (tid < 2) sh.rflag[tid] = 0u;
         __syncthreads();
     }
-    for (uint32_t x = tid; x < SW_HASH_WORDS; x += ST) {
-        sh.hd[x] = 0u;
-        sh.hu[x] = 0u;
-    }
-    for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
-    if (tid < 2) sh.rflag[tid] = 0u;
-    __syncthreads();
     uint32_t par = 0;  // this round's rflag word
     int64_t t_prev = first_window ? -1 : (int64_t)t0 - 1;
     for (;;) {
@@ -680,38 +703,46 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     lim = min(sh.hi[i], bxv);
                 }
                 const bool scan = free && cu < lim;
-                const uint64_t smask = __ballot(scan);
-                if (smask) {
-                    // G = 64 / next_pow2(k) lanes per scanning link, two
-                    // words per lane per step; a min over each lane group
-                    // gives the first hit (the new cursor) and the first hit
-                    // the source switch is not sending (the row candidate)
-                    if (scan) sh.wsl[wave][__popcll(smask & ((1ull << lane) - 1ull))] = (uint8_t)lane;
-                    wave_sync();
-                    const uint32_t ks = (uint32_t)__popcll(smask);
-                    const uint32_t lg = ks <= 1u ? 0u : 32u - (uint32_t)__builtin_clz(ks - 1u);
-                    const uint32_t G = 64u >> lg, g = lane >> (6u - lg), sub = lane & (G - 1u);
-                    const bool act = g < ks;
-                    const uint32_t jl = sh.wsl[wave][act ? g : 0u];
-                    const uint32_t cj = (uint32_t)__shfl((int)cu, (int)jl);
-                    const uint32_t lj = (uint32_t)__shfl((int)lim, (int)jl);
-                    const uint32_t uj = (uint32_t)__shfl((int)u, (int)jl);
-                    const uint32_t ij = (wave << 6) | jl;
-                    const uint64_t *hrow = ly.holds + (uint64_t)sh.lsrc[ij] * sz.Wp;
-                    const uint64_t *nrow = ly.needs + (uint64_t)sh.ldst[ij] * sz.Wp;
-                    const uint64_t wl = ((uint64_t)lj + 63u) >> 6;
-                    uint64_t pos = (cj >> 6) & ~1ull;
-                    bool live = act && cj < lj;
-                    uint32_t fh = NONE32, rc = NONE32;
-                    while (__ballot(live)) {
+                if (__ballot(scan)) {
+                    // Steps of G = 64 / next_pow2(k) lanes for each of the k
+                    // links still scanning, two words per lane; the lanes are
+                    // dealt again before every step, so the few links whose
+                    // scan runs long get the whole wave.  A link's position,
+                    // first hit (its new cursor) and first hit the source
+                    // switch is not sending (its row candidate) stay on the
+                    // link's own lane; a min over each lane group gives the
+                    // step's result, which the group's first lane hands back.
+                    const uint64_t below = (1ull << lane) - 1ull;
+                    uint32_t opos = (cu >> 6) & ~1u, ofh = NONE32, orc = NONE32;
+                    const uint32_t owl = (uint32_t)(((uint64_t)lim + 63u) >> 6);
+                    bool olive = scan;
+                    for (;;) {
+                        const uint64_t lm = __ballot(olive);
+                        if (!lm) break;
+                        const uint32_t rank = (uint32_t)__popcll(lm & below);
+                        if (olive) sh.wsl[wave][rank] = (uint8_t)lane;
+                        wave_sync();
+                        const uint32_t ks = (uint32_t)__popcll(lm);
+                        const uint32_t lg = ks <= 1u ? 0u : 32u - (uint32_t)__builtin_clz(ks - 1u);
+                        const uint32_t G = 64u >> lg, g = lane >> (6u - lg), sub = lane & (G - 1u);
+                        const bool act = g < ks;
+                        const uint32_t jl = sh.wsl[wave][act ? g : 0u];
+                        const uint32_t pj = (uint32_t)__shfl((int)opos, (int)jl);
+                        const uint32_t cj = (uint32_t)__shfl((int)cu, (int)jl);
+                        const uint32_t lj = (uint32_t)__shfl((int)lim, (int)jl);
+                        const uint32_t uj = (uint32_t)__shfl((int)u, (int)jl);
+                        const uint32_t ij = (wave << 6) | jl;
+                        const uint64_t *hrow = ly.holds + (uint64_t)sh.lsrc[ij] * sz.Wp;
+                        const uint64_t *nrow = ly.needs + (uint64_t)sh.ldst[ij] * sz.Wp;
+                        const uint64_t wl = ((uint64_t)lj + 63u) >> 6;
                         // loads at a clamped, always valid word pair (rows
                         // have an even number of words), masked after
-                        const uint64_t w = pos + 2ull * sub;
+                        const uint64_t w = (uint64_t)pj + 2ull * sub;
                         const uint64_t wc = min<uint64_t>(w, sz.Wp - 2);
                         const uint4 hv = *reinterpret_cast<const uint4 *>(hrow + wc);
                         const uint4 nv = *reinterpret_cast<const uint4 *>(nrow + wc);
                         uint32_t lfh = NONE32, lrc = NONE32;
-                        if (live && w < wl) {
+                        if (act && w < wl) {
                             uint64_t a[2];
                             a[0] = ((((uint64_t)hv.y << 32) | hv.x) & (((uint64_t)nv.y << 32) | nv.x)) &
                                    range_bits(w, cj, lj);
@@ -734,18 +765,27 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                             lfh = min(lfh, (uint32_t)__shfl_xor((int)lfh, (int)off));
                             lrc = min(lrc, (uint32_t)__shfl_xor((int)lrc, (int)off));
                         }
-                        if (live) {
-                            fh = min(fh, lfh);
-                            rc = lrc;
-                            pos += 2ull * G;
-                            if (lrc != NONE32 || pos >= wl) live = false;
+                        // (an owner's group is its rank among the live links)
+                        const uint32_t src = (rank * G) & 63u;
+                        const uint32_t rfh = (uint32_t)__shfl((int)lfh, (int)src);
+                        const uint32_t rrc = (uint32_t)__shfl((int)lrc, (int)src);
+                        if (olive) {
+                            ofh = min(ofh, rfh);
+                            opos += 2u * G;
+                            if (rrc != NONE32) {
+                                orc = rrc;
+                                olive = false;
+                            } else if (opos >= owl) {
+                                olive = false;
+                            }
                         }
+                        // (the list is rewritten for the next step)
+                        wave_sync();
                     }
-                    if (act && sub == 0) {
-                        sh.pick[ij] = rc;
-                        sh.cur[ij] = fh != NONE32 ? fh : max(cj, lj);
+                    if (scan) {
+                        sh.pick[i] = orc;
+                        sh.cur[i] = ofh != NONE32 ? ofh : max(cu, lim);
                     }
-                    wave_sync();
                 }
                 uint32_t pk = NONE32;
                 if (free) {
@@ -1057,8 +1097,9 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             ly.sw.pool_n[gp.pool_base + x] = sh.pn[x];
         }
         for (uint32_t x = tid; x < gp.nB; x += ST) ly.sw.occ[gp.bbase + x] = sh.occ[x];
+        // (the next group's state replaces this one's in LDS)
+        __syncthreads();
     }
-    __syncthreads();
 }
 
 // Can the no-multicast rule change the schedule?  Only when two
@@ -1125,15 +1166,7 @@ __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
         acc.sent = 0;
         for (uint32_t q = q0; q < q1; q++)
             match_group(ly, sz, load_group(sw, sw.blk_list[q]), sh, t0, t1, k == 0, resident, acc);
-        const uint32_t btmin = block_min(sh, acc.tmin);
-        uint32_t bsent = acc.sent;
-        for (int off = 32; off; off >>= 1) bsent += (uint32_t)__shfl_xor(bsent, off);
-        if ((tid & 63) == 0) sh.red[tid >> 6] = bsent;
-        __syncthreads();
-        bsent = 0;
-        for (uint32_t w = 0; w < SWAVES; w++) bsent += sh.red[w];
-        const int berr = __syncthreads_or(acc.err != 0);
-        if (!sw_sync(ctl, ly.xslot, ++gen, btmin, bsent, (uint32_t)berr, sh)) break;
+        if (!sw_sync(ctl, ly.xslot, ++gen, acc.tmin, acc.sent, acc.err ? 1u : 0u, sh)) break;
         remaining -= sh.x_sent;
         if (sh.x_err || remaining == 0) break;
         if (sh.x_tmin == NONE32) {
