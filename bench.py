@@ -38,22 +38,32 @@ COUNTERS = os.path.join(ROOT, "profiles", "k_match_switch2level_512_a2a_hbm_coun
 MATCH_SRC = os.path.join(ROOT, "paper_2606_07019_amd", "csrc", "pccl_match.hip")
 
 
+def code_sha256(path: str) -> str:
+    """sha256 of a source file's code: // comments, surrounding blanks and
+    empty lines dropped, so that a comment edit keeps the hash."""
+    import hashlib
+    lines = []
+    with open(path) as f:
+        for line in f:
+            code = line.split("//", 1)[0].strip()
+            if code:
+                lines.append(code)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()
+
+
 def measured_traffic(config: int):
     """HBM bytes per k_match launch from the committed counter summary, or
-    None when the kernel source changed since the counters were taken."""
-    import hashlib
+    None when the kernel's code changed since the counters were taken."""
     if config != 4 or not os.path.exists(COUNTERS):
         return None
     want, traffic = None, None
     with open(COUNTERS) as f:
         for line in f:
-            if "k_match source sha256:" in line:
+            if "k_match code sha256:" in line:
                 want = line.split(":", 1)[1].strip()
             elif "k_match traffic bytes per launch:" in line:
                 traffic = int(line.split(":", 1)[1].strip())
-    with open(MATCH_SRC, "rb") as f:
-        have = hashlib.sha256(f.read()).hexdigest()
-    return traffic if want == have else None
+    return traffic if want == code_sha256(MATCH_SRC) else None
 
 
 def log(*a):
