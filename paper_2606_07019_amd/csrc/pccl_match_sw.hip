@@ -148,9 +148,58 @@ __device__ inline uint64_t link_key(const SwShared &sh, uint32_t i)
     return ((uint64_t)sh.ltim[i] << 32) | sh.llink[i];
 }
 
+// Cross-lane steps that need no lane-index registers (index arithmetic the
+// compiler would hoist out of the loops and spill at this kernel's register
+// limit): a lane swizzle exchanges the lanes whose ids differ in bit K
+// inside each half of the wave, and the two halves meet through two lane
+// reads, whose result is the same on every lane.
+template <uint32_t K>
+__device__ __forceinline__ uint32_t swz_xor(uint32_t v)
+{
+    static_assert(K >= 1 && K <= 16 && (K & (K - 1)) == 0, "one lane-id bit inside a half wave");
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (int)((K << 10) | 0x1Fu));
+}
+
+__device__ __forceinline__ uint32_t lane_at(uint32_t v, int l)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+
+__device__ __forceinline__ uint32_t wave_min(uint32_t v)
+{
+    v = min(v, swz_xor<16>(v));
+    v = min(v, swz_xor<8>(v));
+    v = min(v, swz_xor<4>(v));
+    v = min(v, swz_xor<2>(v));
+    v = min(v, swz_xor<1>(v));
+    return min(lane_at(v, 0), lane_at(v, 32));
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v)
+{
+    v += swz_xor<16>(v);
+    v += swz_xor<8>(v);
+    v += swz_xor<4>(v);
+    v += swz_xor<2>(v);
+    v += swz_xor<1>(v);
+    return lane_at(v, 0) + lane_at(v, 32);
+}
+
+__device__ __forceinline__ uint32_t wave_or(uint32_t v)
+{
+    v |= swz_xor<16>(v);
+    v |= swz_xor<8>(v);
+    v |= swz_xor<4>(v);
+    v |= swz_xor<2>(v);
+    v |= swz_xor<1>(v);
+    return lane_at(v, 0) | lane_at(v, 32);
+}
+
+static_assert(MAX_MATCH_GRID <= (1u << 13), "the window exchange sums 19-bit counts in 32 bits");
+
 __device__ uint32_t block_min(SwShared &sh, uint32_t v)
 {
-    for (int off = 32; off; off >>= 1) v = min(v, (uint32_t)__shfl_xor(v, off));
+    v = wave_min(v);
     if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = v;
     __syncthreads();
     uint32_t m = NONE32;
@@ -172,11 +221,9 @@ __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tm
     const uint32_t nb = gridDim.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint64_t tag = (uint64_t)(gen & 0xFFFu) << 52;
     uint64_t *slot = xslot + (uint64_t)(gen & 1u) * MAX_MATCH_GRID * XSLOT_WORDS;
-    for (int off = 32; off; off >>= 1) {
-        tmin = min(tmin, (uint32_t)__shfl_xor((int)tmin, off));
-        sent += (uint32_t)__shfl_xor((int)sent, off);
-        err |= (uint32_t)__shfl_xor((int)err, off);
-    }
+    tmin = wave_min(tmin);
+    sent = wave_sum(sent);
+    err = wave_or(err);
     if (lane == 0) {
         sh.xr_t[wave] = tmin;
         sh.xr_s[wave] = sent;
@@ -230,15 +277,15 @@ __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tm
         }
         // acquire: drop cached lines that other workgroups wrote
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        for (int off = 32; off; off >>= 1) {
-            tn = min(tn, (uint32_t)__shfl_xor(tn, off));
-            e |= (uint32_t)__shfl_xor(e, off);
-            s += (unsigned long long)__shfl_xor(s, off);
-        }
+        // (a slot's count has 19 bits and there are at most MAX_MATCH_GRID
+        // slots: the sum fits in 32 bits)
+        tn = wave_min(tn);
+        e = wave_or(e);
+        const uint32_t s32 = wave_sum((uint32_t)s);
         if (lane == 0) {
             sh.x_tmin = tn;
             sh.x_err = e;
-            sh.x_sent = s;
+            sh.x_sent = s32;
             sh.x_ok = ok;
         }
     }
@@ -560,10 +607,30 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         const uint32_t lane = tid & 63u, wave = tid >> 6;
         const uint32_t np_me =
             tid < gp.nL ? (uint32_t)(sh.poff[sh.lsrcj[tid] + 1] - sh.poff[sh.lsrcj[tid]]) : 0u;
-        uint32_t inc = np_me;
-        for (uint32_t o = 1; o < 64; o <<= 1) {
-            const uint32_t y = (uint32_t)__shfl_up((int)inc, (int)o);
-            if (lane >= o) inc += y;
+        // inclusive prefix over the wave, one lane-id bit per step: `blk`
+        // is the sum of the lane's aligned block of 2^k lanes, `inc` its
+        // prefix inside the block
+        uint32_t inc = np_me, blk = np_me;
+        {
+            uint32_t o;
+            o = swz_xor<1>(blk);
+            inc += (lane & 1u) ? o : 0u;
+            blk += o;
+            o = swz_xor<2>(blk);
+            inc += (lane & 2u) ? o : 0u;
+            blk += o;
+            o = swz_xor<4>(blk);
+            inc += (lane & 4u) ? o : 0u;
+            blk += o;
+            o = swz_xor<8>(blk);
+            inc += (lane & 8u) ? o : 0u;
+            blk += o;
+            o = swz_xor<16>(blk);
+            inc += (lane & 16u) ? o : 0u;
+            blk += o;
+            // (the lane read runs on every lane, outside the select)
+            const uint32_t lo = lane_at(blk, 0);
+            inc += (lane & 32u) ? lo : 0u;
         }
         if (lane == 63) sh.red[wave] = inc;
         if (tid < gp.nL) sh.amask[tid] = 0ull;
@@ -761,9 +828,30 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                                 }
                             }
                         }
-                        for (uint32_t off = 1; off < G; off <<= 1) {
-                            lfh = min(lfh, (uint32_t)__shfl_xor((int)lfh, (int)off));
-                            lrc = min(lrc, (uint32_t)__shfl_xor((int)lrc, (int)off));
+                        // (G is the same on every lane of the wave)
+                        if (G > 1u) {
+                            lfh = min(lfh, swz_xor<1>(lfh));
+                            lrc = min(lrc, swz_xor<1>(lrc));
+                        }
+                        if (G > 2u) {
+                            lfh = min(lfh, swz_xor<2>(lfh));
+                            lrc = min(lrc, swz_xor<2>(lrc));
+                        }
+                        if (G > 4u) {
+                            lfh = min(lfh, swz_xor<4>(lfh));
+                            lrc = min(lrc, swz_xor<4>(lrc));
+                        }
+                        if (G > 8u) {
+                            lfh = min(lfh, swz_xor<8>(lfh));
+                            lrc = min(lrc, swz_xor<8>(lrc));
+                        }
+                        if (G > 16u) {
+                            lfh = min(lfh, swz_xor<16>(lfh));
+                            lrc = min(lrc, swz_xor<16>(lrc));
+                        }
+                        if (G > 32u) {
+                            lfh = min(lane_at(lfh, 0), lane_at(lfh, 32));
+                            lrc = min(lane_at(lrc, 0), lane_at(lrc, 32));
                         }
                         // (an owner's group is its rank among the live links)
                         const uint32_t src = (rank * G) & 63u;
