@@ -97,6 +97,8 @@ struct SwShared {
     // per wave, at the window barrier: earliest transfer end, transfers
     // committed, error flag (reduced by the thread that publishes the slot)
     uint32_t xr_t[SWAVES], xr_s[SWAVES], xr_e[SWAVES];
+    // word positions the workgroup's scans passed (whole run)
+    unsigned long long st_words;
     uint32_t x_tmin, x_err, x_ok;
     unsigned long long x_sent;
 };
@@ -160,6 +162,16 @@ __device__ __forceinline__ uint32_t swz_xor(uint32_t v)
     return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (int)((K << 10) | 0x1Fu));
 }
 
+// v itself, opaque to the compiler at this point: address arithmetic
+// derived from it is done where it is used instead of being hoisted out of
+// the window loop (where, at the register limit, it would be spilled and
+// reloaded behind a wait for every load in flight).
+__device__ __forceinline__ uint32_t here(uint32_t v)
+{
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
 __device__ __forceinline__ uint32_t lane_at(uint32_t v, int l)
 {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
@@ -200,7 +212,7 @@ static_assert(MAX_MATCH_GRID <= (1u << 13), "the window exchange sums 19-bit cou
 __device__ uint32_t block_min(SwShared &sh, uint32_t v)
 {
     v = wave_min(v);
-    if ((threadIdx.x & 63) == 0) sh.red[threadIdx.x >> 6] = v;
+    if ((threadIdx.x & 63) == 0) sh.red[here(threadIdx.x) >> 6] = v;
     __syncthreads();
     uint32_t m = NONE32;
     for (uint32_t w = 0; w < SWAVES; w++) m = min(m, sh.red[w]);
@@ -225,9 +237,10 @@ __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tm
     sent = wave_sum(sent);
     err = wave_or(err);
     if (lane == 0) {
-        sh.xr_t[wave] = tmin;
-        sh.xr_s[wave] = sent;
-        sh.xr_e[wave] = err;
+        const uint32_t wv = here(wave);
+        sh.xr_t[wv] = tmin;
+        sh.xr_s[wv] = sent;
+        sh.xr_e[wv] = err;
     }
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores and atomics are done
     __syncthreads();
@@ -581,15 +594,16 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     // dependent round trips (slot indices, then the entries)
     static_assert(SW_MAX_PAIRS <= 8u * ST, "one pass of eight pairs per thread");
     if (gp.nP) {
+        const uint32_t tp = here(tid);
         uint32_t sl[8];
         uint64_t e[8];
 #pragma unroll
-        for (uint32_t k = 0; k < 8; k++) sl[k] = ly.sw.p_slot[gp.pbase + min(tid + k * ST, gp.nP - 1u)];
+        for (uint32_t k = 0; k < 8; k++) sl[k] = ly.sw.p_slot[gp.pbase + min(tp + k * ST, gp.nP - 1u)];
 #pragma unroll
         for (uint32_t k = 0; k < 8; k++) e[k] = ly.snap[sl[k]];
 #pragma unroll
         for (uint32_t k = 0; k < 8; k++) {
-            const uint32_t p = tid + k * ST, b = (uint32_t)e[k];
+            const uint32_t p = tp + k * ST, b = (uint32_t)e[k];
             if (p >= gp.nP) continue;
             const bool in = e[k] != NONE64 && b >= t0 && (uint64_t)b < t1;
             sh.arr_t[p] = in ? b : NONE32;
@@ -632,7 +646,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             const uint32_t lo = lane_at(blk, 0);
             inc += (lane & 32u) ? lo : 0u;
         }
-        if (lane == 63) sh.red[wave] = inc;
+        if (lane == 63) sh.red[here(wave)] = inc;
         if (tid < gp.nL) sh.amask[tid] = 0ull;
         __syncthreads();
         uint32_t below = 0, tot = 0;
@@ -815,7 +829,6 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                                    range_bits(w, cj, lj);
                             a[1] = ((((uint64_t)hv.w << 32) | hv.z) & (((uint64_t)nv.w << 32) | nv.z)) &
                                    range_bits(w + 1, cj, lj);
-                            acc.words += 2;
 #pragma unroll
                             for (uint32_t k = 0; k < 2; k++) {
                                 for (uint64_t y = lrc == NONE32 ? a[k] : 0ull; y; y &= y - 1) {
@@ -827,6 +840,11 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                                     }
                                 }
                             }
+                        }
+                        {
+                            // word positions of the step, counted by the wave
+                            const uint64_t sm = __ballot(act && w < wl);
+                            if (lane == 0 && sm) atomicAdd(&sh.st_words, 2ull * (uint64_t)__popcll(sm));
                         }
                         // (G is the same on every lane of the wave)
                         if (G > 1u) {
@@ -1243,6 +1261,8 @@ __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
     const unsigned long long max_windows = ctl->needs_total + 2ull;
     unsigned long long remaining = ctl->needs_total;
     SwAcc acc = {NONE32, 0u, 0u, 0u, 0ull, 0ull, 0ull};
+    if (tid == 0) sh.st_words = 0ull;
+    __syncthreads();
     uint32_t t0 = 0, gen = 0;
     unsigned long long k = 0;
     for (;; k++) {
@@ -1278,6 +1298,8 @@ __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
         acc.clashes += (unsigned long long)__shfl_xor(acc.clashes, off);
         acc.words += (unsigned long long)__shfl_xor(acc.words, off);
     }
+    __syncthreads();
+    if (tid == 0 && sh.st_words) atomicAdd(&ctl->scan_words, sh.st_words);
     if ((tid & 63) == 0) {
         atomicMax(&ctl->cstar, acc.cstar);
         if (acc.clashes) atomicAdd(&ctl->clashes, acc.clashes);
