@@ -184,8 +184,8 @@ pccl_status pccl_set_collective(pccl_ctx *ctx, uint32_t n_chunks, uint64_t chunk
  * matcher runs one workgroup per switch group: a unicast switch's
  * out-neighbours, and a limited switch together with its out-neighbours,
  * form one group.  PCCL_EUNSUPPORTED (from pccl_workspace_bytes /
- * pccl_set_workspace) when a group has more than 1024 in-links, 1024
- * distinct sources of those links, 8192 in-links of those sources, a source
+ * pccl_set_workspace) when a group has more than 768 in-links, 768
+ * distinct sources of those links, 6144 in-links of those sources, a source
  * with more than 64 in-links, 64 limited or unicast switches, or more than
  * 1024 buffer places (capacities at or above the chunk count count as
  * unlimited).  Buffers can deadlock: then

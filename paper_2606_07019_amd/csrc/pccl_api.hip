@@ -397,6 +397,17 @@ pccl_status build_switch_tables(pccl_ctx *c)
         pool += pl;
         c->sw_links.push_back(nl);
     }
+    // the matcher indexes its snapshot entries by group link position (each
+    // link is an in-link of exactly one group's destination): a pair names
+    // the position of its in-link
+    {
+        std::vector<uint32_t> gpos(L, NONE32);
+        for (uint32_t x = 0; x < (uint32_t)lk_slot.size(); x++) gpos[lk_slot[x]] = x;
+        for (uint32_t &v : p_slot) {
+            if (gpos[v] == NONE32) return fail(c, PCCL_EINTERNAL, "arrival pair on slot %u outside every group", v);
+            v = gpos[v];
+        }
+    }
     // with no binding buffer limit only the no-multicast rule can change the
     // schedule, and only if two out-neighbours of one unicast switch need the
     // same chunk: the device checks that after the setup (the needs rows

@@ -28,10 +28,12 @@ constexpr uint32_t XSLOT_WORDS = 16;        // one 128-byte line per window exch
 
 // Switch-model matching kernel envelope (one workgroup owns a switch group:
 // a switch with its out-neighbours; checked on the host).
-constexpr uint32_t SW_THREADS = 1024;
-constexpr uint32_t SW_MAX_LINKS = 1024;  // in-links of the destinations of one group
-constexpr uint32_t SW_MAX_SRC = 1024;    // distinct sources of those links
-constexpr uint32_t SW_MAX_PAIRS = 8192;  // in-links of those sources (arrival slots)
+// 768 threads: three waves per SIMD, so a wave may hold 168 registers
+// (with four waves, 128 were not enough for the pick stage).
+constexpr uint32_t SW_THREADS = 768;
+constexpr uint32_t SW_MAX_LINKS = 768;   // in-links of the destinations of one group
+constexpr uint32_t SW_MAX_SRC = 768;     // distinct sources of those links
+constexpr uint32_t SW_MAX_PAIRS = 6144;  // in-links of those sources (arrival slots)
 constexpr uint32_t SW_MAX_SW = 64;       // unicast or limited switches in one group
 constexpr uint32_t SW_MAX_SRC_IN = 64;   // in-links of one source of a group link (one bit each in a link's arrival mask)
 constexpr uint32_t SW_MAX_POOL = 1024;   // buffer places of a group's limited switches
@@ -102,7 +104,7 @@ struct SwTab {
     const uint32_t *lk_sbuf;  // group index of its source if a limited switch, else NONE32
     const uint32_t *d_off;    // [nD + 1] per group: links of destination dl
     const uint32_t *s_poff;   // [nS + 1] per group: arrival pairs of source j
-    const uint32_t *p_slot;   // slot of each pair's link (an in-link of the source)
+    const uint32_t *p_slot;   // group link position of each pair's link (an in-link of the source)
     const uint32_t *u_off;    // [nU + 1] per group: out-links of unicast switch u
     const uint32_t *u_list;   // group-local link indices
     const uint32_t *b_cap;    // [nB + 1] per group: buffer capacity of limited switch b

@@ -26,11 +26,15 @@
 //
 // Groups interact only through chunk arrivals, which take at least the
 // smallest link time, so the windows [t0, t0 + Tmin) of the plain matcher
-// carry over: each window folds the previous window's arrivals into the
-// holds rows and publishes the transfers in flight at t0 (first grid
-// barrier), then every group matches its events inside the window against
-// holds-at-t0 plus the arrival list read from those entries (second grid
-// barrier, which also finds the next event time).
+// carry over, with one grid barrier per window: every group reads the
+// transfers in flight at t0 (published by their owners at the end of the
+// previous window, in one of two alternating planes), folds the transfers
+// into its own destinations that end inside the window into their holds
+// rows at once, and matches its events against the rows plus the window's
+// arrival list; a row chunk whose arrival in the window comes after the
+// event is skipped, so the early fold never shows a chunk before its time.
+// The barrier at the window's end publishes the next window's entries and
+// finds the next event time.
 #include "pccl_internal.h"
 
 namespace pccl {
@@ -40,6 +44,10 @@ constexpr uint32_t ST = SW_THREADS;
 constexpr uint32_t SWAVES = ST / 64;
 constexpr uint32_t SW_SPIN_LIMIT = 1u << 24;
 constexpr uint32_t SCAN_STEP = 4;  // row words one link's scan loads at once
+// (link, pair) items of the arrival masks a thread reads in one batch of
+// need-word loads: the 8,192 items of a 576-link rail-switch group take
+// one batch at 768 threads
+constexpr uint32_t AMASK_BATCH = 12;
 constexpr uint32_t PEND = 2;       // needed chunks below a link's cursor it keeps as explicit candidates
 static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
@@ -306,27 +314,6 @@ __device__ bool sw_sync(Control *ctl, uint64_t *xslot, uint32_t gen, uint32_t tm
     return sh.x_ok != 0;
 }
 
-// First half of a window, for one group: fold the arrivals of the previous
-// window into the destinations' holds rows, then publish the transfers in
-// flight at t0 (the entries other groups read their arrival lists from).
-__device__ void fold_and_publish(const Layout &ly, const Sizes &sz, const SwGroup &gp, uint32_t t0,
-                                 const SwShared &sh, bool in_lds)
-{
-    for (uint32_t i = threadIdx.x; i < gp.nL; i += ST) {
-        const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
-        const uint32_t d = in_lds ? sh.ldst[i] : ly.ldst[ly.slot_link[sl]];
-        const uint64_t e = ly.snap[sl];
-        if (e != NONE64 && (uint32_t)e < t0) {
-            const uint32_t c = (uint32_t)(e >> 32);
-            __hip_atomic_fetch_or(&ly.holds[(uint64_t)d * sz.Wp + (c >> 6)], 1ull << (c & 63u), __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT);
-        }
-        const uint32_t in = in_lds ? sh.infl[i] : ly.infl[sl], b = in_lds ? sh.busy[i] : ly.busy[sl];
-        const uint64_t ne = (in != NONE32 && b >= t0) ? (((uint64_t)in << 32) | b) : NONE64;
-        __hip_atomic_store(&ly.snap[sl], ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-}
-
 __device__ void load_group_state(const Layout &ly, const Sizes &sz, const SwGroup &gp, SwShared &sh)
 {
     const SwTab &sw = ly.sw;
@@ -449,6 +436,22 @@ __device__ inline bool clash_alone(const uint32_t *tab, uint32_t slot)
     return !((tab[slot >> 4] >> ((slot & 15u) * 2u + 1u)) & 1u);
 }
 
+// Chunk c, found in the holds row of link i's source, reaches the source
+// only after t: each group folds the transfers that end inside a window
+// into its destinations' rows when the window opens, so a row can show a
+// chunk before its arrival time.  Such a chunk is one of the window's
+// arrivals at the source that the link's destination needed at the window
+// start, so it is listed in the link's arrival mask, with its time.
+__device__ inline bool arrives_later(const SwShared &sh, uint32_t i, uint32_t c, uint32_t t)
+{
+    const uint32_t base = sh.poff[sh.lsrcj[i]];
+    for (uint64_t y = sh.amask[i]; y; y &= y - 1) {
+        const uint32_t p = base + (uint32_t)__builtin_ctzll(y);
+        if (sh.arr_c[p] == c && sh.arr_t[p] > t) return true;
+    }
+    return false;
+}
+
 // Bits of word w (chunks 64 w .. 64 w + 63) that lie in [lo, hi).
 __device__ inline uint64_t range_bits(uint64_t w, uint32_t lo, uint32_t hi)
 {
@@ -515,7 +518,7 @@ __device__ __attribute__((noinline)) uint32_t pick_link(const Layout &ly, const 
                         break;
                     }
                     if (first == NONE32) first = c;
-                    if (c >= skip && (u == NONE32 || !sending(sh, u, c, t))) {
+                    if (c >= skip && (u == NONE32 || !sending(sh, u, c, t)) && !arrives_later(sh, i, c, t)) {
                         row = c;
                         done = true;
                         break;
@@ -573,14 +576,28 @@ struct SwAcc {
     unsigned long long rounds, clashes, words;
 };
 
-// Second half of a window, for one group: the group's events inside
-// [t0, t1), in time order, each with its round loop.
+// A window of one group: its events inside [t0, t1), in time order, each
+// with its round loop.  snap_rd holds the transfers in flight when the
+// window opens (published at the end of the previous one, indexed by group
+// link position); the group publishes its own for the next window in
+// snap_wr at the end.
 __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp, SwShared &sh, uint32_t t0,
-                            uint64_t t1, bool first_window, bool resident, SwAcc &acc)
+                            uint64_t t1, bool first_window, bool resident, SwAcc &acc, const uint64_t *snap_rd,
+                            uint64_t *snap_wr)
 {
     const uint32_t tid = threadIdx.x;
     // a workgroup with one group keeps its tables and state in LDS
     if (!resident || first_window) load_group_state(ly, sz, gp, sh);
+    // the transfers into the group's destinations that end inside the
+    // window join the destinations' holds rows now (a reader skips a row
+    // chunk whose arrival in this window comes after its event, see
+    // arrives_later); the window exchange at its end makes them visible
+    for (uint32_t i = tid; i < gp.nL; i += ST) {
+        const uint32_t b = sh.busy[i], c = sh.infl[i];
+        if (c != NONE32 && b >= t0 && (uint64_t)b < t1)
+            __hip_atomic_fetch_or(&ly.holds[(uint64_t)sh.ldst[i] * sz.Wp + (c >> 6)], 1ull << (c & 63u),
+                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     const uint32_t fl = filter_log2(gp.nU);
     // the sending filter is built once per window, from the transfers in
     // flight on the unicast switches' out-links at t0 (a superset at every
@@ -600,7 +617,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
 #pragma unroll
         for (uint32_t k = 0; k < 8; k++) sl[k] = ly.sw.p_slot[gp.pbase + min(tp + k * ST, gp.nP - 1u)];
 #pragma unroll
-        for (uint32_t k = 0; k < 8; k++) e[k] = ly.snap[sl[k]];
+        for (uint32_t k = 0; k < 8; k++) e[k] = snap_rd[sl[k]];
 #pragma unroll
         for (uint32_t k = 0; k < 8; k++) {
             const uint32_t p = tp + k * ST, b = (uint32_t)e[k];
@@ -615,7 +632,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     // pair) items of all links, spread evenly over the workgroup's threads
     // (a block prefix over the links' pair counts, kept in `pick`, which
     // the rounds overwrite later); each thread loads the needs words of its
-    // items eight at a time, all in flight together, through the caches (a
+    // items AMASK_BATCH at a time, all in flight together, through the caches (a
     // superset: picks confirm each candidate)
     {
         const uint32_t lane = tid & 63u, wave = tid >> 6;
@@ -672,10 +689,10 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             uint32_t i = lo, q = x - sh.pick[i];
             uint32_t p0 = sh.poff[sh.lsrcj[i]], np = sh.poff[sh.lsrcj[i] + 1] - p0;
             while (x < xe) {
-                uint32_t li[8], qb[8], c[8];
-                bool v[8];
+                uint32_t li[AMASK_BATCH], qb[AMASK_BATCH], c[AMASK_BATCH];
+                bool v[AMASK_BATCH];
 #pragma unroll
-                for (uint32_t k = 0; k < 8; k++) {
+                for (uint32_t k = 0; k < AMASK_BATCH; k++) {
                     while (q >= np && i + 1 < gp.nL) {
                         q -= np;
                         i++;
@@ -690,12 +707,12 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     q++;
                 }
                 // unconditional loads (row 0, word 0 for an item without an arrival)
-                uint64_t nw[8];
+                uint64_t nw[AMASK_BATCH];
 #pragma unroll
-                for (uint32_t k = 0; k < 8; k++)
+                for (uint32_t k = 0; k < AMASK_BATCH; k++)
                     nw[k] = ly.needs[(uint64_t)(v[k] ? sh.ldst[li[k]] : 0u) * sz.Wp + (c[k] >> 6)];
 #pragma unroll
-                for (uint32_t k = 0; k < 8; k++)
+                for (uint32_t k = 0; k < AMASK_BATCH; k++)
                     if (v[k] && ((nw[k] >> (c[k] & 63u)) & 1ull))
                         atomicOr((unsigned long long *)&sh.amask[li[k]], 1ull << qb[k]);
             }
@@ -834,7 +851,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                                 for (uint64_t y = lrc == NONE32 ? a[k] : 0ull; y; y &= y - 1) {
                                     const uint32_t c = (uint32_t)((w + k) * 64 + (uint64_t)__builtin_ctzll(y));
                                     if (lfh == NONE32) lfh = c;
-                                    if (uj == NONE32 || !sent_by(sh, uj, c, t, fl)) {
+                                    if ((uj == NONE32 || !sent_by(sh, uj, c, t, fl)) && !arrives_later(sh, ij, c, t)) {
                                         lrc = c;
                                         break;
                                     }
@@ -1182,7 +1199,11 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         }
         sh.cur[i] = c;
         sh.hi[i] = h;
-        if (sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1) tm = min(tm, sh.busy[i]);
+        // the next window's entry: the transfer still in flight at its start
+        const bool fl_next = sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1;
+        __hip_atomic_store(&snap_wr[gp.lbase + i], fl_next ? (((uint64_t)sh.infl[i] << 32) | sh.busy[i]) : NONE64,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (fl_next) tm = min(tm, sh.busy[i]);
         if (!resident) {
             const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
             ly.cur[sl] = c;
@@ -1265,15 +1286,16 @@ __global__ void __launch_bounds__(ST) k_match_sw(Layout ly, Sizes sz)
     __syncthreads();
     uint32_t t0 = 0, gen = 0;
     unsigned long long k = 0;
+    // two snapshot planes (the first and the third; the second holds the
+    // pending candidates of groups that leave LDS), alternating by window
+    uint64_t *const plane[2] = {ly.snap, ly.snap + 2ull * sz.L};
     for (;; k++) {
         const uint64_t t1 = (uint64_t)t0 + sz.tmin;
-        for (uint32_t q = q0; q < q1; q++)
-            fold_and_publish(ly, sz, load_group(sw, sw.blk_list[q]), t0, sh, resident && k > 0);
-        if (!sw_sync(ctl, ly.xslot, ++gen, NONE32, 0u, 0u, sh)) break;
         acc.tmin = NONE32;
         acc.sent = 0;
         for (uint32_t q = q0; q < q1; q++)
-            match_group(ly, sz, load_group(sw, sw.blk_list[q]), sh, t0, t1, k == 0, resident, acc);
+            match_group(ly, sz, load_group(sw, sw.blk_list[q]), sh, t0, t1, k == 0, resident, acc, plane[k & 1],
+                        plane[(k + 1) & 1]);
         if (!sw_sync(ctl, ly.xslot, ++gen, acc.tmin, acc.sent, acc.err ? 1u : 0u, sh)) break;
         remaining -= sh.x_sent;
         if (sh.x_err || remaining == 0) break;
