@@ -72,6 +72,7 @@ struct SwShared {
     uint64_t amask[SW_MAX_LINKS];     // arrivals (bit q: pair q of the source) the link's destination needs
     uint32_t pend[SW_MAX_LINKS][PEND];  // needed arrivals outside [cur, hi), NONE32 = empty
     uint32_t hi[SW_MAX_LINKS];          // a link's row candidates lie in [cur, hi) (or in pend)
+    uint32_t foldc[SW_MAX_LINKS];       // the chunk a link's transfer delivers inside the window, NONE32 if none
     uint16_t uoff[SW_MAX_SW + 1], ulist[SW_MAX_LINKS];
     uint32_t bcap[SW_MAX_SW];
     uint16_t bpoff[SW_MAX_SW + 1], booff[SW_MAX_SW + 1];
@@ -589,14 +590,14 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     // a workgroup with one group keeps its tables and state in LDS
     if (!resident || first_window) load_group_state(ly, sz, gp, sh);
     // the transfers into the group's destinations that end inside the
-    // window join the destinations' holds rows now (a reader skips a row
-    // chunk whose arrival in this window comes after its event, see
-    // arrives_later); the window exchange at its end makes them visible
+    // window: their chunks join the destinations' holds rows during the
+    // window (issued at its end, next to the published entries, so that no
+    // wait for a load in between waits for them too); a reader skips a row
+    // chunk whose arrival in this window comes after its event (see
+    // arrives_later), and the window exchange makes them visible
     for (uint32_t i = tid; i < gp.nL; i += ST) {
         const uint32_t b = sh.busy[i], c = sh.infl[i];
-        if (c != NONE32 && b >= t0 && (uint64_t)b < t1)
-            __hip_atomic_fetch_or(&ly.holds[(uint64_t)sh.ldst[i] * sz.Wp + (c >> 6)], 1ull << (c & 63u),
-                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sh.foldc[i] = (c != NONE32 && b >= t0 && (uint64_t)b < t1) ? c : NONE32;
     }
     const uint32_t fl = filter_log2(gp.nU);
     // the sending filter is built once per window, from the transfers in
@@ -1203,6 +1204,10 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         const bool fl_next = sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1;
         __hip_atomic_store(&snap_wr[gp.lbase + i], fl_next ? (((uint64_t)sh.infl[i] << 32) | sh.busy[i]) : NONE64,
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t fc = sh.foldc[i];
+        if (fc != NONE32)
+            __hip_atomic_fetch_or(&ly.holds[(uint64_t)sh.ldst[i] * sz.Wp + (fc >> 6)], 1ull << (fc & 63u),
+                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (fl_next) tm = min(tm, sh.busy[i]);
         if (!resident) {
             const uint32_t sl = ly.sw.lk_slot[gp.lbase + i];
