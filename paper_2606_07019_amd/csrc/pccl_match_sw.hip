@@ -73,6 +73,10 @@ struct SwShared {
     uint32_t pend[SW_MAX_LINKS][PEND];  // needed arrivals outside [cur, hi), NONE32 = empty
     uint32_t hi[SW_MAX_LINKS];          // a link's row candidates lie in [cur, hi) (or in pend)
     uint32_t foldc[SW_MAX_LINKS];       // the chunk a link's transfer delivers inside the window, NONE32 if none
+    // where a thread's arrival-mask items start (the link, the pair of its
+    // source) and the group's item count: static, set with the group state
+    uint16_t it_link[SW_THREADS], it_q[SW_THREADS];
+    uint32_t it_tot;
     uint16_t uoff[SW_MAX_SW + 1], ulist[SW_MAX_LINKS];
     uint32_t bcap[SW_MAX_SW];
     uint16_t bpoff[SW_MAX_SW + 1], booff[SW_MAX_SW + 1];
@@ -376,6 +380,65 @@ __device__ void load_group_state(const Layout &ly, const Sizes &sz, const SwGrou
             if (x + 32 < gp.nD) sh.dord[(x >> 5) + 1] = (uint32_t)(m >> 32);
         }
     }
+    for (uint32_t i = tid; i < gp.nL; i += ST) sh.amask[i] = 0ull;
+    // the arrival-mask items: link i's are the pairs of its source; per link
+    // its first item (a block prefix, kept in `pick`, which the rounds
+    // overwrite), then per thread the link holding its first item (the last
+    // link whose first item is at or below it; the walk steps past links
+    // without pairs)
+    {
+        const uint32_t lane = tid & 63u, wave = tid >> 6;
+        const uint32_t np_me =
+            tid < gp.nL ? (uint32_t)(sh.poff[sh.lsrcj[tid] + 1] - sh.poff[sh.lsrcj[tid]]) : 0u;
+        // inclusive prefix over the wave, one lane-id bit per step: `blk`
+        // is the sum of the lane's aligned block of 2^k lanes, `inc` its
+        // prefix inside the block
+        uint32_t inc = np_me, blk = np_me;
+        {
+            uint32_t o;
+            o = swz_xor<1>(blk);
+            inc += (lane & 1u) ? o : 0u;
+            blk += o;
+            o = swz_xor<2>(blk);
+            inc += (lane & 2u) ? o : 0u;
+            blk += o;
+            o = swz_xor<4>(blk);
+            inc += (lane & 4u) ? o : 0u;
+            blk += o;
+            o = swz_xor<8>(blk);
+            inc += (lane & 8u) ? o : 0u;
+            blk += o;
+            o = swz_xor<16>(blk);
+            inc += (lane & 16u) ? o : 0u;
+            blk += o;
+            // (the lane read runs on every lane, outside the select)
+            const uint32_t lo = lane_at(blk, 0);
+            inc += (lane & 32u) ? lo : 0u;
+        }
+        if (lane == 63) sh.red[here(wave)] = inc;
+        __syncthreads();
+        uint32_t below = 0, tot = 0;
+        for (uint32_t w = 0; w < SWAVES; w++) {
+            const uint32_t r = sh.red[w];
+            if (w < wave) below += r;
+            tot += r;
+        }
+        if (tid < gp.nL) sh.pick[tid] = below + inc - np_me;
+        if (tid == 0) sh.it_tot = tot;
+        __syncthreads();
+        const uint32_t x = tid * ((tot + ST - 1) / ST);
+        uint32_t lo = 0;
+        if (x < tot) {
+            uint32_t hi2 = gp.nL;
+            while (hi2 - lo > 1) {
+                const uint32_t m = (lo + hi2) >> 1;
+                if (sh.pick[m] <= x) lo = m;
+                else hi2 = m;
+            }
+        }
+        sh.it_link[tid] = (uint16_t)lo;
+        sh.it_q[tid] = (uint16_t)(x < tot ? x - sh.pick[lo] : 0u);
+    }
 }
 
 // A unicast switch keeps one copy of a chunk in flight: is chunk c in flight
@@ -631,63 +694,17 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
     __syncthreads();
     // which arrivals each link's destination may still need: the (link,
     // pair) items of all links, spread evenly over the workgroup's threads
-    // (a block prefix over the links' pair counts, kept in `pick`, which
-    // the rounds overwrite later); each thread loads the needs words of its
-    // items AMASK_BATCH at a time, all in flight together, through the caches (a
-    // superset: picks confirm each candidate)
+    // (each thread's first item was found with the group state); each thread
+    // loads the needs words of its items AMASK_BATCH at a time, all in
+    // flight together, through the caches (a superset: picks confirm each
+    // candidate).  The masks start empty (cleared where the last window
+    // used them last).
     {
-        const uint32_t lane = tid & 63u, wave = tid >> 6;
-        const uint32_t np_me =
-            tid < gp.nL ? (uint32_t)(sh.poff[sh.lsrcj[tid] + 1] - sh.poff[sh.lsrcj[tid]]) : 0u;
-        // inclusive prefix over the wave, one lane-id bit per step: `blk`
-        // is the sum of the lane's aligned block of 2^k lanes, `inc` its
-        // prefix inside the block
-        uint32_t inc = np_me, blk = np_me;
-        {
-            uint32_t o;
-            o = swz_xor<1>(blk);
-            inc += (lane & 1u) ? o : 0u;
-            blk += o;
-            o = swz_xor<2>(blk);
-            inc += (lane & 2u) ? o : 0u;
-            blk += o;
-            o = swz_xor<4>(blk);
-            inc += (lane & 4u) ? o : 0u;
-            blk += o;
-            o = swz_xor<8>(blk);
-            inc += (lane & 8u) ? o : 0u;
-            blk += o;
-            o = swz_xor<16>(blk);
-            inc += (lane & 16u) ? o : 0u;
-            blk += o;
-            // (the lane read runs on every lane, outside the select)
-            const uint32_t lo = lane_at(blk, 0);
-            inc += (lane & 32u) ? lo : 0u;
-        }
-        if (lane == 63) sh.red[here(wave)] = inc;
-        if (tid < gp.nL) sh.amask[tid] = 0ull;
-        __syncthreads();
-        uint32_t below = 0, tot = 0;
-        for (uint32_t w = 0; w < SWAVES; w++) {
-            const uint32_t r = sh.red[w];
-            if (w < wave) below += r;
-            tot += r;
-        }
-        if (tid < gp.nL) sh.pick[tid] = below + inc - np_me;
-        __syncthreads();
-        const uint32_t per = (tot + ST - 1) / ST;
+        const uint32_t tot = sh.it_tot, per = (tot + ST - 1) / ST;
         uint32_t x = tid * per;
         const uint32_t xe = min(x + per, tot);
         if (x < xe) {
-            // the link holding item x: the last link whose first item is at
-            // or below x, then past the links without pairs
-            uint32_t lo = 0, hi2 = gp.nL;
-            while (hi2 - lo > 1) {
-                const uint32_t m = (lo + hi2) >> 1;
-                if (sh.pick[m] <= x) lo = m;
-                else hi2 = m;
-            }
-            uint32_t i = lo, q = x - sh.pick[i];
+            uint32_t i = sh.it_link[tid], q = sh.it_q[tid];
             uint32_t p0 = sh.poff[sh.lsrcj[i]], np = sh.poff[sh.lsrcj[i] + 1] - p0;
             while (x < xe) {
                 uint32_t li[AMASK_BATCH], qb[AMASK_BATCH], c[AMASK_BATCH];
@@ -1200,6 +1217,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         }
         sh.cur[i] = c;
         sh.hi[i] = h;
+        sh.amask[i] = 0ull;  // (the next window's masks start empty)
         // the next window's entry: the transfer still in flight at its start
         const bool fl_next = sh.infl[i] != NONE32 && (uint64_t)sh.busy[i] >= t1;
         __hip_atomic_store(&snap_wr[gp.lbase + i], fl_next ? (((uint64_t)sh.infl[i] << 32) | sh.busy[i]) : NONE64,
