@@ -933,7 +933,13 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     pk = min(scan ? sh.pick[i] : NONE32, bxv);
                     // a candidate delivered since its needs word was cached:
                     // the serial pick drops it and finds the next one
-                    if (pk != NONE32 && !need_bit(nd, pk)) pk = pick_link(ly, sz, sh, i, t, acc.words);
+                    if (pk != NONE32 && !need_bit(nd, pk)) {
+                        // (a local counter: the thread's statistics stay in
+                        // registers, out of the call's reach)
+                        unsigned long long pw = 0;
+                        pk = pick_link(ly, sz, sh, i, t, pw);
+                        acc.words += pw;
+                    }
                 }
                 if (i < gp.nU) sh.ucnt[i] = 0u;
                 if (i < gp.nL) sh.pick[i] = pk;
