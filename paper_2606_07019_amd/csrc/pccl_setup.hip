@@ -216,23 +216,45 @@ __global__ void k_chunk_dist(Layout ly, Sizes sz, const uint64_t *pre, const uin
     }
 }
 
+// Priority order (distance descending, then the SplitMix64 key ascending,
+// then chunk id): one stable sort of the bitwise-not of the distance (high
+// word) and the key's high word (low word), from chunk id order, then runs
+// of equal sort keys ordered by the key's low word (k_key_ties).
 __global__ void k_keys_hash(Layout ly, Sizes sz, uint64_t seed)
 {
     const uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= sz.C) return;
-    ly.skey[0][c] = splitmix64_key(seed, c);
+    const uint32_t nd = ~(uint32_t)ly.chunk_dist[c];
+    ly.skey[0][c] = ((uint64_t)nd << 32) | (splitmix64_key(seed, c) >> 32);
     ly.sval[0][c] = (uint32_t)c;
 }
 
-// After the stable sort by tie-break key: key = bitwise-not of the distance,
-// so an ascending stable sort gives distance descending, ties by key.
-__global__ void k_keys_dist(Layout ly, Sizes sz)
+// After the sort: the first thread of a run of equal sort keys (equal
+// distance and key high word; with random keys a run is rare and short)
+// orders the run by (key low word, chunk id), in place.
+__global__ void k_key_ties(Layout ly, Sizes sz, uint64_t seed)
 {
     const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= sz.C) return;
     const uint32_t cur = ly.ctl->sort_cur;
-    const uint32_t c = ly.sval[cur][i];
-    ly.skey[cur][i] = (uint64_t)(~(uint32_t)ly.chunk_dist[c]);
+    const uint64_t *k = ly.skey[cur];
+    uint32_t *v = ly.sval[cur];
+    const uint64_t ki = k[i];
+    if ((i > 0 && k[i - 1] == ki) || i + 1 >= sz.C || k[i + 1] != ki) return;
+    uint64_t j = i + 2;
+    while (j < sz.C && k[j] == ki) j++;
+    // insertion sort; the stable sort left the run in chunk id order
+    for (uint64_t a = i + 1; a < j; a++) {
+        const uint32_t c = v[a], lo = (uint32_t)splitmix64_key(seed, c);
+        uint64_t b = a;
+        while (b > i) {
+            const uint32_t p = v[b - 1], plo = (uint32_t)splitmix64_key(seed, p);
+            if (plo < lo || (plo == lo && p < c)) break;
+            v[b] = p;
+            b--;
+        }
+        v[b] = c;
+    }
 }
 
 __global__ void k_rank(Layout ly, Sizes sz)
@@ -395,11 +417,9 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
     if (sz.W) k_chunk_dist<<<gw, T, 0, st>>>(ly, sz, pre, post);
     if (C) {
         k_keys_hash<<<blocks_for(C, T), T, 0, st>>>(ly, sz, seed);
-        hipError_t e = radix_sort_pairs(ly, C, 0, 8, sz.max_tiles, true, st);
+        const hipError_t e = radix_sort_pairs(ly, C, 0, 8, sz.max_tiles, true, st);
         if (e != hipSuccess) return e;
-        k_keys_dist<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
-        e = radix_sort_pairs(ly, C, 0, 4, sz.max_tiles, false, st);
-        if (e != hipSuccess) return e;
+        k_key_ties<<<blocks_for(C, T), T, 0, st>>>(ly, sz, seed);
         k_rank<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
         k_holds<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
     }
