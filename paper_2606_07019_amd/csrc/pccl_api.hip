@@ -59,7 +59,7 @@ struct pccl_ctx {
     bool sw_active = false;        // the switch-model matching kernel runs
     std::vector<uint32_t> swt;     // switch-model tables, uploaded as one region
     std::vector<uint32_t> sw_links;  // links of each switch group
-    uint64_t swo[20] = {};         // offsets of the tables inside swt (order of SwTab)
+    uint64_t swo[21] = {};         // offsets of the tables inside swt (order of SwTab)
     bool sw_gate = false;          // only the no-multicast rule may bind: the plain kernel runs when it cannot
     uint32_t sw_nuni = 0;          // unicast switches with out-links
     bool ran_sw = false;           // the last synthesis ran the switch-group kernel
@@ -167,6 +167,7 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     sz.tmin = c->tmin;
     sz.resident = c->resident ? 1u : 0u;
     sz.sw_gate = c->sw_active && c->sw_gate ? 1u : 0u;
+    sz.sw_nbt = c->sw_active ? c->sw_nbt : 0u;
     const uint64_t hb = (uint64_t)sz.D * sz.Wp * sizeof(uint64_t);
     sz.hbytes = hb < (1ull << 31) ? (uint32_t)hb : 0u;
     const uint64_t nsort = std::max<uint64_t>(c->C, max_sends);
@@ -219,14 +220,16 @@ void carve(pccl_ctx *c, char *base, uint64_t max_sends, Layout &ly, Sizes &sz, s
     ly.sw = SwTab{};
     if (c->sw_active) {
         uint32_t *t = cv.take<uint32_t>(c->swt.size());
-        const uint32_t **p[20] = {&ly.sw.grp,    &ly.sw.blk,     &ly.sw.blk_list, &ly.sw.lk_slot, &ly.sw.lk_dl,
+        const uint32_t **p[21] = {&ly.sw.grp,    &ly.sw.blk,     &ly.sw.blk_list, &ly.sw.lk_slot, &ly.sw.lk_dl,
                                   &ly.sw.lk_srcj, &ly.sw.lk_uni,  &ly.sw.lk_dbuf,  &ly.sw.lk_sbuf, &ly.sw.d_off,
                                   &ly.sw.s_poff, &ly.sw.p_slot,  &ly.sw.u_off,    &ly.sw.u_list,  &ly.sw.b_cap,
-                                  &ly.sw.b_poff, &ly.sw.b_ooff,  &ly.sw.b_out,    &ly.sw.uc_off,  &ly.sw.uc_dst};
-        for (int i = 0; i < 20; i++) *p[i] = t ? t + c->swo[i] : nullptr;
+                                  &ly.sw.b_poff, &ly.sw.b_ooff,  &ly.sw.b_out,    &ly.sw.uc_off,  &ly.sw.uc_dst,
+                                  &ly.sw.b_abs};
+        for (int i = 0; i < 21; i++) *p[i] = t ? t + c->swo[i] : nullptr;
         ly.sw.pool_c = cv.take<uint32_t>(c->sw_pool);
         ly.sw.pool_n = cv.take<uint32_t>(c->sw_pool);
         ly.sw.occ = cv.take<uint32_t>(c->sw_nbt);
+        ly.sw.acnt = cv.take<uint32_t>((uint64_t)c->sw_nbt * std::max<uint64_t>(C, 1));
     }
     total = (cv.off + 255) & ~size_t(255);
 }
@@ -301,7 +304,7 @@ pccl_status build_switch_tables(pccl_ctx *c)
         if (cap[i] && gid_of_root[find(N + i)] != NONE32) limited[gid_of_root[find(N + i)]].push_back(N + i);
     const uint32_t G = (uint32_t)members.size();
     std::vector<uint32_t> grp(16ull * G), lk_slot, lk_dl, lk_srcj, lk_uni, lk_dbuf, lk_sbuf, d_off, s_poff, p_slot,
-        u_off, u_list, b_cap, b_poff, b_ooff, b_out;
+        u_off, u_list, b_cap, b_poff, b_ooff, b_out, b_abs;
     std::vector<uint32_t> loc(L, NONE32), sidx(D, NONE32), bidx(D, NONE32), uidx(D, NONE32);
     uint32_t pool = 0;
     for (uint32_t g = 0; g < G; g++) {
@@ -353,10 +356,20 @@ pccl_status build_switch_tables(pccl_ctx *c)
             b_cap.push_back(cap[w - N]);
             b_poff.push_back(pl);
             b_ooff.push_back(no);
+            b_abs.push_back(bobase + no);
+            b_abs.push_back(out_off[w + 1] - out_off[w]);
             pl += cap[w - N];
-            for (uint32_t k = out_off[w]; k < out_off[w + 1]; k++, no++) b_out.push_back(c->dst[out_l[k]]);
+            for (uint32_t k = out_off[w]; k < out_off[w + 1]; k++, no++) {
+                // the out-neighbour (an in-link from w makes it a group
+                // destination) and its destination index in the group
+                const uint32_t li = loc[slot_of[out_l[k]]];
+                if (li == NONE32) return fail(c, PCCL_EINTERNAL, "limited switch %u: out-link outside its group", w);
+                b_out.push_back(c->dst[out_l[k]] | (lk_dl[lbase + li] << 16));
+            }
         }
         b_cap.push_back(0);
+        b_abs.push_back(0);
+        b_abs.push_back(0);
         b_poff.push_back(pl);
         b_ooff.push_back(no);
         for (uint32_t i = 0; i < nl; i++) {
@@ -427,15 +440,15 @@ pccl_status build_switch_tables(pccl_ctx *c)
     std::vector<const std::vector<uint32_t> *> parts = {&grp,    nullptr, nullptr, &lk_slot, &lk_dl,  &lk_srcj,
                                                         &lk_uni, &lk_dbuf, &lk_sbuf, &d_off,  &s_poff, &p_slot,
                                                         &u_off,  &u_list,  &b_cap,   &b_poff, &b_ooff, &b_out,
-                                                        &uc_off, &uc_dst};
+                                                        &uc_off, &uc_dst,  &b_abs};
     uint64_t off = 0;
-    for (int i = 0; i < 20; i++) {
+    for (int i = 0; i < 21; i++) {
         c->swo[i] = off;
         off += i == 1 ? MAX_MATCH_GRID + 1ull : i == 2 ? (uint64_t)G : parts[i]->size();
         off = (off + 63) & ~63ull;
     }
     c->swt.assign(off, 0u);
-    for (int i = 0; i < 20; i++)
+    for (int i = 0; i < 21; i++)
         if (parts[i]) std::copy(parts[i]->begin(), parts[i]->end(), c->swt.begin() + c->swo[i]);
     c->sw_groups = G;
     c->sw_pool = pool;

@@ -22,6 +22,7 @@ constexpr uint32_t MAX_PAIRS = 512;       // sum over a wave's in-links of their
 // over the waves of one workgroup (each wave one part of its in-links).
 constexpr uint32_t MAX_SPLIT_LINKS = MATCH_WAVES * MAX_IN_LINKS;
 constexpr uint32_t MAX_DEVICES_SP = 8000; // shortest paths keep one 64-bit distance per device in LDS
+static_assert(MAX_DEVICES_SP <= 0xFFFF, "switch-group tables hold device ids in 16 bits");
 constexpr uint32_t MAX_MATCH_GRID = 1024; // workgroups of the matching kernel (window exchange slots)
 constexpr uint32_t MATCH_TARGET_GRID = 128; // workgroups the matching kernel aims for (measured on MI355X)
 constexpr uint32_t XSLOT_WORDS = 16;        // one 128-byte line per window exchange slot
@@ -110,11 +111,13 @@ struct SwTab {
     const uint32_t *b_cap;    // [nB + 1] per group: buffer capacity of limited switch b
     const uint32_t *b_poff;   // [nB + 1] per group: its places in the group's pool
     const uint32_t *b_ooff;   // [nB + 1] per group: its out-neighbours
-    const uint32_t *b_out;    // out-neighbour device ids
+    const uint32_t *b_out;    // out-neighbours: device id (low 16 bits), group destination index (high 16)
     const uint32_t *uc_off;   // [n_uni + 1] every unicast switch of the model: its out-neighbours in uc_dst
     const uint32_t *uc_dst;   // out-neighbour device ids
+    const uint32_t *b_abs;    // [2 nBt] per limited-switch row (group's bbase + b): first out-neighbour in b_out, count
     uint32_t *pool_c, *pool_n;  // buffer places: chunk, out-neighbours still needing it (0 = free)
     uint32_t *occ;              // [nB + 1] per group: occupied places
+    uint32_t *acnt;             // [nBt C] per limited-switch row and chunk rank: out-links whose destination still needs it
 };
 
 // Pointers into the caller's workspace (all device memory).
@@ -172,6 +175,7 @@ struct Sizes {
     uint32_t hbytes;  // bytes of the holds bitmap (D rows of Wp words) when below 2 GiB, else 0
     uint32_t resident; // every wave of the matching kernel owns one destination (or part) for the whole run
     uint32_t sw_gate;  // both matching kernels are queued; Control::sw_binds picks the one that runs
+    uint32_t sw_nbt;   // limited-switch rows of the switch tables (0: no switch model or no limited switch)
 };
 
 // ---- launchers (each defined in the translation unit that holds its kernels)

@@ -48,6 +48,8 @@ constexpr uint32_t SCAN_STEP = 4;  // row words one link's scan loads at once
 // need-word loads: the 8,192 items of a 576-link rail-switch group take
 // one batch at 768 threads
 constexpr uint32_t AMASK_BATCH = 12;
+constexpr uint32_t SW_ADM_LIST = SWAVES * 64u / 2u;  // admissions of a round whose deliveries are counted in the commits
+constexpr uint32_t SW_ADM_FILTER = 32;                // words of the round's hashed filter of admitted chunks
 constexpr uint32_t PEND = 2;       // needed chunks below a link's cursor it keeps as explicit candidates
 static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
@@ -102,8 +104,14 @@ struct SwShared {
     // destinations whose links lie in one wave in (link time, link id) order
     // (the buffer-place order is then a ballot and a bit count)
     uint32_t dord[SW_MAX_LINKS / 32];
-    // admissions of a round (their list and counts reuse wsl and uwin)
+    // admissions of a round: their number; switch and chunk of each, with
+    // the round's deliveries of that chunk to the switch's out-neighbours;
+    // a hashed filter of the admitted chunks (set and cleared by the
+    // admitting links within the round)
     uint32_t acount;
+    uint8_t adm_b[SW_ADM_LIST];
+    uint32_t adm_c[SW_ADM_LIST], adel[SW_ADM_LIST];
+    uint32_t admf[SW_ADM_FILTER];
     // next send-log slot of each destination of the group (its segment)
     unsigned long long lcur[SW_MAX_LINKS];
     uint32_t red[SWAVES];
@@ -161,6 +169,17 @@ __device__ inline bool need_bit(const uint64_t *row, uint32_t c)
 __device__ inline uint64_t link_key(const SwShared &sh, uint32_t i)
 {
     return ((uint64_t)sh.ltim[i] << 32) | sh.llink[i];
+}
+
+__device__ inline uint32_t adm_hash(uint32_t c) { return (c * 2654435761u) >> 22; }
+
+// one of the pick round's winners delivers chunk c to group destination dl
+// (read after the round's winners are final)
+__device__ inline bool delivered_now(const SwShared &sh, uint32_t dl, uint32_t c)
+{
+    for (uint32_t j = sh.doff[dl], je = sh.doff[dl + 1]; j < je; j++)
+        if (sh.pick[j] == c && ((sh.winf[j] >> 2) & 1u)) return true;
+    return false;
 }
 
 // Cross-lane steps that need no lane-index registers (index arithmetic the
@@ -749,6 +768,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             sh.hu[x] = 0u;
         }
         for (uint32_t x = tid; x < SW_MAX_LINKS / 32; x += ST) sh.dpk[x] = 0u;
+        for (uint32_t x = tid; x < SW_ADM_FILTER; x += ST) sh.admf[x] = 0u;
         if (tid < 2) sh.rflag[tid] = 0u;
         __syncthreads();
     }
@@ -769,6 +789,10 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
         const uint32_t t = block_min(sh, m);
         if (t == NONE32) break;
         for (;;) {
+            // a pick into a limited switch: how many of the switch's
+            // out-links lead to a device that needs the chunk, before this
+            // round's commits (loaded with the pick, used if it is admitted)
+            uint32_t acl = 0;
             // picks of the free links (a full buffer admits nothing), in three
             // steps inside each wave: every free link's lowest explicit
             // candidate (pending or arrived); the row scans below it, shared
@@ -942,7 +966,11 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     }
                 }
                 if (i < gp.nU) sh.ucnt[i] = 0u;
+                if (i == 0) sh.acount = 0u;
                 if (i < gp.nL) sh.pick[i] = pk;
+                if (pk != NONE32 && sh.ldbuf[i] != SW_NONE8)
+                    acl = __hip_atomic_load(&ly.sw.acnt[(uint64_t)(gp.bbase + sh.ldbuf[i]) * sz.C + pk],
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (pk != NONE32) {
                     const uint32_t dl = sh.ldl[i];
                     clash_mark(sh.hd, clash_slot(dl, pk));
@@ -994,6 +1022,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             }
             __syncthreads();
             // free places of a limited switch, in (link time, link id) order
+            uint32_t myadm = NONE32;
             {
                 const uint32_t i = tid;
                 const uint8_t wf = i < gp.nL ? sh.winf[i] : 0u;
@@ -1023,8 +1052,19 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 }
                 // (bits 0 and 1, which other links read in this stage, keep their values)
                 if (i < gp.nL) sh.winf[i] = (uint8_t)((wf & 3u) | (w << 2));
-                if (i == 0) sh.acount = 0u;
+                if (w && b != SW_NONE8) {
+                    const uint32_t pk = sh.pick[i], h = adm_hash(pk);
+                    myadm = atomicAdd(&sh.acount, 1u);
+                    if (myadm < SW_ADM_LIST) {
+                        sh.adm_b[myadm] = (uint8_t)b;
+                        sh.adm_c[myadm] = pk;
+                        sh.adel[myadm] = 0u;
+                    }
+                    atomicOr(&sh.admf[h >> 5], 1u << (h & 31u));
+                }
             }
+            // the counts are read before any commit of this round updates them
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             __syncthreads();
             // commit: the destination no longer needs the chunk, so neither
             // do the limited switches feeding it on its behalf (and the
@@ -1037,7 +1077,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
             // the next round's flags (last read right after the previous
             // round's final barrier, first set after this round's)
             if (tid == 0) sh.rflag[par ^ 1u] = 0u;
-            uint32_t mine = 0, myadm = NONE32;
+            uint32_t mine = 0;
             for (uint32_t i = tid; i < gp.nL; i += ST) {
                 const uint32_t pk = sh.pick[i];
                 if (pk == NONE32) continue;
@@ -1059,6 +1099,17 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         for (uint32_t k = 0; k < 8; k++) {
                             const uint32_t b = bj[k];
                             if (b == SW_NONE8) continue;
+                            // one out-link of b less leads to a device needing
+                            // pk (and a delivery of an admission's chunk to
+                            // its switch's out-neighbour is counted for it)
+                            __hip_atomic_fetch_sub(&ly.sw.acnt[(uint64_t)(gp.bbase + b) * sz.C + pk], 1u,
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            const uint32_t h = adm_hash(pk);
+                            if ((sh.admf[h >> 5] >> (h & 31u)) & 1u) {
+                                const uint32_t na = min(sh.acount, SW_ADM_LIST);
+                                for (uint32_t a = 0; a < na; a++)
+                                    if (sh.adm_c[a] == pk && sh.adm_b[a] == b) atomicAdd(&sh.adel[a], 1u);
+                            }
                             // the place holding pk, four places compared at a time
                             bool done = false;
                             for (uint32_t s0 = sh.bpoff[b], se = sh.bpoff[b + 1]; s0 < se && !done; s0 += 4) {
@@ -1094,74 +1145,41 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 }
                 acc.cstar = max(acc.cstar, e32);
                 const unsigned long long q = atomicAdd(&sh.lcur[dl], 1ull);
-                if (sh.ldbuf[i] != SW_NONE8) myadm = atomicAdd(&sh.acount, 1u);
                 ly.skey[0][q] = ((uint64_t)t << 32) | sh.llink[i];
                 ly.sval[0][q] = pk;
                 mine++;
             }
-            // the needs updates are done before admissions and the next
-            // round's picks read them
-            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             __syncthreads();
             // a limited switch that took a chunk buffers it while an
-            // out-neighbour still needs it.  The out-neighbours' need bits
-            // are counted by whole waves (admission k on wave k mod 16, a
-            // lane per out-neighbour, one round trip for up to 16
-            // admissions), then the admitting link takes a free place
-            const uint32_t nadm = sh.acount;
-            uint16_t *alist = reinterpret_cast<uint16_t *>(&sh.wsl[0][0]);
-            if (nadm && nadm <= SWAVES * 64u / 2u) {
-                if (myadm != NONE32) alist[myadm] = (uint16_t)tid;
-                __syncthreads();
-                const uint32_t lane = tid & 63u, wave = tid >> 6;
-                for (uint32_t k = wave; k < nadm; k += SWAVES) {
-                    const uint32_t i = alist[k], b = sh.ldbuf[i], pk = sh.pick[i];
-                    const uint32_t q0 = sh.booff[b], qe = sh.booff[b + 1];
-                    uint32_t cnt = 0;
-                    for (uint32_t q = q0; q < qe; q += 64) {
-                        const uint32_t qq = min(q + lane, qe - 1u);
-                        const uint64_t nw = __hip_atomic_load(&ly.needs[(uint64_t)sh.bout[qq] * sz.Wp + (pk >> 6)],
-                                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        cnt += (uint32_t)__popcll(__ballot(q + lane < qe && ((nw >> (pk & 63u)) & 1ull)));
-                    }
-                    if (lane == 0) sh.uwin[k] = (uint16_t)cnt;
+            // out-link leads to a device that still needs it after this
+            // round's commits: the count loaded with the pick less the
+            // round's deliveries of the chunk to the switch's out-neighbours
+            // (every one of them is a destination of this group), counted by
+            // the commits (past the listed admissions, asked here link by
+            // link); then the admitting link takes a free place
+            if (myadm != NONE32) {
+                const uint32_t i = tid, b = sh.ldbuf[i], pk = sh.pick[i], h = adm_hash(pk);
+                atomicAnd(&sh.admf[h >> 5], ~(1u << (h & 31u)));
+                uint32_t got = 0;
+                if (myadm < SW_ADM_LIST) {
+                    got = sh.adel[myadm];
+                } else {
+                    for (uint32_t q = sh.booff[b], qe = sh.booff[b + 1]; q < qe; q++)
+                        got += delivered_now(sh, sh.bout[q] >> 16, pk) ? 1u : 0u;
                 }
-                __syncthreads();
-                if (myadm != NONE32) {
-                    const uint32_t i = tid, b = sh.ldbuf[i], pk = sh.pick[i], cnt = sh.uwin[myadm];
-                    if (cnt)
-                        for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
-                            if (atomicCAS(&sh.pn[s], 0u, cnt) == 0u) {
-                                sh.pc[s] = pk;
-                                atomicAdd(&sh.occ[b], 1u);
-                                break;
-                            }
-                }
-            } else if (nadm) for (uint32_t i = tid; i < gp.nL; i += ST) {
-                const uint32_t b = sh.ldbuf[i];
-                if (!((sh.winf[i] >> 2) & 1u) || b == SW_NONE8) continue;
-                const uint32_t pk = sh.pick[i];
-                uint32_t cnt = 0;
-                for (uint32_t q0 = sh.booff[b], qe = sh.booff[b + 1]; q0 < qe; q0 += 16) {
-                    // unconditional loads (the last out-neighbour again past
-                    // the end, not counted)
-                    uint64_t nw[16];
-#pragma unroll
-                    for (uint32_t k = 0; k < 16; k++)
-                        nw[k] = __hip_atomic_load(&ly.needs[(uint64_t)sh.bout[min(q0 + k, qe - 1u)] * sz.Wp + (pk >> 6)],
-                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-                    for (uint32_t k = 0; k < 16; k++) cnt += (q0 + k < qe && ((nw[k] >> (pk & 63u)) & 1ull)) ? 1u : 0u;
-                }
-                if (!cnt) continue;
-                for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
-                    if (atomicCAS(&sh.pn[s], 0u, cnt) == 0u) {
-                        sh.pc[s] = pk;
-                        atomicAdd(&sh.occ[b], 1u);
-                        break;
-                    }
+                const uint32_t cnt = acl - got;
+                if (cnt)
+                    for (uint32_t s = sh.bpoff[b]; s < sh.bpoff[b + 1]; s++)
+                        if (atomicCAS(&sh.pn[s], 0u, cnt) == 0u) {
+                            sh.pc[s] = pk;
+                            atomicAdd(&sh.occ[b], 1u);
+                            break;
+                        }
             }
             acc.sent += mine;
+            // the commits' needs and count updates are done before the next
+            // round's picks read them
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             // another round picks something only for a link that lost a
             // clash, or one a full buffer held back when a place was freed:
             // holds do not change inside an event, needs and free places only

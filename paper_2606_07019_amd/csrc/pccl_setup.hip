@@ -216,6 +216,26 @@ __global__ void k_chunk_dist(Layout ly, Sizes sz, const uint64_t *pre, const uin
     }
 }
 
+// Switch model: for every limited-switch row and chunk rank, how many of the
+// switch's out-links lead to a device that needs the chunk once the needs
+// rows are set up (the matching kernel keeps the count as those devices
+// receive it, and reads it when the switch takes the chunk into a buffer
+// place).  One thread per (row, chunk): the 64 threads of a wave read the
+// same needs word of each out-neighbour.
+__global__ void k_adm_counts(Layout ly, Sizes sz)
+{
+    const uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t row = blockIdx.y;
+    if (c >= sz.C) return;
+    const uint32_t o0 = ly.sw.b_abs[2 * row], no = ly.sw.b_abs[2 * row + 1];
+    uint32_t n = 0;
+    for (uint32_t q = 0; q < no; q++) {
+        const uint32_t o = ly.sw.b_out[o0 + q] & 0xFFFFu;
+        n += (uint32_t)((ly.needs[(uint64_t)o * sz.Wp + (c >> 6)] >> (c & 63u)) & 1ull);
+    }
+    ly.sw.acnt[(uint64_t)row * sz.C + c] = n;
+}
+
 // Priority order (distance descending, then the SplitMix64 key ascending,
 // then chunk id): one stable sort of the bitwise-not of the distance (high
 // word) and the key's high word (low word), from chunk id order, then runs
@@ -424,6 +444,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
         k_holds<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
     }
     if (sz.W) k_needs<<<gw, T, 0, st>>>(ly, sz, pre, post);
+    if (sz.sw_nbt && C) k_adm_counts<<<dim3(blocks_for(C, T), sz.sw_nbt), T, 0, st>>>(ly, sz);
     if (sz.L) k_link_counts<<<blocks_for(sz.L, 4), 256, 0, st>>>(ly, sz);
     k_needs_count<<<sz.D, 256, 0, st>>>(ly, sz);
     k_log_offsets<<<1, 1024, 0, st>>>(ly, sz);
