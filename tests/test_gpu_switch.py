@@ -52,6 +52,26 @@ def test_broadcast_parity(n, k, buffer, unicast):
     _compare(_broadcast(n, k, buffer, unicast), "broadcast")
 
 
+def _many_admissions(buffer: int):
+    # seven limited switches with 56 in-links each feed the same four NPUs
+    # (one switch group): every uplink picks its chunk at time 0, so the
+    # first round admits 392 chunks, past the 384 admissions whose
+    # deliveries the commits count (the others count them link by link)
+    n_src, per, n_dst, n_sw = 392, 56, 4, 7
+    n = n_src + n_dst
+    pairs = [(k, n + k // per) for k in range(n_src)]
+    pairs += [(n + s, n_src + d) for s in range(n_sw) for d in range(n_dst)]
+    topo = W.with_switch_model(W.make_topology(n, n_sw, pairs, 500, 50), buffer, 0)
+    coll = W.collective_from_lists(n, n_src, 4096, list(range(n_src)), [list(range(n_src, n))] * n_src,
+                                   [range(n)])
+    return W.Workload(f"many_admissions_b{buffer}", topo, coll, 0)
+
+
+@pytest.mark.parametrize("buffer", [56, 50])
+def test_admissions_past_the_round_list(buffer):
+    _compare(_many_admissions(buffer), "admissions past the round list")
+
+
 @pytest.mark.parametrize("buffer", [1, 2])
 def test_crossing_parity(buffer):
     # buffer 1 deadlocks: both sides must report PCCL_EDEADLOCK
