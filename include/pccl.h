@@ -188,8 +188,11 @@ pccl_status pccl_set_collective(pccl_ctx *ctx, uint32_t n_chunks, uint64_t chunk
  * distinct sources of those links, 6144 in-links of those sources, a source
  * with more than 64 in-links, 64 limited or unicast switches, or more than
  * 1024 buffer places (capacities at or above the chunk count count as
- * unlimited).  Buffers can deadlock: then
- * pccl_synthesize returns PCCL_EDEADLOCK.  PCCL_EINVAL on a count mismatch.
+ * unlimited).  With limited switches the workspace also holds a 4-byte
+ * count per chunk for every limited switch plus one spare row per group
+ * (16 MiB for the 512-NPU rail cluster's eight limited switches).  Buffers
+ * can deadlock: then pccl_synthesize returns PCCL_EDEADLOCK.  PCCL_EINVAL
+ * on a count mismatch.
  */
 pccl_status pccl_set_switch_model(pccl_ctx *ctx, uint32_t n_switches, const uint32_t *buffer_chunks,
                                   const uint8_t *unicast);
