@@ -67,7 +67,7 @@ constexpr uint32_t SEG_STEPS = 3;    // lane-group probe steps before the whole 
 constexpr uint32_t LA_WORDS = 16;    // words per row of one look-ahead step
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
-constexpr uint32_t SWEEPS_LDS = 8;   // the same with the needs row in LDS (only holds words are loaded)
+constexpr uint32_t SWEEPS_LDS = 2;   // the same with the needs row in LDS (only holds words are loaded)
 constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
 constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
 constexpr uint32_t FEW_PICKS = 8;       // up to this many picking links compare picks lane to lane
@@ -260,8 +260,10 @@ __device__ __forceinline__ uint4 holds_load4(const uint64_t *holds, uint32_t byt
 // a count-trailing-zeros gives the chunk.  `words` counts the words per row the
 // scan needed (through the word holding the pick, or to the row end).
 //
-// With the needs row in LDS (MIRROR) only the holds words are loaded, and
-// twice as many sweeps are in flight per round trip.
+// With the needs row in LDS (MIRROR) only the holds words are loaded, two
+// sweeps per round trip (measured fastest of one to eight on the workloads
+// here: more sweeps in flight cost more to issue and evaluate than the round
+// trips they save).
 template <bool MIRROR>
 __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ holds, uint32_t hbytes,
                                                          const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
