@@ -68,7 +68,7 @@ constexpr uint32_t LA_WORDS = 16;    // words per row of one look-ahead step
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
 constexpr uint32_t SWEEPS_LDS = 2;   // the same with the needs row in LDS (only holds words are loaded)
-constexpr uint32_t FEW_SCANS = 2;    // up to this many full scans go straight to whole-wave scans
+constexpr uint32_t FEW_SCANS = 1;    // up to this many full scans go straight to whole-wave scans
 constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
 constexpr uint32_t FEW_PICKS = 8;       // up to this many picking links compare picks lane to lane
 constexpr uint32_t POLL_BATCH = 4;      // exchange slots one polling lane loads per batch (256 workgroups)
@@ -872,12 +872,12 @@ __device__ void process_window(const Layout &ly, const Sizes &sz, WaveShared &ws
             // bitmap part of the full scans.  First every scanning lane
             // probes PROBE_WORDS words of its own link's two rows (most scans
             // end there: the look-ahead put the cursor on the candidate);
-            // when three or more links are still scanning, the wave is split
-            // among them, G = 64 / next_pow2(k) lanes each, every lane
+            // when more than FEW_SCANS links are still scanning, the wave is
+            // split among them, G = 64 / next_pow2(k) lanes each, every lane
             // reading PROBE_WORDS words per step, and a min over each lane
             // group gives the link's first candidate.  Scans that are left
-            // (at most two, or after SEG_STEPS group steps) continue with the
-            // whole wave, one link at a time.
+            // (at most FEW_SCANS, or after SEG_STEPS group steps) continue
+            // with the whole wave, one link at a time.
             uint32_t p = NONE32, scanned = 0;
             bool scanning = false;
             uint64_t pos = 0, w0 = 0;
