@@ -54,7 +54,8 @@ constexpr uint32_t PEND = 2;       // needed chunks below a link's cursor it kee
 static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
 constexpr uint32_t SW_FILTER_WORDS = 512;  // 16,384 filter bits, shared by the group's unicast switches
-constexpr uint32_t SW_HASH_WORDS = 256;    // 4,096 two-bit slots per clash table
+constexpr uint32_t SW_HASH_WORDS = 2048;   // 32,768 two-bit slots per clash table
+static_assert(SW_HASH_WORDS * 16u == 1u << 15, "clash_slot yields 15-bit slots");
 
 static_assert(SW_MAX_LINKS <= SW_THREADS, "the pick stage gives link i to thread i");
 
@@ -505,7 +506,7 @@ __device__ inline bool sent_by(const SwShared &sh, uint32_t u, uint32_t c, uint3
 // after all inserts holds one pick only.
 __device__ inline uint32_t clash_slot(uint32_t owner, uint32_t c)
 {
-    return ((c ^ (owner * 0x9E3779B9u)) * 2654435761u) >> 20;  // 12 bits
+    return ((c ^ (owner * 0x9E3779B9u)) * 2654435761u) >> 17;  // 15 bits
 }
 
 __device__ inline void clash_mark(uint32_t *tab, uint32_t slot)
