@@ -49,7 +49,8 @@ constexpr uint32_t SCAN_STEP = 4;  // row words one link's scan loads at once
 // one batch at 768 threads
 constexpr uint32_t AMASK_BATCH = 12;
 constexpr uint32_t SW_ADM_LIST = SWAVES * 64u / 2u;  // admissions of a round whose deliveries are counted in the commits
-constexpr uint32_t SW_ADM_FILTER = 32;                // words of the round's hashed filter of admitted chunks
+constexpr uint32_t SW_ADM_FILTER = 512;               // words of the round's hashed filter of admitted chunks
+static_assert(SW_ADM_FILTER * 32u == 1u << 14, "adm_hash yields 14-bit positions");
 constexpr uint32_t PEND = 2;       // needed chunks below a link's cursor it keeps as explicit candidates
 static_assert(PEND % 2 == 0, "pending candidates fill whole 64-bit snapshot words");
 constexpr uint64_t STAG_MASK = 0xFFFull << 52;
@@ -172,7 +173,7 @@ __device__ inline uint64_t link_key(const SwShared &sh, uint32_t i)
     return ((uint64_t)sh.ltim[i] << 32) | sh.llink[i];
 }
 
-__device__ inline uint32_t adm_hash(uint32_t c) { return (c * 2654435761u) >> 22; }
+__device__ inline uint32_t adm_hash(uint32_t c) { return (c * 2654435761u) >> 18; }
 
 // one of the pick round's winners delivers chunk c to group destination dl
 // (read after the round's winners are final)
