@@ -67,7 +67,8 @@ constexpr uint32_t SEG_STEPS = 3;    // lane-group probe steps before the whole 
 constexpr uint32_t LA_WORDS = 16;    // words per row of one look-ahead step
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
-constexpr uint32_t SWEEPS_LDS = 2;   // the same with the needs row in LDS (only holds words are loaded)
+constexpr uint32_t SWEEPS_LDS = 2;   // the same with the needs row in LDS (only holds words are loaded), first round trip
+constexpr uint32_t SWEEPS_LDS_MORE = 8;  // with the needs row in LDS, every later round trip of a scan
 constexpr uint32_t FEW_SCANS = 1;    // up to this many full scans go straight to whole-wave scans
 constexpr uint32_t CLASH_SLOTS = 1024;  // hash slots of the clash detection table (10 bits)
 constexpr uint32_t FEW_PICKS = 8;       // up to this many picking links compare picks lane to lane
@@ -255,66 +256,80 @@ __device__ __forceinline__ uint4 holds_load4(const uint64_t *holds, uint32_t byt
 
 // Bitset intersect + select for one link, by a whole wave: the first set bit
 // at position >= cur of holds[src] & needs[dst], in priority order.  Each
-// lane loads 16 bytes of each row per sweep (four sweeps in flight, 8 KiB
-// per row per wave), a ballot finds the first lane with a non-zero AND, and
-// a count-trailing-zeros gives the chunk.  `words` counts the words per row the
-// scan needed (through the word holding the pick, or to the row end).
+// lane loads 16 bytes of each row per sweep (SW sweeps in flight, 1 KiB per
+// row per sweep and wave), a ballot finds the first lane with a non-zero
+// AND, and a count-trailing-zeros gives the chunk.  `words` counts the words
+// per row the scan needed (through the word holding the pick, or to the row
+// end).
 //
-// With the needs row in LDS (MIRROR) only the holds words are loaded, two
-// sweeps per round trip (measured fastest of one to eight on the workloads
-// here: more sweeps in flight cost more to issue and evaluate than the round
-// trips they save).
+// With the needs row in LDS (MIRROR) only the holds words are loaded: the
+// first round trip takes SWEEPS_LDS sweeps (most scans end there), a scan
+// that goes on SWEEPS_LDS_MORE per round trip.
+template <bool MIRROR, uint32_t SW>
+__device__ __forceinline__ bool wave_sweeps(const uint64_t *__restrict__ holds, uint32_t hbytes,
+                                            const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
+                                            uint32_t cur, uint32_t w0, uint32_t wp, uint32_t wb, uint64_t &words,
+                                            uint32_t &pick)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    uint4 a[SW];
+    if constexpr (MIRROR) {
+        // every load is issued before any is used (a load past the row end
+        // reads its last piece and is masked out)
+        uint4 hv[SW];
+        const uint32_t hrow = (uint32_t)(h - holds);
+#pragma unroll
+        for (uint32_t u = 0; u < SW; u++) {
+            const uint32_t idx = wb + 128 * u + 2 * lane;
+            hv[u] = holds_load4(holds, hbytes, hrow + min(idx, wp - 2u));
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < SW; u++) {
+            const uint32_t idx = wb + 128 * u + 2 * lane;
+            a[u] = idx < wp ? and4(hv[u], *reinterpret_cast<const uint4 *>(nd + idx)) : make_uint4(0, 0, 0, 0);
+        }
+    } else {
+#pragma unroll
+        for (uint32_t u = 0; u < SW; u++) {
+            const uint32_t idx = wb + 128 * u + 2 * lane;
+            a[u] = make_uint4(0, 0, 0, 0);
+            if (idx < wp)
+                a[u] = and4(*reinterpret_cast<const uint4 *>(h + idx), *reinterpret_cast<const uint4 *>(nd + idx));
+        }
+    }
+    // only a piece of the scan's first sweep can hold bits below the cursor
+    // (the scan starts at the even word below it)
+    a[0] = keep_from(a[0], (wb + 2 * lane) * 64, cur);
+#pragma unroll
+    for (uint32_t u = 0; u < SW; u++) {
+        const uint64_t m = __ballot(any4(a[u]));
+        if (m) {
+            const uint32_t fl = (uint32_t)__builtin_ffsll((long long)m) - 1u;
+            const uint32_t r = readlane32(first4(a[u]), fl);
+            const uint32_t idx = wb + 128 * u + 2 * fl;
+            words += (uint64_t)(idx + (r >> 6) + 1 - w0);
+            pick = idx * 64 + r;
+            return true;
+        }
+    }
+    return false;
+}
+
 template <bool MIRROR>
 __device__ __forceinline__ uint32_t wave_first_candidate(const uint64_t *__restrict__ holds, uint32_t hbytes,
                                                          const uint64_t *__restrict__ h, const uint64_t *__restrict__ nd,
                                                          uint32_t cur, uint64_t Ws, uint64_t &words)
 {
-    constexpr uint32_t SW = MIRROR ? SWEEPS_LDS : SWEEPS;
-    const uint32_t lane = threadIdx.x & 63;
+    constexpr uint32_t SW1 = MIRROR ? SWEEPS_LDS : SWEEPS, SW2 = MIRROR ? SWEEPS_LDS_MORE : SWEEPS;
     const uint32_t w0 = cur >> 6, wp = (uint32_t)Ws;
     if (w0 >= wp) return NONE32;
-    for (uint32_t wb = w0 & ~1u; wb < wp; wb += 128 * SW) {
-        uint4 a[SW];
-        if constexpr (MIRROR) {
-            // every load is issued before any is used (a load past the row
-            // end reads its last piece and is masked out)
-            uint4 hv[SW];
-            const uint32_t hrow = (uint32_t)(h - holds);
-#pragma unroll
-            for (uint32_t u = 0; u < SW; u++) {
-                const uint32_t idx = wb + 128 * u + 2 * lane;
-                hv[u] = holds_load4(holds, hbytes, hrow + min(idx, wp - 2u));
-            }
-#pragma unroll
-            for (uint32_t u = 0; u < SW; u++) {
-                const uint32_t idx = wb + 128 * u + 2 * lane;
-                a[u] = idx < wp ? and4(hv[u], *reinterpret_cast<const uint4 *>(nd + idx)) : make_uint4(0, 0, 0, 0);
-            }
-            // wb is the even word below the cursor: only the first sweep's
-            // piece in lane 0 holds bits below it
-            a[0] = keep_from(a[0], (wb + 2 * lane) * 64, cur);
-        } else {
-#pragma unroll
-            for (uint32_t u = 0; u < SW; u++) {
-                const uint32_t idx = wb + 128 * u + 2 * lane;
-                a[u] = make_uint4(0, 0, 0, 0);
-                if (idx < wp)
-                    a[u] = and4(*reinterpret_cast<const uint4 *>(h + idx), *reinterpret_cast<const uint4 *>(nd + idx));
-            }
-            a[0] = keep_from(a[0], (wb + 2 * lane) * 64, cur);
-        }
-#pragma unroll
-        for (uint32_t u = 0; u < SW; u++) {
-            const uint64_t m = __ballot(any4(a[u]));
-            if (m) {
-                const uint32_t fl = (uint32_t)__builtin_ffsll((long long)m) - 1u;
-                const uint32_t r = readlane32(first4(a[u]), fl);
-                const uint32_t idx = wb + 128 * u + 2 * fl;
-                words += (uint64_t)(idx + (r >> 6) + 1 - w0);
-                return idx * 64 + r;
-            }
-        }
-    }
+    uint32_t pick = NONE32;
+    uint32_t wb = w0 & ~1u;
+    if (wave_sweeps<MIRROR, SW1>(holds, hbytes, h, nd, cur, w0, wp, wb, words, pick)) return pick;
+    // (past the first round trip no piece lies below the cursor: keep_from
+    // passes every bit of a piece that starts above it)
+    for (wb += 128 * SW1; wb < wp; wb += 128 * SW2)
+        if (wave_sweeps<MIRROR, SW2>(holds, hbytes, h, nd, cur, w0, wp, wb, words, pick)) return pick;
     words += Ws - w0;
     return NONE32;
 }
