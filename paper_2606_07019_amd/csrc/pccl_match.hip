@@ -63,7 +63,7 @@ constexpr uint32_t M_IDLE = 0, M_FULL = 1, M_ARR = 2, M_ARR_WON = 3;
 constexpr uint32_t K_NONE = 0, K_BUSY = 1, K_IDLE = 2;
 constexpr uint32_t SPIN_LIMIT = 1u << 24;
 constexpr uint32_t PROBE_WORDS = 8;  // words per row one lane probes per step
-constexpr uint32_t SEG_STEPS = 3;    // lane-group probe steps before the whole wave helps
+constexpr uint32_t SEG_STEPS = 4;    // lane-group probe steps before the whole wave helps
 constexpr uint32_t LA_WORDS = 8;     // words per row of one look-ahead step
 constexpr uint32_t PAIRS_PER_LANE = PAIRS / 64;
 constexpr uint32_t SWEEPS = 4;       // 128-word sweeps of a whole-wave scan in flight together
