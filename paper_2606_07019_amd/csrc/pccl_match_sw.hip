@@ -847,7 +847,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                 const bool scan = free && cu < lim;
                 if (__ballot(scan)) {
                     // Steps of G = 64 / next_pow2(k) lanes for each of the k
-                    // links still scanning, two words per lane; the lanes are
+                    // links still scanning, four words per lane; the lanes are
                     // dealt again before every step, so the few links whose
                     // scan runs long get the whole wave.  A link's position,
                     // first hit (its new cursor) and first hit the source
@@ -855,7 +855,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                     // link's own lane; a min over each lane group gives the
                     // step's result, which the group's first lane hands back.
                     const uint64_t below = (1ull << lane) - 1ull;
-                    uint32_t opos = (cu >> 6) & ~1u, ofh = NONE32, orc = NONE32;
+                    uint32_t opos = (cu >> 6) & ~3u, ofh = NONE32, orc = NONE32;
                     const uint32_t owl = (uint32_t)(((uint64_t)lim + 63u) >> 6);
                     bool olive = scan;
                     for (;;) {
@@ -879,19 +879,25 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         const uint64_t wl = ((uint64_t)lj + 63u) >> 6;
                         // loads at a clamped, always valid word pair (rows
                         // have an even number of words), masked after
-                        const uint64_t w = (uint64_t)pj + 2ull * sub;
-                        const uint64_t wc = min<uint64_t>(w, sz.Wp - 2);
+                        const uint64_t w = (uint64_t)pj + 4ull * sub;
+                        const uint64_t wc = min<uint64_t>(w, sz.Wp - 4);
                         const uint4 hv = *reinterpret_cast<const uint4 *>(hrow + wc);
                         const uint4 nv = *reinterpret_cast<const uint4 *>(nrow + wc);
+                        const uint4 hv2 = *reinterpret_cast<const uint4 *>(hrow + wc + 2);
+                        const uint4 nv2 = *reinterpret_cast<const uint4 *>(nrow + wc + 2);
                         uint32_t lfh = NONE32, lrc = NONE32;
                         if (act && w < wl) {
-                            uint64_t a[2];
+                            uint64_t a[4];
                             a[0] = ((((uint64_t)hv.y << 32) | hv.x) & (((uint64_t)nv.y << 32) | nv.x)) &
                                    range_bits(w, cj, lj);
                             a[1] = ((((uint64_t)hv.w << 32) | hv.z) & (((uint64_t)nv.w << 32) | nv.z)) &
                                    range_bits(w + 1, cj, lj);
+                            a[2] = ((((uint64_t)hv2.y << 32) | hv2.x) & (((uint64_t)nv2.y << 32) | nv2.x)) &
+                                   range_bits(w + 2, cj, lj);
+                            a[3] = ((((uint64_t)hv2.w << 32) | hv2.z) & (((uint64_t)nv2.w << 32) | nv2.z)) &
+                                   range_bits(w + 3, cj, lj);
 #pragma unroll
-                            for (uint32_t k = 0; k < 2; k++) {
+                            for (uint32_t k = 0; k < 4; k++) {
                                 for (uint64_t y = lrc == NONE32 ? a[k] : 0ull; y; y &= y - 1) {
                                     const uint32_t c = (uint32_t)((w + k) * 64 + (uint64_t)__builtin_ctzll(y));
                                     if (lfh == NONE32) lfh = c;
@@ -905,7 +911,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         {
                             // word positions of the step, counted by the wave
                             const uint64_t sm = __ballot(act && w < wl);
-                            if (lane == 0 && sm) atomicAdd(&sh.st_words, 2ull * (uint64_t)__popcll(sm));
+                            if (lane == 0 && sm) atomicAdd(&sh.st_words, 4ull * (uint64_t)__popcll(sm));
                         }
                         // (G is the same on every lane of the wave)
                         if (G > 1u) {
@@ -938,7 +944,7 @@ __device__ void match_group(const Layout &ly, const Sizes &sz, const SwGroup &gp
                         const uint32_t rrc = (uint32_t)__shfl((int)lrc, (int)src);
                         if (olive) {
                             ofh = min(ofh, rfh);
-                            opos += 2u * G;
+                            opos += 4u * G;
                             if (rrc != NONE32) {
                                 orc = rrc;
                                 olive = false;
