@@ -128,7 +128,7 @@ constexpr uint32_t SP_BATCH = 8;  // links whose loads one thread issues togethe
 // the alpha-beta link times): Bellman-Ford relaxation with the distances in
 // LDS, then the parent of each device = the smallest-id in-neighbour on a
 // shortest path (the tree the pruned BFS of Sec. 4.3 keeps).
-__global__ void __launch_bounds__(256) k_shortest_paths(Layout ly, Sizes sz)
+__global__ void __launch_bounds__(512) k_shortest_paths(Layout ly, Sizes sz)
 {
     extern __shared__ unsigned long long dist[];
     __shared__ uint32_t changed;
@@ -433,7 +433,7 @@ hipError_t launch_setup(const Layout &ly, const Sizes &sz, const uint64_t *pre, 
     if (sz.W) k_conditions<<<gw, T, 0, st>>>(ly, sz, pre, post, chunk_group);
     if (C) k_chunk_check<<<blocks_for(C, T), T, 0, st>>>(ly, sz);
     k_compact_sources<<<1, 1024, 0, st>>>(ly, sz);
-    k_shortest_paths<<<sz.N, 256, sizeof(unsigned long long) * sz.D, st>>>(ly, sz);
+    k_shortest_paths<<<sz.N, 512, sizeof(unsigned long long) * sz.D, st>>>(ly, sz);
     if (sz.W) k_chunk_dist<<<gw, T, 0, st>>>(ly, sz, pre, post);
     if (C) {
         k_keys_hash<<<blocks_for(C, T), T, 0, st>>>(ly, sz, seed);
